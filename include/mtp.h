@@ -1,0 +1,194 @@
+/*
+ * mtp.h -- C ABI of the MI355X FastMTP greedy speculative-decode step.
+ *
+ * One decode step of Jina-OCR-v1 (arxiv 2609.03181) is
+ *   mtp_draft_k        K draft tokens from one shared FastMTP block applied
+ *                      recursively (Section "Draft-head architecture",
+ *                      state-shift equation);
+ *   moe_verify_step    one verifier pass over the K+1 rows [pending token,
+ *                      drafts] -- decode attention over the KV cache, top-k
+ *                      routed + shared-expert MoE FFN, final norm, LM head
+ *                      and greedy argmax (Table "Model specification");
+ *   greedy_accept      the longest equality prefix m of drafts vs verifier
+ *                      tokens and the committed tokens x_1..x_m, v_{m+1}
+ *                      (acceptance equation and the paragraph after it);
+ *   kv_commit_rollback the committed-token cache update: the K/V rows of
+ *                      the m+1 committed rows already sit at their absolute
+ *                      positions, so commit is a length update and rollback
+ *                      discards nothing but the length (no data moves).
+ * With k = 0 the same calls are plain greedy decoding.
+ *
+ * Conventions
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns
+ *     and allocates every buffer; step calls never allocate, never copy
+ *     to or from the host and never synchronise, so a whole step can be
+ *     captured into one HIP graph.  `stream` is a hipStream_t.
+ *   - Matrices are row-major [out][in].  Storage dtype (MTP_F32 or
+ *     MTP_BF16) applies to weights, embeddings, vision rows and KV caches;
+ *     norm gains and router bias are always float32; hidden states and
+ *     logits are float32.
+ *   - Each call validates its host-side scalars and pointers; a failure
+ *     returns MTP_EINVAL and enqueues nothing.  Conditions only visible on
+ *     the device (a position past max_ctx, a token id outside the
+ *     vocabulary) set a sticky status word in the workspace, read with
+ *     mtp_status_read after the caller synchronises; the affected rows are
+ *     skipped rather than written out of bounds.  A failed launch returns
+ *     MTP_EHIP.  No exception crosses the ABI.
+ *   - The workspace `ws` (size mtp_workspace_bytes) must be zero-filled
+ *     once before its first use; it holds scratch, self-resetting counters
+ *     and the status word.  Calls sharing one workspace must be ordered on
+ *     one stream.
+ */
+#ifndef MTP_H
+#define MTP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MTP_OK = 0,
+  MTP_EINVAL = -1,       /* bad host argument; nothing enqueued */
+  MTP_ECAPACITY = -2,    /* device: a position would pass max_ctx */
+  MTP_EHIP = -3,         /* a HIP call failed */
+  MTP_EUNSUPPORTED = -4, /* shape outside what the kernels support */
+  MTP_ETOKEN = -5        /* device: a token id outside [0, vocab) */
+} mtp_status;
+
+enum { MTP_F32 = 0, MTP_BF16 = 1 };
+
+/* (host) model shape and limits. */
+typedef struct {
+  int32_t n_layers, hidden, n_heads, head_dim;
+  int32_t n_routed, top_k, n_shared, moe_inter; /* MoE: E routed, top-k, S shared, width I */
+  int32_t draft_inter;                          /* draft dense FFN width F */
+  int32_t vocab, tie_lm_head, dtype;            /* dtype: MTP_F32 or MTP_BF16 */
+  int32_t max_batch, max_ctx, max_k;            /* limits of every later call */
+  double rope_theta, rms_eps;
+} mtp_config;
+
+/* (host struct of device pointers) weights; the context keeps the
+ * pointers, not copies.  Shapes with L layers, H hidden, D = heads*dim:
+ *   embed [V][H]; lm_head [V][H] (ignored when tied); final_norm [H] f32
+ *   attn_norm, ffn_norm [L][H] f32; wqkv [L][3D][H] (q rows, k rows, v
+ *   rows); wo [L][H][D]; router [L][E][H]; router_bias [L][E] f32 or NULL
+ *   exp_gu [L][E][2I][H] (gate rows then up rows); exp_down [L][E][H][I]
+ *   sh_gu [L][2SI][H] (gate rows of the S shared experts, then up rows);
+ *   sh_down [L][H][SI]
+ *   draft: d_enorm, d_hnorm, d_attn_norm, d_ffn_norm [H] f32;
+ *   d_eh_proj [H][2H] (embedding half first); d_wqkv [3D][H]; d_wo [H][D];
+ *   d_gu [2F][H] (gate rows then up rows); d_down [H][F]. */
+typedef struct {
+  const void *embed, *lm_head;
+  const float* final_norm;
+  const float *attn_norm, *ffn_norm;
+  const void *wqkv, *wo, *router;
+  const float* router_bias;
+  const void *exp_gu, *exp_down, *sh_gu, *sh_down;
+  const float *d_enorm, *d_hnorm, *d_attn_norm, *d_ffn_norm;
+  const void *d_eh_proj, *d_wqkv, *d_wo, *d_gu, *d_down;
+} mtp_weights;
+
+typedef struct mtp_ctx mtp_ctx;
+
+/* Cache layouts (storage dtype), with cap = max_ctx:
+ *   verifier KV  [L][B][2][nh][cap][dh]   (k then v)
+ *   draft KV     [B][2][nh][cap][dh]
+ * Position p of sequence b holds the K/V of the row at absolute position p. */
+
+/* Creates a context: validates the shape, uploads a float32 RoPE table
+ * [max_ctx][dh/2] (cos, sin from float64 angles) -- the only allocation the
+ * library makes.  Returns MTP_EUNSUPPORTED for shapes the kernels do not
+ * cover (hidden % 64, head_dim not 64 or 128, n_routed > 64, ...). */
+mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out /* (host) */);
+void mtp_destroy(mtp_ctx* ctx);
+
+/* Workspace bytes for steps over `batch` sequences with up to `rows`
+ * rows per sequence (a step needs rows = k+1; prefill uses chunks of at
+ * most `rows` rows). */
+size_t mtp_workspace_bytes(const mtp_ctx* ctx, int32_t batch, int32_t rows);
+
+/* Blocking read of the sticky device status word (after the caller has
+ * synchronised the stream the step ran on). */
+mtp_status mtp_status_read(const mtp_ctx* ctx, const void* ws, int32_t* status /* (host) */);
+/* Enqueues a reset of the status word to MTP_OK. */
+mtp_status mtp_status_clear(const mtp_ctx* ctx, void* ws, void* stream);
+
+/* Prefill (the step before the hot path): runs the verifier over n_rows
+ * rows per sequence at positions 0..n_rows-1 -- row i is the token
+ * tok[b][i], or when tok[b][i] < 0 the vision row vision[b][i] -- writes
+ * their K/V, takes the greedy token of the last row, and fills the draft
+ * cache in base form for rows 0..n_rows-2 (state b_p, input row p+1).
+ * Leaves the step state for the first step:
+ *   kv_len = n_rows, draft_len = n_rows-1, n_rows_out = 1,
+ *   row_pos = n_rows-1, hid[b][0] = b_{n_rows-1}, next_tok[b][0] = pending[b]
+ *   = the greedy token, out_tok[b][0] = that token, n_out = 1.
+ * k is the draft depth the following steps use: hid is [B][k+1][H] f32,
+ * next_tok [B][k+1]; tok is [B][n_rows]; vision [B][n_rows][H] (storage
+ * dtype) or NULL when every tok >= 0; out_tok [B][max_out]. */
+mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, const int32_t* tok,
+                       const void* vision, void* kv_cache, void* draft_kv, int32_t* kv_len,
+                       int32_t* draft_len, float* hid, int32_t* next_tok, int32_t* n_rows_out,
+                       int32_t* row_pos, int32_t* pending, int32_t* out_tok, int32_t max_out,
+                       int32_t* n_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Draft (state-shift equation).  Depth 1 runs the catch-up rows
+ * i = 0..n_rows[b]-1 at positions row_pos[b]+i, each with state
+ * hid[b][i] and next input next_tok[b][i]; their draft K/V are written in
+ * base form and the last row's LM-head argmax is draft_tok[b][0].  Depth
+ * d = 2..k runs one row at position row_pos[b]+n_rows[b]-1+(d-1) with the
+ * previous depth's output state and token.  Sets draft_len[b] =
+ * row_pos[b]+n_rows[b].  Requires row_pos[b] <= draft_len[b] on entry
+ * (device check).  draft_logits [B][k][V] f32 or NULL.  k = 0: no-op. */
+mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
+                       const int32_t* next_tok, const int32_t* n_rows, const int32_t* row_pos,
+                       void* draft_kv, int32_t* draft_len, int32_t* draft_tok,
+                       float* draft_logits, void* ws, size_t ws_bytes, void* stream);
+
+/* Verify: rows i = 0..k of sequence b hold pending[b] (i = 0) then
+ * draft_tok[b][i-1], at positions kv_len[b]+i.  Writes their K/V in place,
+ * runs the verifier, and returns verify_tok [B][k+1] (greedy token of each
+ * row), hid [B][k+1][H] (final-norm state b of each row), and optionally
+ * logits [B][k+1][V], margin [B][k+1] (top-1 minus top-2 logit),
+ * route_idx [L][B*(k+1)][top_k] and route_gap [L][B*(k+1)] (k-th minus
+ * (k+1)-th router logit).  kv_len is not changed. */
+mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t* pending,
+                           const int32_t* draft_tok, const int32_t* kv_len, void* kv_cache,
+                           int32_t* verify_tok, float* hid, float* logits, float* margin,
+                           int32_t* route_idx, float* route_gap, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* Acceptance equation: accept_len[b] = m, the longest r <= k with
+ * draft_tok[b][s] == verify_tok[b][s] for all s < r; commit_tok[b] =
+ * [draft_tok[b][0..m-1], verify_tok[b][m]] followed by -1 padding to k+1. */
+mtp_status greedy_accept(int32_t batch, int32_t k, const int32_t* draft_tok,
+                         const int32_t* verify_tok, int32_t* accept_len, int32_t* commit_tok,
+                         void* stream);
+
+/* Commit / rollback for each unfinished sequence (n_out[b] < limit, limit
+ * = min(max_new[b], max_out), max_new NULL = max_out):
+ *   n_rows[b] = m+1, row_pos[b] = kv_len[b], kv_len[b] += m+1,
+ *   pending[b] = commit_tok[b][m], next_tok[b][0..m] = commit_tok[b][0..m],
+ *   out_tok[b][n_out..] += the committed tokens (truncated at the limit).
+ * Finished sequences are left unchanged.  Rejected K/V rows need no
+ * action: they lie at positions >= the new kv_len. */
+mtp_status kv_commit_rollback(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t* accept_len,
+                              const int32_t* commit_tok, int32_t* kv_len, int32_t* n_rows,
+                              int32_t* row_pos, int32_t* pending, int32_t* next_tok,
+                              const int32_t* max_new, int32_t* out_tok, int32_t max_out,
+                              int32_t* n_out, void* stream);
+
+/* Benchmark harness only (forced acceptance; not part of the method):
+ * copies table[step][b][0..k-1] into draft_tok, step = *step_ctr, then
+ * increments *step_ctr (wrapping at n_steps). */
+mtp_status mtp_bench_override_drafts(int32_t batch, int32_t k, const int32_t* table,
+                                     int32_t n_steps, int32_t* step_ctr, int32_t* draft_tok,
+                                     void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MTP_H */

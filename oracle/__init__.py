@@ -248,6 +248,7 @@ class SeqState:
     draft_len: int          # draft KV positions held in base form
     out: list               # generated tokens
     max_new: int = 1 << 30
+    last_logits: np.ndarray | None = None   # logits of the last prefill row
 
     @property
     def finished(self) -> bool:
@@ -269,13 +270,14 @@ def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30) -> Se
     kv, dkv = orc.new_kv(cap), orc.new_dkv(cap)
     hm = np.zeros(P, np.uint8)
     hm[P - 1] = 1
-    r = orc.verify_rows(kv, tok, np.arange(P), emb=emb, head_mask=hm)
+    r = orc.verify_rows(kv, tok, np.arange(P), emb=emb, head_mask=hm, want_logits=True)
     pending = int(r["amax"][P - 1])
     if P >= 2:
         orc.draft_rows(dkv, tok[1:], r["b"][:P - 1], np.arange(P - 1), emb=emb[1:])
     return SeqState(kv=kv, dkv=dkv, kv_len=P, pending=pending, hid=r["b"][P - 1:P].copy(),
                     next_tok=np.array([pending], np.int32), n_rows=1, row_pos=P - 1,
-                    draft_len=P - 1, out=[pending], max_new=max_new)
+                    draft_len=P - 1, out=[pending], max_new=max_new,
+                    last_logits=r["logits"][P - 1].copy())
 
 
 def draft_chain(orc: Oracle, st: SeqState, K: int):

@@ -1,0 +1,201 @@
+// Row bookkeeping, embeddings, RMSNorm, RoPE + KV append.
+#pragma once
+#include "common.h"
+
+namespace mtp {
+
+// Row r = b*C + i of a pass over B sequences with C rows each sits at
+// position pos0[b] + off + i (pos0 NULL: off + i).  It is valid when
+// i < nvalid[b] (nvalid NULL: all) and its position is inside the cache.
+// head_row[b] (optional) receives the index of the last valid row.
+__global__ void k_rows_setup(int B, int C, const int32_t* __restrict__ pos0, int off,
+                             const int32_t* __restrict__ nvalid, int cap,
+                             int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
+                             int32_t* __restrict__ head_row, int32_t* __restrict__ status) {
+  int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= B * C) return;
+  int b = r / C, i = r - b * C;
+  int p = (pos0 ? pos0[b] : 0) + off + i;
+  int nv = nvalid ? nvalid[b] : C;
+  if (nv < 0 || nv > C) {
+    set_status(status, MTP_ECAPACITY);
+    nv = nv < 0 ? 0 : C;
+  }
+  int valid = i < nv;
+  if (valid && (p < 0 || p >= cap)) {
+    set_status(status, MTP_ECAPACITY);
+    valid = 0;
+  }
+  row_pos[r] = p;
+  row_valid[r] = valid;
+  if (head_row && i == (nv > 0 ? nv - 1 : 0)) head_row[b] = r;
+}
+
+// row_tok[b*C + i] = src[b*ld + off + i] for off + i < ld, else -1
+__global__ void k_row_tokens(int B, int C, const int32_t* __restrict__ src, int ld, int off,
+                             int32_t* __restrict__ row_tok) {
+  int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= B * C) return;
+  int b = r / C, i = r - b * C;
+  row_tok[r] = off + i < ld ? src[(size_t)b * ld + off + i] : -1;
+}
+
+// verify rows: row (b, 0) = pending[b], row (b, i>0) = draft[b][i-1]
+__global__ void k_row_tokens_verify(int B, int K, const int32_t* __restrict__ pending,
+                                    const int32_t* __restrict__ draft,
+                                    int32_t* __restrict__ row_tok) {
+  int r = blockIdx.x * blockDim.x + threadIdx.x;
+  int C = K + 1;
+  if (r >= B * C) return;
+  int b = r / C, i = r - b * C;
+  row_tok[r] = i == 0 ? pending[b] : draft[(size_t)b * K + i - 1];
+}
+
+// Loads input row r (token embedding, or a vision row when the token is
+// negative) as float32 into smem[0..H).  Vision row of (b, i):
+// vision[((size_t)b*vis_ld + vis_off + i)*H].  Invalid rows and bad tokens
+// give a zero row (bad tokens of valid rows also set MTP_ETOKEN).
+template <bool BF>
+__device__ __forceinline__ void load_input_row(int r, int C, int H, int V, int valid,
+                                               const int32_t* row_tok,
+                                               const typename St<BF>::T* embed,
+                                               const typename St<BF>::T* vision, int vis_ld,
+                                               int vis_off, float* smem, int32_t* status) {
+  using S = St<BF>;
+  int t = row_tok[r];
+  const typename S::T* src = nullptr;
+  if (!valid) {
+  } else if (t >= 0 && t < V) {
+    src = embed + (size_t)t * H;
+  } else if (t < 0 && vision) {
+    int b = r / C, i = r - b * C;
+    src = vision + ((size_t)b * vis_ld + vis_off + i) * H;
+  } else if (threadIdx.x == 0) {
+    set_status(status, MTP_ETOKEN);
+  }
+  for (int j = threadIdx.x; j < H; j += blockDim.x) smem[j] = src ? S::ld(src, j) : 0.f;
+  __syncthreads();
+}
+
+// h[r][:] = input row r (float32 residual stream)
+template <bool BF>
+__global__ void k_embed(int R, int C, int H, int V, const int32_t* __restrict__ row_valid,
+                        const int32_t* __restrict__ row_tok,
+                        const typename St<BF>::T* __restrict__ embed,
+                        const typename St<BF>::T* __restrict__ vision, int vis_ld, int vis_off,
+                        float* __restrict__ h, int32_t* __restrict__ status) {
+  extern __shared__ float sm[];
+  int r = blockIdx.x;
+  load_input_row<BF>(r, C, H, V, row_valid[r], row_tok, embed, vision, vis_ld, vis_off, sm,
+                     status);
+  for (int j = threadIdx.x; j < H; j += blockDim.x) h[(size_t)r * H + j] = sm[j];
+}
+
+// RMSNorm of x[src_row] (float32, row stride ldx) with gain g:
+//   y = x * rsqrt(mean(x^2) + eps) * g
+// written as float32 to yf[o] (optional) and at the product-input
+// precision to yin[o] (optional, row stride ldin, column offset col).
+// src_row = idx ? idx[o] : o.  One block per output row o.
+template <bool BF>
+__global__ void k_rmsnorm(int H, const float* __restrict__ x, int ldx,
+                          const int32_t* __restrict__ idx, const float* __restrict__ g, float eps,
+                          float* __restrict__ yf, int ldf, typename St<BF>::T* __restrict__ yin,
+                          int ldin, int col) {
+  __shared__ float red[16];
+  using S = St<BF>;
+  int o = blockIdx.x;
+  int r = idx ? idx[o] : o;
+  const float* xr = x + (size_t)r * ldx;
+  float ss = 0.f;
+  for (int j = threadIdx.x; j < H; j += blockDim.x) ss += xr[j] * xr[j];
+  ss = block_sum(ss, red);
+  float rinv = rsqrtf(ss / (float)H + eps);
+  for (int j = threadIdx.x; j < H; j += blockDim.x) {
+    float y = xr[j] * rinv * g[j];
+    if (yf) yf[(size_t)o * ldf + j] = y;
+    if (yin) S::st(yin, (size_t)o * ldin + col + j, y);
+  }
+}
+
+// FastMTP draft input: x[r] = [N_e(e_r); N_h(a_r)] at product-input
+// precision, e_r = input row r, a_r = state row (float32).  State row of
+// (b, i) is a[(size_t)b*a_ld + i*H].  One block per row.
+template <bool BF>
+__global__ void k_draft_in(int C, int H, int V, const int32_t* __restrict__ row_valid,
+                           const int32_t* __restrict__ row_tok,
+                           const typename St<BF>::T* __restrict__ embed,
+                           const typename St<BF>::T* __restrict__ vision, int vis_ld, int vis_off,
+                           const float* __restrict__ a, size_t a_ld,
+                           const float* __restrict__ ge, const float* __restrict__ gh, float eps,
+                           typename St<BF>::T* __restrict__ x, int32_t* __restrict__ status) {
+  extern __shared__ float sm[];
+  __shared__ float red[16];
+  using S = St<BF>;
+  int r = blockIdx.x;
+  int b = r / C, i = r - b * C;
+  const int valid = row_valid[r];
+  load_input_row<BF>(r, C, H, V, valid, row_tok, embed, vision, vis_ld, vis_off, sm, status);
+  const float* ar = a + (size_t)b * a_ld + (size_t)i * H;
+  float* sa_row = sm + H;  // state row (zero for invalid rows)
+  for (int j = threadIdx.x; j < H; j += blockDim.x) sa_row[j] = valid ? ar[j] : 0.f;
+  __syncthreads();
+  float se = 0.f, sa = 0.f;
+  for (int j = threadIdx.x; j < H; j += blockDim.x) {
+    se += sm[j] * sm[j];
+    sa += sa_row[j] * sa_row[j];
+  }
+  se = block_sum(se, red);
+  sa = block_sum(sa, red);
+  float re = rsqrtf(se / (float)H + eps), ra = rsqrtf(sa / (float)H + eps);
+  typename S::T* xr = x + (size_t)r * 2 * H;
+  for (int j = threadIdx.x; j < H; j += blockDim.x) {
+    S::st(xr, j, sm[j] * re * ge[j]);
+    S::st(xr, H + j, sa_row[j] * ra * gh[j]);
+  }
+}
+
+// RoPE (rotate-half) on q and k of every valid row, then K/V append:
+// qkv [R][3D] float32 (q, k, v blocks of D = nh*dh); q_out [R][D] float32;
+// k/v stored at cache[(b*seq_stride) + ((c*nh + h)*cap + pos)*dh + j].
+// rope[pos][i] = (cos, sin) of pos * theta^(-2i/dh), i < dh/2.
+template <bool BF>
+__global__ void k_rope_kv(int C, int nh, int dh, const float* __restrict__ qkv,
+                          const float2* __restrict__ rope, const int32_t* __restrict__ row_pos,
+                          const int32_t* __restrict__ row_valid,
+                          typename St<BF>::T* __restrict__ cache, size_t seq_stride, int cap,
+                          float* __restrict__ q_out) {
+  using S = St<BF>;
+  int r = blockIdx.x;
+  int D = nh * dh, half = dh >> 1;
+  const float* q = qkv + (size_t)r * 3 * D;
+  const float* k = q + D;
+  const float* v = k + D;
+  int valid = row_valid[r];
+  int pos = valid ? row_pos[r] : 0;
+  int b = r / C;
+  typename S::T* kc = cache + (size_t)b * seq_stride;
+  for (int t = threadIdx.x; t < nh * half; t += blockDim.x) {
+    int hh = t / half, i = t - hh * half;
+    float2 cs = rope[(size_t)pos * half + i];
+    int j0 = hh * dh + i, j1 = j0 + half;
+    float q0 = q[j0], q1 = q[j1];
+    q_out[(size_t)r * D + j0] = q0 * cs.x - q1 * cs.y;
+    q_out[(size_t)r * D + j1] = q1 * cs.x + q0 * cs.y;
+    if (valid) {
+      float k0 = k[j0], k1 = k[j1];
+      size_t kb = ((size_t)(0 * nh + hh) * cap + pos) * dh;
+      size_t vb = ((size_t)(1 * nh + hh) * cap + pos) * dh;
+      S::st(kc, kb + i, k0 * cs.x - k1 * cs.y);
+      S::st(kc, kb + i + half, k1 * cs.x + k0 * cs.y);
+      S::st(kc, vb + i, v[j0]);
+      S::st(kc, vb + i + half, v[j1]);
+    }
+  }
+}
+
+__global__ void k_fill_i32(int32_t* p, int n, int32_t v) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+}  // namespace mtp

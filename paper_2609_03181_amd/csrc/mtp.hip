@@ -1,0 +1,451 @@
+// C-ABI implementation of the MI355X FastMTP greedy speculative-decode
+// step (declarations and contracts in include/mtp.h).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "common.h"
+#include "kernels_generic.h"
+#include "kernels_rows.h"
+#include "kernels_spec.h"
+
+using namespace mtp;
+
+struct mtp_ctx {
+  mtp_config cfg;
+  mtp_weights w;
+  float2* rope;  // [max_ctx][head_dim/2] (cos, sin)
+};
+
+namespace {
+
+constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
+
+inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace carve for B sequences x C rows.
+struct Ws {
+  int32_t* status;
+  int32_t *row_pos, *row_valid, *row_tok, *head_row, *tok_stage, *chain_pos;
+  float *h, *bbuf, *qkv, *q, *rw, *rgap, *gu, *ustate, *pv, *p2, *margin_stage;
+  int32_t *ridx, *pi;
+  void *xin, *attn, *act, *xhead;
+  size_t bytes;
+};
+
+Ws carve(const mtp_config& c, int B, int C, void* base) {
+  const size_t R = (size_t)B * C;
+  const size_t es = c.dtype == MTP_BF16 ? 2 : 4;
+  const int H = c.hidden, D = c.n_heads * c.head_dim, k = c.top_k;
+  const int SI = c.n_shared * c.moe_inter;
+  const size_t nblk = (c.vocab + kLmBlk - 1) / kLmBlk;
+  size_t off = 0;
+  char* p = (char*)base;
+  auto take = [&](size_t bytes) {
+    void* r = p ? p + off : nullptr;
+    off += align_up(bytes);
+    return r;
+  };
+  Ws w;
+  w.status = (int32_t*)take(256);
+  w.row_pos = (int32_t*)take(R * 4);
+  w.row_valid = (int32_t*)take(R * 4);
+  w.row_tok = (int32_t*)take(R * 4);
+  w.head_row = (int32_t*)take((size_t)B * 4);
+  w.tok_stage = (int32_t*)take(R * 4);
+  w.chain_pos = (int32_t*)take((size_t)B * 4);
+  w.h = (float*)take(R * H * 4);
+  w.bbuf = (float*)take(R * H * 4);
+  w.qkv = (float*)take(R * 3 * D * 4);
+  w.q = (float*)take(R * D * 4);
+  w.ridx = (int32_t*)take(R * k * 4);
+  w.rw = (float*)take(R * k * 4);
+  w.rgap = (float*)take(R * 4);
+  w.gu = (float*)take(R * 2 * (size_t)c.draft_inter * 4);
+  w.ustate = (float*)take((size_t)B * H * 4);
+  w.pv = (float*)take(R * nblk * 4);
+  w.pi = (int32_t*)take(R * nblk * 4);
+  w.p2 = (float*)take(R * nblk * 4);
+  w.margin_stage = (float*)take(R * 4);
+  w.xin = take(R * 2 * H * es);
+  w.attn = take(R * D * es);
+  size_t act_cols = (size_t)(k + 1) * SI;
+  if ((size_t)c.draft_inter > act_cols) act_cols = c.draft_inter;
+  w.act = take(R * act_cols * es);
+  w.xhead = take(R * H * es);
+  w.bytes = off;
+  return w;
+}
+
+inline unsigned cdiv(size_t a, size_t b) { return (unsigned)((a + b - 1) / b); }
+
+template <bool BF>
+struct Model {
+  using T = typename St<BF>::T;
+  const mtp_config& c;
+  const mtp_weights& w;
+  const float2* rope;
+  hipStream_t s;
+
+  const T* wp(const void* p, size_t off_elems) const { return (const T*)p + off_elems; }
+
+  // one pre-norm attention sub-layer: h += Wo attn(RMSNorm(h; g))
+  void attn_sublayer(const Ws& ws, int B, int C, const float* g, const T* wqkv, const T* wo,
+                     T* cache, size_t seq_stride) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, g, (float)c.rms_eps, nullptr, 0,
+                                    (T*)ws.xin, H, 0);
+    k_linear<BF, false><<<cdiv(3 * D, 4), 256, 0, s>>>(R, 3 * D, H, (const T*)ws.xin, H, wqkv,
+                                                       ws.qkv, 3 * D);
+    k_rope_kv<BF><<<R, 256, 0, s>>>(C, nh, dh, ws.qkv, rope, ws.row_pos, ws.row_valid, cache,
+                                    seq_stride, c.max_ctx, ws.q);
+    k_attn<BF><<<dim3(nh, R), 256, 0, s>>>(C, nh, dh, ws.q, cache, seq_stride, c.max_ctx,
+                                           ws.row_pos, ws.row_valid,
+                                           1.0f / sqrtf((float)dh), (T*)ws.attn);
+    k_linear<BF, true><<<cdiv(H, 4), 256, 0, s>>>(R, H, D, (const T*)ws.attn, D, wo, ws.h, H);
+  }
+
+  // LM head + greedy argmax over nr rows of xhead; token of row o goes to
+  // tok[(o / per) * ostride + ooff + o % per].
+  void lm_head(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
+               int32_t* tok, float* margin) {
+    const int V = c.vocab, H = c.hidden;
+    const T* W = (const T*)(c.tie_lm_head ? w.embed : w.lm_head);
+    const unsigned nblk = cdiv(V, kLmBlk);
+    k_lm_partial<BF><<<nblk, 256, 0, s>>>(nr, V, H, (const T*)ws.xhead, W, logits, ldl, ws.pv,
+                                          ws.pi, ws.p2);
+    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
+                                               tok, margin);
+  }
+
+  // Verifier over B x C rows (row tokens and row setup already in ws).
+  // b states go to hid (row stride H); LM head on every row (head_all)
+  // or on ws.head_row only.
+  void verifier(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
+                float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
+                float* margin, int32_t* route_idx, float* route_gap) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter;
+    const int SI = c.n_shared * I;
+    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
+    const size_t layer_stride = (size_t)B * seq_stride;
+    k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed,
+                                                  vision, vis_ld, vis_off, ws.h, ws.status);
+    for (int l = 0; l < L; ++l) {
+      attn_sublayer(ws, B, C, w.attn_norm + (size_t)l * H, wp(w.wqkv, (size_t)l * 3 * D * H),
+                    wp(w.wo, (size_t)l * H * D), kv + (size_t)l * layer_stride, seq_stride);
+      k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.ffn_norm + (size_t)l * H,
+                                      (float)c.rms_eps, nullptr, 0, (T*)ws.xin, H, 0);
+      k_router<BF><<<cdiv(R, 4), 256, 0, s>>>(
+          R, E, k, H, (const T*)ws.xin, wp(w.router, (size_t)l * E * H),
+          w.router_bias ? w.router_bias + (size_t)l * E : nullptr, ws.ridx, ws.rw,
+          route_gap ? route_gap + (size_t)l * R : ws.rgap,
+          route_idx ? route_idx + (size_t)l * R * k : nullptr);
+      k_moe_gu<BF><<<dim3(cdiv(SI > I ? SI : I, 4), R * (k + 1)), 256, 0, s>>>(
+          R, k, H, I, SI, (const T*)ws.xin, ws.ridx, wp(w.exp_gu, (size_t)l * E * 2 * I * H),
+          wp(w.sh_gu, (size_t)l * 2 * SI * H), (T*)ws.act);
+      k_moe_down<BF><<<dim3(cdiv(H, 4), R), 256, 0, s>>>(
+          R, k, H, I, SI, (const T*)ws.act, ws.ridx, ws.rw, wp(w.exp_down, (size_t)l * E * H * I),
+          wp(w.sh_down, (size_t)l * H * SI), ws.h);
+    }
+    k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.final_norm, (float)c.rms_eps, hid, H,
+                                    nullptr, 0, 0);
+    if (!tok) return;
+    if (head_all) {
+      k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.final_norm, (float)c.rms_eps,
+                                      nullptr, 0, (T*)ws.xhead, H, 0);
+      lm_head(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
+    } else {
+      k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, (float)c.rms_eps,
+                                      nullptr, 0, (T*)ws.xhead, H, 0);
+      lm_head(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
+    }
+  }
+
+  // Draft block over B x C rows with states a (row (b, i) at
+  // a + b*a_ld + i*H) and inputs from ws.row_tok / vision.  With a head,
+  // the last valid row of each sequence gives ws.ustate[b] (its u) and its
+  // greedy token at tok[b*ostride + ooff].
+  void draft(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision, int vis_ld,
+             int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
+             size_t ldl) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    const int F = c.draft_inter;
+    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
+    k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed,
+                                                     vision, vis_ld, vis_off, a, a_ld, w.d_enorm,
+                                                     w.d_hnorm, (float)c.rms_eps, (T*)ws.xin,
+                                                     ws.status);
+    k_linear<BF, false><<<cdiv(H, 4), 256, 0, s>>>(R, H, 2 * H, (const T*)ws.xin, 2 * H,
+                                                   (const T*)w.d_eh_proj, ws.h, H);
+    attn_sublayer(ws, B, C, w.d_attn_norm, (const T*)w.d_wqkv, (const T*)w.d_wo, dkv, seq_stride);
+    k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.d_ffn_norm, (float)c.rms_eps, nullptr,
+                                    0, (T*)ws.xin, H, 0);
+    k_linear<BF, false><<<cdiv(2 * F, 4), 256, 0, s>>>(R, 2 * F, H, (const T*)ws.xin, H,
+                                                       (const T*)w.d_gu, ws.gu, 2 * F);
+    k_swiglu<BF><<<cdiv((size_t)R * F, 256), 256, 0, s>>>(R, F, ws.gu, (T*)ws.act);
+    k_linear<BF, true><<<cdiv(H, 4), 256, 0, s>>>(R, H, F, (const T*)ws.act, F,
+                                                  (const T*)w.d_down, ws.h, H);
+    if (!head) return;
+    k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, (float)c.rms_eps,
+                                    ws.ustate, H, (T*)ws.xhead, H, 0);
+    lm_head(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
+  }
+};
+
+mtp_status launch_status() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    fprintf(stderr, "mtp: HIP error %s\n", hipGetErrorString(e));
+    return MTP_EHIP;
+  }
+  return MTP_OK;
+}
+
+bool ws_ok(const mtp_ctx* ctx, int B, int C, const void* ws, size_t ws_bytes) {
+  return ws && carve(ctx->cfg, B, C, nullptr).bytes <= ws_bytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out) {
+  if (!cfg || !w || !out) return MTP_EINVAL;
+  *out = nullptr;
+  const mtp_config& c = *cfg;
+  if (c.n_layers < 1 || c.hidden < 64 || c.n_heads < 1 || c.n_routed < 1 || c.top_k < 1 ||
+      c.top_k > c.n_routed || c.n_shared < 1 || c.moe_inter < 4 || c.draft_inter < 4 ||
+      c.vocab < 2 || c.max_batch < 1 || c.max_ctx < 2 || c.max_k < 0 || c.rope_theta <= 0 ||
+      c.rms_eps < 0 || (c.dtype != MTP_F32 && c.dtype != MTP_BF16))
+    return MTP_EINVAL;
+  if (c.hidden % 64 || (c.head_dim != 64 && c.head_dim != 128) || c.n_routed > 64 ||
+      c.moe_inter % 4 || c.draft_inter % 4 || (c.n_heads * c.head_dim) % 64)
+    return MTP_EUNSUPPORTED;
+  if (!w->embed || (!c.tie_lm_head && !w->lm_head) || !w->final_norm || !w->attn_norm ||
+      !w->ffn_norm || !w->wqkv || !w->wo || !w->router || !w->exp_gu || !w->exp_down ||
+      !w->sh_gu || !w->sh_down || !w->d_enorm || !w->d_hnorm || !w->d_attn_norm ||
+      !w->d_ffn_norm || !w->d_eh_proj || !w->d_wqkv || !w->d_wo || !w->d_gu || !w->d_down)
+    return MTP_EINVAL;
+  mtp_ctx* ctx = new (std::nothrow) mtp_ctx;
+  if (!ctx) return MTP_EINVAL;
+  ctx->cfg = c;
+  ctx->w = *w;
+  ctx->rope = nullptr;
+  const int half = c.head_dim / 2;
+  const size_t n = (size_t)c.max_ctx * half;
+  float2* host = new (std::nothrow) float2[n];
+  if (!host) {
+    delete ctx;
+    return MTP_EINVAL;
+  }
+  for (int p = 0; p < c.max_ctx; ++p)
+    for (int i = 0; i < half; ++i) {
+      double inv = std::pow(c.rope_theta, -2.0 * i / c.head_dim);
+      double ang = (double)p * inv;
+      host[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+    }
+  if (hipMalloc(&ctx->rope, n * sizeof(float2)) != hipSuccess ||
+      hipMemcpy(ctx->rope, host, n * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
+    delete[] host;
+    if (ctx->rope) (void)hipFree(ctx->rope);
+    delete ctx;
+    return MTP_EHIP;
+  }
+  delete[] host;
+  *out = ctx;
+  return MTP_OK;
+}
+
+void mtp_destroy(mtp_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->rope) (void)hipFree(ctx->rope);
+  delete ctx;
+}
+
+size_t mtp_workspace_bytes(const mtp_ctx* ctx, int32_t batch, int32_t rows) {
+  if (!ctx || batch < 1 || rows < 1) return 0;
+  return carve(ctx->cfg, batch, rows, nullptr).bytes;
+}
+
+mtp_status mtp_status_read(const mtp_ctx* ctx, const void* ws, int32_t* status) {
+  if (!ctx || !ws || !status) return MTP_EINVAL;
+  if (hipMemcpy(status, ws, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess) return MTP_EHIP;
+  return MTP_OK;
+}
+
+mtp_status mtp_status_clear(const mtp_ctx* ctx, void* ws, void* stream) {
+  if (!ctx || !ws) return MTP_EINVAL;
+  k_fill_i32<<<1, 64, 0, (hipStream_t)stream>>>((int32_t*)ws, 1, 0);
+  return launch_status();
+}
+
+mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, const int32_t* tok,
+                       const void* vision, void* kv_cache, void* draft_kv, int32_t* kv_len,
+                       int32_t* draft_len, float* hid, int32_t* next_tok, int32_t* n_rows_out,
+                       int32_t* row_pos, int32_t* pending, int32_t* out_tok, int32_t max_out,
+                       int32_t* n_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!ctx) return MTP_EINVAL;
+  const mtp_config& c = ctx->cfg;
+  if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k || n_rows < 1 ||
+      n_rows > c.max_ctx || !tok || !kv_cache || !draft_kv || !kv_len || !draft_len || !hid ||
+      !next_tok || !n_rows_out || !row_pos || !pending || !n_out || max_out < 0 ||
+      (max_out > 0 && !out_tok) || !ws)
+    return MTP_EINVAL;
+  // largest chunk whose workspace fits
+  int C = 0;
+  for (int t = n_rows; t >= 1; t = t > 64 ? t / 2 : t - 1)
+    if (carve(c, batch, t, nullptr).bytes <= ws_bytes) {
+      C = t;
+      break;
+    }
+  if (C < 1) return MTP_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  auto run = [&](auto tag) -> mtp_status {
+    constexpr bool BF = decltype(tag)::value;
+    using T = typename St<BF>::T;
+    Model<BF> m{c, ctx->w, ctx->rope, s};
+    Ws w = carve(c, batch, C, ws);
+    for (int c0 = 0; c0 < n_rows; c0 += C) {
+      const int Cc = n_rows - c0 < C ? n_rows - c0 : C;
+      const int R = batch * Cc;
+      const bool last = c0 + Cc == n_rows;
+      k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, nullptr, c0, nullptr, c.max_ctx,
+                                                 w.row_pos, w.row_valid, w.head_row, w.status);
+      k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, tok, n_rows, c0, w.row_tok);
+      m.verifier(w, batch, Cc, (const T*)vision, n_rows, c0, (T*)kv_cache, w.bbuf, false,
+                 last ? w.tok_stage : nullptr, 1, 1, nullptr, nullptr, nullptr, nullptr);
+      if (last)
+        k_copy_rows<<<batch, 256, 0, s>>>(batch, c.hidden, w.head_row, w.bbuf, hid,
+                                          (size_t)(k + 1) * c.hidden);
+      // draft prefill: rows p = c0..c0+Cc-1 with p <= n_rows-2, input row p+1
+      const int nv = (n_rows - 1 - c0) < Cc ? (n_rows - 1 - c0) : Cc;
+      if (nv > 0) {
+        k_fill_i32<<<cdiv(batch, 256), 256, 0, s>>>(w.chain_pos, batch, nv);
+        k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, nullptr, c0, w.chain_pos, c.max_ctx,
+                                                   w.row_pos, w.row_valid, nullptr, w.status);
+        k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, tok, n_rows, c0 + 1, w.row_tok);
+        m.draft(w, batch, Cc, w.bbuf, (size_t)Cc * c.hidden, (const T*)vision, n_rows, c0 + 1,
+                (T*)draft_kv, false, nullptr, 0, 0, nullptr, 0);
+      }
+    }
+    k_prefill_state<<<cdiv(batch, 256), 256, 0, s>>>(batch, k, n_rows, w.tok_stage, kv_len,
+                                                     draft_len, next_tok, n_rows_out, row_pos,
+                                                     pending, out_tok, max_out, n_out);
+    return launch_status();
+  };
+  if (c.dtype == MTP_BF16) return run(std::true_type{});
+  return run(std::false_type{});
+}
+
+mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
+                       const int32_t* next_tok, const int32_t* n_rows, const int32_t* row_pos,
+                       void* draft_kv, int32_t* draft_len, int32_t* draft_tok,
+                       float* draft_logits, void* ws, size_t ws_bytes, void* stream) {
+  if (!ctx) return MTP_EINVAL;
+  const mtp_config& c = ctx->cfg;
+  if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k) return MTP_EINVAL;
+  if (k == 0) return MTP_OK;
+  if (!hid || !next_tok || !n_rows || !row_pos || !draft_kv || !draft_len || !draft_tok ||
+      !ws_ok(ctx, batch, k + 1, ws, ws_bytes))
+    return MTP_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  auto run = [&](auto tag) -> mtp_status {
+    constexpr bool BF = decltype(tag)::value;
+    using T = typename St<BF>::T;
+    Model<BF> m{c, ctx->w, ctx->rope, s};
+    const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
+    Ws w = carve(c, batch, C, ws);
+    k_draft_len<<<cdiv(batch, 256), 256, 0, s>>>(batch, n_rows, row_pos, draft_len, w.status);
+    // depth 1 over the catch-up rows; the last valid row starts the chain
+    k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, 0, n_rows, c.max_ctx, w.row_pos,
+                                               w.row_valid, w.head_row, w.status);
+    k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, C, next_tok, C, 0, w.row_tok);
+    m.draft(w, batch, C, hid, (size_t)C * H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k, 0,
+            draft_logits, (size_t)k * V);
+    // depth d = 2..k: one row at (row_pos + n_rows - 1) + (d - 1), state u
+    // of depth d-1, input the depth d-1 draft token
+    k_chain_pos<<<cdiv(batch, 256), 256, 0, s>>>(batch, row_pos, n_rows, w.chain_pos);
+    for (int d = 2; d <= k; ++d) {
+      k_rows_setup<<<cdiv(batch, 256), 256, 0, s>>>(batch, 1, w.chain_pos, d - 1, nullptr,
+                                                     c.max_ctx, w.row_pos, w.row_valid,
+                                                     w.head_row, w.status);
+      k_row_tokens<<<cdiv(batch, 256), 256, 0, s>>>(batch, 1, draft_tok, k, d - 2, w.row_tok);
+      k_copy_rows<<<batch, 256, 0, s>>>(batch, H, nullptr, w.ustate, w.bbuf, (size_t)H);
+      m.draft(w, batch, 1, w.bbuf, (size_t)H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k,
+              d - 1, draft_logits ? draft_logits + (size_t)(d - 1) * V : nullptr, (size_t)k * V);
+    }
+    return launch_status();
+  };
+  if (c.dtype == MTP_BF16) return run(std::true_type{});
+  return run(std::false_type{});
+}
+
+mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t* pending,
+                           const int32_t* draft_tok, const int32_t* kv_len, void* kv_cache,
+                           int32_t* verify_tok, float* hid, float* logits, float* margin,
+                           int32_t* route_idx, float* route_gap, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (!ctx) return MTP_EINVAL;
+  const mtp_config& c = ctx->cfg;
+  if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k || !pending ||
+      (k > 0 && !draft_tok) || !kv_len || !kv_cache || !verify_tok || !hid ||
+      !ws_ok(ctx, batch, k + 1, ws, ws_bytes))
+    return MTP_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  auto run = [&](auto tag) -> mtp_status {
+    constexpr bool BF = decltype(tag)::value;
+    using T = typename St<BF>::T;
+    Model<BF> m{c, ctx->w, ctx->rope, s};
+    const int C = k + 1, R = batch * C;
+    Ws w = carve(c, batch, C, ws);
+    k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, kv_len, 0, nullptr, c.max_ctx, w.row_pos,
+                                               w.row_valid, nullptr, w.status);
+    k_row_tokens_verify<<<cdiv(R, 256), 256, 0, s>>>(batch, k, pending, draft_tok, w.row_tok);
+    m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
+               margin, route_idx, route_gap);
+    return launch_status();
+  };
+  if (c.dtype == MTP_BF16) return run(std::true_type{});
+  return run(std::false_type{});
+}
+
+mtp_status greedy_accept(int32_t batch, int32_t k, const int32_t* draft_tok,
+                         const int32_t* verify_tok, int32_t* accept_len, int32_t* commit_tok,
+                         void* stream) {
+  if (batch < 1 || k < 0 || (k > 0 && !draft_tok) || !verify_tok || !accept_len || !commit_tok)
+    return MTP_EINVAL;
+  k_accept<<<cdiv(batch, 256), 256, 0, (hipStream_t)stream>>>(batch, k, draft_tok, verify_tok,
+                                                               accept_len, commit_tok);
+  return launch_status();
+}
+
+mtp_status kv_commit_rollback(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t* accept_len,
+                              const int32_t* commit_tok, int32_t* kv_len, int32_t* n_rows,
+                              int32_t* row_pos, int32_t* pending, int32_t* next_tok,
+                              const int32_t* max_new, int32_t* out_tok, int32_t max_out,
+                              int32_t* n_out, void* stream) {
+  if (!ctx) return MTP_EINVAL;
+  const mtp_config& c = ctx->cfg;
+  if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k || !accept_len || !commit_tok ||
+      !kv_len || !n_rows || !row_pos || !pending || !next_tok || max_out < 0 ||
+      (max_out > 0 && !out_tok) || !n_out)
+    return MTP_EINVAL;
+  k_commit<<<cdiv(batch, 256), 256, 0, (hipStream_t)stream>>>(
+      batch, k, accept_len, commit_tok, kv_len, n_rows, row_pos, pending, next_tok, max_new,
+      out_tok, max_out, n_out);
+  return launch_status();
+}
+
+mtp_status mtp_bench_override_drafts(int32_t batch, int32_t k, const int32_t* table,
+                                     int32_t n_steps, int32_t* step_ctr, int32_t* draft_tok,
+                                     void* stream) {
+  if (batch < 1 || k < 1 || !table || n_steps < 1 || !step_ctr || !draft_tok) return MTP_EINVAL;
+  k_override<<<1, 256, 0, (hipStream_t)stream>>>(batch, k, table, n_steps, step_ctr, draft_tok);
+  return launch_status();
+}
+
+}  // extern "C"
