@@ -63,7 +63,7 @@ def load():
         "mtp_workspace_bytes": ([P, I32, I32], SZ),
         "mtp_status_read": ([P, P, P], I32),
         "mtp_status_clear": ([P, P, P], I32),
-        "mtp_prefill": ([P, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, P, SZ, P],
+        "mtp_prefill": ([P, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, P, SZ, P],
                         I32),
         "mtp_draft_k": ([P, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "moe_verify_step": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),

@@ -47,3 +47,30 @@ def test_host_validation_without_gpu():
     assert lib.moe_verify_step(None, 1, 3, *([None] * 11), 0, None) == _lib.MTP_EINVAL
     assert lib.mtp_draft_k(None, 1, 3, *([None] * 9), 0, None) == _lib.MTP_EINVAL
     assert lib.mtp_workspace_bytes(None, 1, 4) == 0
+
+
+def _param_types(name):
+    src = open(os.path.join(ROOT, "include", "mtp.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    m = re.search(r"\b" + name + r"\s*\(([^)]*)\)\s*;", src)
+    params = [p.strip() for p in m.group(1).split(",")]
+    out = []
+    for p in params:
+        if "*" in p:
+            out.append("ptr")
+        elif p.startswith("size_t"):
+            out.append("size")
+        elif p.startswith("int32_t"):
+            out.append("i32")
+        else:
+            raise AssertionError(p)
+    return out
+
+
+def test_ctypes_signatures_match_header():
+    lib = _lib.load()
+    kind = {ctypes.c_void_p: "ptr", ctypes.c_int32: "i32", ctypes.c_size_t: "size"}
+    for name in _lib.EXPORTS:
+        want = _param_types(name)
+        got = [kind[t] for t in getattr(lib, name).argtypes]
+        assert got == want, name

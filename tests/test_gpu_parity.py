@@ -160,15 +160,16 @@ def test_forced_acceptance_reaches_every_m_and_is_lossless():
             base += m + 1
     sp = gpu_prefill(model, B, K, tok, vis, N, record=False)
     sp.set_forced_drafts(torch.from_numpy(table))
-    got_m = []
+    seen = []
     for s_ in range(n_steps):
         if finished(sp):
             break
+        active = (sp.n_out < N).cpu().numpy()       # finished sequences are frozen
         sp.step()
-        got_m.append(sp.accept_len.cpu().numpy().copy())
-    got_m = np.array(got_m)
-    assert np.array_equal(got_m, m_star[:len(got_m)])
-    assert set(np.unique(got_m).tolist()) == set(range(K + 1))
+        got = sp.accept_len.cpu().numpy()
+        assert np.array_equal(got[active], m_star[s_][active]), s_
+        seen += got[active].tolist()
+    assert set(seen) == set(range(K + 1))
     outs = sp.outputs()
     for b in range(B):
         assert outs[b] == traj[b][:N]
@@ -209,9 +210,10 @@ def test_commit_rollback_bookkeeping_and_max_new_clamp():
     t = dict(kv=T(kv_len), nr=T(np.ones(B, np.int32)), rp=T(kv_len - 1),
              pend=T(np.zeros(B, np.int32)), nt=T(np.zeros((B, K + 1), np.int32)),
              out=T(np.full((B, max_out), -7, np.int32)), no=T(n_out))
-    _lib.kv_commit_rollback(model.ctx, B, K, T(m).data_ptr(), T(commit).data_ptr(),
+    m_d, commit_d, max_new_d = T(m), T(commit), T(max_new)     # keep alive across the launch
+    _lib.kv_commit_rollback(model.ctx, B, K, m_d.data_ptr(), commit_d.data_ptr(),
                             t["kv"].data_ptr(), t["nr"].data_ptr(), t["rp"].data_ptr(),
-                            t["pend"].data_ptr(), t["nt"].data_ptr(), T(max_new).data_ptr(),
+                            t["pend"].data_ptr(), t["nt"].data_ptr(), max_new_d.data_ptr(),
                             t["out"].data_ptr(), max_out, t["no"].data_ptr(),
                             torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
