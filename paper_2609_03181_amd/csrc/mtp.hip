@@ -10,14 +10,26 @@
 #include "common.h"
 #include "kernels_generic.h"
 #include "kernels_rows.h"
+#include "kernels_mfma.h"
 #include "kernels_spec.h"
 
 using namespace mtp;
+
+// Matrices of a bf16 model repacked into MFMA operand tiles (see
+// kernels_mfma.h); strides are in uint4 units.
+struct Packed {
+  uint4* base;
+  const uint4 *wqkv, *wo, *router, *exp_gu, *exp_down, *sh_gu, *sh_down, *lm;
+  const uint4 *d_eh, *d_qkv, *d_wo, *d_gu, *d_down;
+  size_t wqkv_s, wo_s, router_s, exp_gu_s, exp_down_s, sh_gu_s, sh_down_s;
+};
 
 struct mtp_ctx {
   mtp_config cfg;
   mtp_weights w;
   float2* rope;  // [max_ctx][head_dim/2] (cos, sin)
+  Packed pk;     // bf16 models only
+  int n_split;   // attention key splits of ATT_SPL positions
 };
 
 namespace {
@@ -29,16 +41,22 @@ inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 // Workspace carve for B sequences x C rows.
 struct Ws {
   int32_t* status;
+  int32_t* counter;  // self-resetting grid counter (router grouping)
   int32_t *row_pos, *row_valid, *row_tok, *head_row, *tok_stage, *chain_pos;
   float *h, *bbuf, *qkv, *q, *rw, *rgap, *gu, *ustate, *pv, *p2, *margin_stage;
   int32_t *ridx, *pi;
   void *xin, *attn, *act, *xhead;
+  // bf16 fast path
+  float *part, *slot, *ent_w;
+  int32_t *cnt, *off, *ent_row, *ent_slot;
+  uint16_t* act_sh;
   size_t bytes;
 };
 
-Ws carve(const mtp_config& c, int B, int C, void* base) {
+Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
   const size_t R = (size_t)B * C;
   const size_t es = c.dtype == MTP_BF16 ? 2 : 4;
+  if (n_split < 1) n_split = 1;
   const int H = c.hidden, D = c.n_heads * c.head_dim, k = c.top_k;
   const int SI = c.n_shared * c.moe_inter;
   const size_t nblk = (c.vocab + kLmBlk - 1) / kLmBlk;
@@ -50,7 +68,8 @@ Ws carve(const mtp_config& c, int B, int C, void* base) {
     return r;
   };
   Ws w;
-  w.status = (int32_t*)take(256);
+  w.status = (int32_t*)take(128);
+  w.counter = (int32_t*)take(128);
   w.row_pos = (int32_t*)take(R * 4);
   w.row_valid = (int32_t*)take(R * 4);
   w.row_tok = (int32_t*)take(R * 4);
@@ -74,8 +93,24 @@ Ws carve(const mtp_config& c, int B, int C, void* base) {
   w.attn = take(R * D * es);
   size_t act_cols = (size_t)(k + 1) * SI;
   if ((size_t)c.draft_inter > act_cols) act_cols = c.draft_inter;
+  if (c.dtype == MTP_BF16) act_cols = (size_t)k * c.moe_inter;  // routed entries only
   w.act = take(R * act_cols * es);
   w.xhead = take(R * H * es);
+  if (c.dtype == MTP_BF16) {
+    w.part = (float*)take(R * c.n_heads * (size_t)n_split * (c.head_dim + 2) * 4);
+    w.slot = (float*)take(R * (k + 1) * (size_t)H * 4);
+    w.ent_w = (float*)take(R * k * 4);
+    w.cnt = (int32_t*)take((size_t)c.n_routed * 4);
+    w.off = (int32_t*)take((size_t)c.n_routed * 4);
+    w.ent_row = (int32_t*)take(R * k * 4);
+    w.ent_slot = (int32_t*)take(R * k * 4);
+    const size_t shw = (size_t)(SI > c.draft_inter ? SI : c.draft_inter);
+    w.act_sh = (uint16_t*)take(R * shw * 2);
+  } else {
+    w.part = w.slot = w.ent_w = nullptr;
+    w.cnt = w.off = w.ent_row = w.ent_slot = nullptr;
+    w.act_sh = nullptr;
+  }
   w.bytes = off;
   return w;
 }
@@ -89,6 +124,8 @@ struct Model {
   const mtp_weights& w;
   const float2* rope;
   hipStream_t s;
+  const Packed& pk;
+  int n_split;
 
   const T* wp(const void* p, size_t off_elems) const { return (const T*)p + off_elems; }
 
@@ -127,6 +164,11 @@ struct Model {
   void verifier(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
                 float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
                 float* margin, int32_t* route_idx, float* route_gap) {
+    if constexpr (BF) {
+      verifier_fast(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
+                    logits, margin, route_idx, route_gap);
+      return;
+    }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
     const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter;
     const int SI = c.n_shared * I;
@@ -172,6 +214,11 @@ struct Model {
   void draft(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision, int vis_ld,
              int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
              size_t ldl) {
+    if constexpr (BF) {
+      draft_fast(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
+                 logits, ldl);
+      return;
+    }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
     const int F = c.draft_inter;
     const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
@@ -194,7 +241,144 @@ struct Model {
                                     ws.ustate, H, (T*)ws.xhead, H, 0);
     lm_head(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
   }
+  // ------------------------------------------------------------ bf16 fast path
+  template <int RT>
+  void mm(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
+          bool add) {
+    dim3 grid(cdiv(cdiv(N, 16), 4), cdiv(R, 16 * RT));
+    if (add)
+      k_mm<RT, true><<<grid, 256, 0, s>>>(R, N, K / 32, X, ldx_, Wp, Y, ldy);
+    else
+      k_mm<RT, false><<<grid, 256, 0, s>>>(R, N, K / 32, X, ldx_, Wp, Y, ldy);
+  }
+  void mmr(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
+           bool add) {
+    if (R <= 16) mm<1>(R, N, K, X, ldx_, Wp, Y, ldy, add);
+    else mm<4>(R, N, K, X, ldx_, Wp, Y, ldy, add);
+  }
+
+  // attention sub-layer on the fast path: xin (normed, bf16 [R][H]) ->
+  // q + K/V append -> split attention -> merge -> h += Wo o
+  void attn_fast(const Ws& ws, int B, int C, const uint4* wqkv, const uint4* wo, uint16_t* cache,
+                 size_t seq_stride) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    const unsigned tasks = D / 8;  // D/16 rope pairs + D/16 v strips
+    if (R <= 16)
+      k_qkv_rope<1><<<dim3(cdiv(tasks, 4), 1), 256, 0, s>>>(
+          R, C, nh, dh, H / 32, (const uint16_t*)ws.xin, wqkv, rope, ws.row_pos, ws.row_valid,
+          cache, seq_stride, c.max_ctx, ws.q);
+    else
+      k_qkv_rope<4><<<dim3(cdiv(tasks, 4), cdiv(R, 64)), 256, 0, s>>>(
+          R, C, nh, dh, H / 32, (const uint16_t*)ws.xin, wqkv, rope, ws.row_pos, ws.row_valid,
+          cache, seq_stride, c.max_ctx, ws.q);
+    const int ng = (C + ATT_ROWS - 1) / ATT_ROWS;
+    dim3 ag(n_split, nh, B * ng);
+    const float scale = 1.0f / sqrtf((float)dh);
+    if (dh == 128)
+      k_attn_split<128><<<ag, 256, 0, s>>>(C, nh, n_split, ws.q, cache, seq_stride, c.max_ctx,
+                                           ws.row_pos, ws.row_valid, scale, ws.part);
+    else
+      k_attn_split<64><<<ag, 256, 0, s>>>(C, nh, n_split, ws.q, cache, seq_stride, c.max_ctx,
+                                          ws.row_pos, ws.row_valid, scale, ws.part);
+    k_attn_merge<<<R, 256, 0, s>>>(nh, dh, n_split, ws.part, ws.row_valid, (uint16_t*)ws.attn);
+    mmr(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
+  }
+
+  void lm_fast(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
+               int32_t* tok, float* margin) {
+    const int V = c.vocab, H = c.hidden;
+    const unsigned nblk = cdiv(cdiv(V, 16), 4);
+    if (nr <= 16)
+      k_lm_mfma<1><<<dim3(nblk, 1), 256, 0, s>>>(nr, V, H / 32, (const uint16_t*)ws.xhead, pk.lm,
+                                                logits, ldl, ws.pv, ws.pi, ws.p2);
+    else
+      k_lm_mfma<4><<<dim3(nblk, cdiv(nr, 64)), 256, 0, s>>>(nr, V, H / 32,
+                                                            (const uint16_t*)ws.xhead, pk.lm,
+                                                            logits, ldl, ws.pv, ws.pi, ws.p2);
+    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
+                                               tok, margin);
+  }
+
+  void verifier_fast(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
+                     float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
+                     float* margin, int32_t* route_idx, float* route_gap) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
+    const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter;
+    const int SI = c.n_shared * I;
+    const float eps = (float)c.rms_eps;
+    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
+    const size_t layer_stride = (size_t)B * seq_stride;
+    k_embed_norm<<<R, 256, H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok,
+                                                   (const uint16_t*)w.embed,
+                                                   (const uint16_t*)vision, vis_ld, vis_off,
+                                                   w.attn_norm, eps, ws.h, (uint16_t*)ws.xin,
+                                                   ws.status);
+    const unsigned gu_tiles = cdiv((SI > I ? SI : I) / 16, 4);
+    const unsigned chunks = cdiv(R, 64);
+    for (int l = 0; l < L; ++l) {
+      if (l > 0)
+        k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.attn_norm + (size_t)l * H, eps,
+                                         nullptr, (uint16_t*)ws.xin);
+      attn_fast(ws, B, C, pk.wqkv + l * pk.wqkv_s, pk.wo + l * pk.wo_s,
+                (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
+      k_combine_norm<<<R, 256, 0, s>>>(H, k, nullptr, ws.h, w.ffn_norm + (size_t)l * H, eps,
+                                       nullptr, (uint16_t*)ws.xin);
+      k_router<<<cdiv(R, 16), 256, 0, s>>>(
+          R, E, k, H / 32, (const uint16_t*)ws.xin, pk.router + l * pk.router_s,
+          w.router_bias ? w.router_bias + (size_t)l * E : nullptr, ws.ridx, ws.rw,
+          route_gap ? route_gap + (size_t)l * R : ws.rgap,
+          route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.counter, ws.cnt, ws.off,
+          ws.ent_row, ws.ent_slot, ws.ent_w);
+      k_moe_gu<<<dim3(gu_tiles, E + 1, chunks), 256, 0, s>>>(
+          R, E, I, SI, H / 32, (const uint16_t*)ws.xin, pk.exp_gu + (size_t)l * E * pk.exp_gu_s,
+          pk.exp_gu_s, pk.sh_gu + l * pk.sh_gu_s, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act,
+          ws.act_sh);
+      k_moe_down<<<dim3(cdiv(H / 16, 4), E + 1, chunks), 256, 0, s>>>(
+          R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh,
+          pk.exp_down + (size_t)l * E * pk.exp_down_s, pk.exp_down_s, pk.sh_down + l * pk.sh_down_s,
+          ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot);
+    }
+    k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.final_norm, eps, hid,
+                                     head_all ? (uint16_t*)ws.xhead : nullptr);
+    if (!tok) return;
+    if (head_all) {
+      lm_fast(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
+    } else {
+      k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, nullptr, 0,
+                                      (T*)ws.xhead, H, 0);
+      lm_fast(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
+    }
+  }
+
+  void draft_fast(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
+                  int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
+                  float* logits, size_t ldl) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    const int F = c.draft_inter;
+    const float eps = (float)c.rms_eps;
+    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
+    k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok,
+                                                         (const T*)w.embed, vision, vis_ld,
+                                                         vis_off, a, a_ld, w.d_enorm, w.d_hnorm,
+                                                         eps, (T*)ws.xin, ws.status);
+    mmr(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
+    k_combine_norm<<<R, 256, 0, s>>>(H, 0, nullptr, ws.h, w.d_attn_norm, eps, nullptr,
+                                     (uint16_t*)ws.xin);
+    attn_fast(ws, B, C, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
+    k_combine_norm<<<R, 256, 0, s>>>(H, 0, nullptr, ws.h, w.d_ffn_norm, eps, nullptr,
+                                     (uint16_t*)ws.xin);
+    k_moe_gu<<<dim3(cdiv(F / 16, 4), 1, cdiv(R, 64)), 256, 0, s>>>(
+        R, 0, F, F, H / 32, (const uint16_t*)ws.xin, nullptr, 0, pk.d_gu, nullptr, nullptr,
+        nullptr, nullptr, ws.act_sh);
+    mmr(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
+    (void)D;
+    if (!head) return;
+    k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
+                                    (T*)ws.xhead, H, 0);
+    lm_fast(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
+  }
 };
+
 
 mtp_status launch_status() {
   hipError_t e = hipGetLastError();
@@ -206,7 +390,60 @@ mtp_status launch_status() {
 }
 
 bool ws_ok(const mtp_ctx* ctx, int B, int C, const void* ws, size_t ws_bytes) {
-  return ws && carve(ctx->cfg, B, C, nullptr).bytes <= ws_bytes;
+  return ws && carve(ctx->cfg, B, C, nullptr, ctx->n_split).bytes <= ws_bytes;
+}
+
+// Repacks every matrix of a bf16 model into MFMA operand tiles (one
+// allocation, owned by the context).
+mtp_status pack_weights(mtp_ctx* ctx) {
+  const mtp_config& c = ctx->cfg;
+  const mtp_weights& w = ctx->w;
+  const int L = c.n_layers, H = c.hidden, D = c.n_heads * c.head_dim, E = c.n_routed;
+  const int I = c.moe_inter, SI = c.n_shared * I, F = c.draft_inter, V = c.vocab;
+  Packed& p = ctx->pk;
+  p.wqkv_s = packed_elems(3 * D, H);
+  p.wo_s = packed_elems(H, D);
+  p.router_s = packed_elems(E, H);
+  p.exp_gu_s = packed_elems(2 * I, H);
+  p.exp_down_s = packed_elems(H, I);
+  p.sh_gu_s = packed_elems(2 * SI, H);
+  p.sh_down_s = packed_elems(H, SI);
+  const size_t lm_s = packed_elems(V, H);
+  const size_t eh_s = packed_elems(H, 2 * H), dq_s = packed_elems(3 * D, H);
+  const size_t dwo_s = packed_elems(H, D), dgu_s = packed_elems(2 * F, H);
+  const size_t ddn_s = packed_elems(H, F);
+  const size_t total = L * (p.wqkv_s + p.wo_s + p.router_s + E * (p.exp_gu_s + p.exp_down_s) +
+                            p.sh_gu_s + p.sh_down_s) +
+                       lm_s + eh_s + dq_s + dwo_s + dgu_s + ddn_s;
+  if (hipMalloc(&p.base, total * sizeof(uint4)) != hipSuccess) {
+    p.base = nullptr;
+    return MTP_EHIP;
+  }
+  uint4* cur = p.base;
+  auto pack = [&](const void* src, size_t src_stride, int count, int N, int K,
+                  const uint4** dst) {
+    *dst = cur;
+    const size_t n = packed_elems(N, K);
+    for (int i = 0; i < count; ++i) {
+      k_pack<<<cdiv(n, 256), 256>>>((const uint16_t*)src + (size_t)i * src_stride, N, K, cur);
+      cur += n;
+    }
+  };
+  pack(w.wqkv, (size_t)3 * D * H, L, 3 * D, H, &p.wqkv);
+  pack(w.wo, (size_t)H * D, L, H, D, &p.wo);
+  pack(w.router, (size_t)E * H, L, E, H, &p.router);
+  pack(w.exp_gu, (size_t)2 * I * H, L * E, 2 * I, H, &p.exp_gu);
+  pack(w.exp_down, (size_t)H * I, L * E, H, I, &p.exp_down);
+  pack(w.sh_gu, (size_t)2 * SI * H, L, 2 * SI, H, &p.sh_gu);
+  pack(w.sh_down, (size_t)H * SI, L, H, SI, &p.sh_down);
+  pack(c.tie_lm_head ? w.embed : w.lm_head, 0, 1, V, H, &p.lm);
+  pack(w.d_eh_proj, 0, 1, H, 2 * H, &p.d_eh);
+  pack(w.d_wqkv, 0, 1, 3 * D, H, &p.d_qkv);
+  pack(w.d_wo, 0, 1, H, D, &p.d_wo);
+  pack(w.d_gu, 0, 1, 2 * F, H, &p.d_gu);
+  pack(w.d_down, 0, 1, H, F, &p.d_down);
+  if (hipGetLastError() != hipSuccess || hipDeviceSynchronize() != hipSuccess) return MTP_EHIP;
+  return MTP_OK;
 }
 
 }  // namespace
@@ -225,6 +462,10 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   if (c.hidden % 64 || (c.head_dim != 64 && c.head_dim != 128) || c.n_routed > 64 ||
       c.moe_inter % 4 || c.draft_inter % 4 || (c.n_heads * c.head_dim) % 64)
     return MTP_EUNSUPPORTED;
+  // bf16 MFMA path: every contraction length a multiple of 128
+  if (c.dtype == MTP_BF16 && (c.hidden % 128 || (c.n_heads * c.head_dim) % 128 ||
+                              c.moe_inter % 128 || c.draft_inter % 128))
+    return MTP_EUNSUPPORTED;
   if (!w->embed || (!c.tie_lm_head && !w->lm_head) || !w->final_norm || !w->attn_norm ||
       !w->ffn_norm || !w->wqkv || !w->wo || !w->router || !w->exp_gu || !w->exp_down ||
       !w->sh_gu || !w->sh_down || !w->d_enorm || !w->d_hnorm || !w->d_attn_norm ||
@@ -235,6 +476,8 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   ctx->cfg = c;
   ctx->w = *w;
   ctx->rope = nullptr;
+  ctx->pk = Packed{};
+  ctx->n_split = (c.max_ctx + ATT_SPL - 1) / ATT_SPL;
   const int half = c.head_dim / 2;
   const size_t n = (size_t)c.max_ctx * half;
   float2* host = new (std::nothrow) float2[n];
@@ -256,6 +499,13 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
     return MTP_EHIP;
   }
   delete[] host;
+  if (c.dtype == MTP_BF16) {
+    mtp_status st = pack_weights(ctx);
+    if (st != MTP_OK) {
+      mtp_destroy(ctx);
+      return st;
+    }
+  }
   *out = ctx;
   return MTP_OK;
 }
@@ -263,12 +513,13 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
 void mtp_destroy(mtp_ctx* ctx) {
   if (!ctx) return;
   if (ctx->rope) (void)hipFree(ctx->rope);
+  if (ctx->pk.base) (void)hipFree(ctx->pk.base);
   delete ctx;
 }
 
 size_t mtp_workspace_bytes(const mtp_ctx* ctx, int32_t batch, int32_t rows) {
   if (!ctx || batch < 1 || rows < 1) return 0;
-  return carve(ctx->cfg, batch, rows, nullptr).bytes;
+  return carve(ctx->cfg, batch, rows, nullptr, ctx->n_split).bytes;
 }
 
 mtp_status mtp_status_read(const mtp_ctx* ctx, const void* ws, int32_t* status) {
@@ -298,7 +549,7 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
   // largest chunk whose workspace fits
   int C = 0;
   for (int t = n_rows; t >= 1; t = t > 64 ? t / 2 : t - 1)
-    if (carve(c, batch, t, nullptr).bytes <= ws_bytes) {
+    if (carve(c, batch, t, nullptr, ctx->n_split).bytes <= ws_bytes) {
       C = t;
       break;
     }
@@ -307,8 +558,8 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s};
-    Ws w = carve(c, batch, C, ws);
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split};
+    Ws w = carve(c, batch, C, ws, ctx->n_split);
     for (int c0 = 0; c0 < n_rows; c0 += C) {
       const int Cc = n_rows - c0 < C ? n_rows - c0 : C;
       const int R = batch * Cc;
@@ -356,9 +607,9 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
-    Ws w = carve(c, batch, C, ws);
+    Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_draft_len<<<cdiv(batch, 256), 256, 0, s>>>(batch, n_rows, row_pos, draft_len, w.status);
     // depth 1 over the catch-up rows; the last valid row starts the chain
     k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, 0, n_rows, c.max_ctx, w.row_pos,
@@ -399,9 +650,9 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split};
     const int C = k + 1, R = batch * C;
-    Ws w = carve(c, batch, C, ws);
+    Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, kv_len, 0, nullptr, c.max_ctx, w.row_pos,
                                                w.row_valid, nullptr, w.status);
     k_row_tokens_verify<<<cdiv(R, 256), 256, 0, s>>>(batch, k, pending, draft_tok, w.row_tok);
