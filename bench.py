@@ -295,29 +295,28 @@ def _load_synthetic(s, cfg, ctx):
 
 def _forced_table(s, cfg, B, K, n_steps):
     """Forced acceptance for timing: m* ~ {0:0.2, 1:0.2, 2:0.25, 3:0.35}
-    (seed 13).  The greedy trajectory of every sequence comes from a K=0
-    run on a copy of the state; at each step drafts 1..m* are the next
-    trajectory tokens and draft m*+1 is a wrong one, so exactly m* are
-    accepted."""
+    (seed 13).  The greedy trajectory of every sequence comes from a
+    natural K-draft run on a copy of the state (lossless, and computed with
+    the same kernels and row count as the timed steps); at each step drafts
+    1..m* are the next trajectory tokens and draft m*+1 is a wrong one, so
+    exactly m* are accepted."""
     import torch
     from paper_2609_03181_amd.session import Session
-    # greedy trajectory of each sequence (K=0 steps on a copy of the state)
-    need = n_steps * (K + 1) + K + 2
-    ar = Session(s.m, B, 0, need, prefill_rows=1)
-    for name in ("kv", "dkv", "kv_len", "row_pos", "draft_len", "n_rows", "pending"):
-        getattr(ar, name).copy_(getattr(s, name))
-    ar.hid[:, 0] = s.hid[:, 0]
-    ar.next_tok[:, 0] = s.next_tok[:, 0]
-    ar.n_out.fill_(0)
-    ar.max_new.fill_(need)
-    while bool((ar.n_out < need).any()):
-        ar.step()
-    traj = ar.out_tok.cpu().numpy()
-    del ar
     import synth
+    need = n_steps * (K + 1) + K + 2
+    tr = Session(s.m, B, K, need, prefill_rows=1)
+    for name in ("kv", "dkv", "kv_len", "row_pos", "draft_len", "n_rows", "pending", "hid",
+                 "next_tok"):
+        getattr(tr, name).copy_(getattr(s, name))
+    tr.n_out.fill_(0)
+    tr.max_new.fill_(need)
+    while bool((tr.n_out < need).any()):
+        tr.step()
+    traj = tr.out_tok.cpu().numpy()
+    del tr
+    torch.cuda.synchronize()
     u = synth.uniform_f64(13, 80, n_steps * B).reshape(n_steps, B)
-    m_star = np.searchsorted(np.cumsum([0.2, 0.2, 0.25, 0.35]), u)
-    m_star = np.minimum(m_star, K)
+    m_star = np.minimum(np.searchsorted(np.cumsum([0.2, 0.2, 0.25, 0.35]), u), K)
     table = np.zeros((n_steps, B, K), np.int32)
     for b in range(B):
         base = 0

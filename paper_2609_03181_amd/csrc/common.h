@@ -40,12 +40,40 @@ struct St<false> {
 };
 
 // ---------------------------------------------------------------- reductions
+// Wave64 reductions with DPP moves (row_shr 1/2/4/8 inside each 16-lane
+// row, then row_bcast15 / row_bcast31 across rows; lane 63 ends with the
+// total, which readlane broadcasts).  Lanes whose DPP source is outside the
+// row keep the identity passed as `old`.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f(float identity, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(identity), __float_as_int(v),
+                                                    CTRL, ROW_MASK, 0xf, false));
+}
 __device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<0x111, 0xf>(0.f, v);  // row_shr:1
+  v += dpp_f<0x112, 0xf>(0.f, v);  // row_shr:2
+  v += dpp_f<0x114, 0xf>(0.f, v);  // row_shr:4
+  v += dpp_f<0x118, 0xf>(0.f, v);  // row_shr:8
+  v += dpp_f<0x142, 0xa>(0.f, v);  // row_bcast:15
+  v += dpp_f<0x143, 0xc>(0.f, v);  // row_bcast:31
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp_f<0x111, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x112, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x114, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x118, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x142, 0xa>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x143, 0xc>(-INFINITY, v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+// reference reductions through LDS permutes (for checks)
+__device__ __forceinline__ float wave_sum_shfl(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, MTP_WAVE);
   return v;
 }
-__device__ __forceinline__ float wave_max(float v) {
+__device__ __forceinline__ float wave_max_shfl(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, MTP_WAVE));
   return v;

@@ -214,177 +214,61 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int R, int C, int nh, int dh, 
   }
 }
 
-// ---------------------------------------------------------------- attention
-// Split-K decode attention.  Block (split s, head h, z = b*ngroups + g)
-// handles keys [s*SPL, (s+1)*SPL) of sequence b for its rows i in
-// [g*AR, g*AR+AR) (AR <= 8 query rows share every K/V load).  Row r
-// attends keys 0..row_pos[r].  Writes per (row, head, split) the running
-// max m, the sum l and the unnormalised o[dh] (float32).
-constexpr int ATT_ROWS = 8;
-constexpr int ATT_SPL = 256;
-
-template <int DH>
-__global__ void __launch_bounds__(256) k_attn_split(int C, int nh, int n_split,
-                                                    const float* __restrict__ q,
-                                                    const uint16_t* __restrict__ cache,
-                                                    size_t seq_stride, int cap,
-                                                    const int32_t* __restrict__ row_pos,
-                                                    const int32_t* __restrict__ row_valid,
-                                                    float scale, float* __restrict__ part) {
-  constexpr int NW = 4, DPL = DH / 64;  // dims per lane in P.V
-  __shared__ float qs[ATT_ROWS][DH];
-  __shared__ float ps[NW][ATT_ROWS][64];
-  __shared__ float wm[NW][ATT_ROWS], wl[NW][ATT_ROWS];
-  __shared__ float wo[NW][ATT_ROWS][DH];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int s = blockIdx.x, h = blockIdx.y;
-  const int ngroups = (C + ATT_ROWS - 1) / ATT_ROWS;
-  const int b = blockIdx.z / ngroups, g = blockIdx.z % ngroups;
-  const int i0 = g * ATT_ROWS, nr = min(ATT_ROWS, C - i0);
-  const int D = nh * DH;
-  // rows of this group and their limits
-  int lim[ATT_ROWS];
-  int maxpos = -1;
+// ---------------------------------------------------------------- top-k helper
+// Router decision for one row, one lane per expert (E <= 64): lv = the
+// float32 logit (lanes >= E ignored).  Every lane reads all E logits from
+// LDS (broadcast reads, no cross-lane chains) and derives its rank --
+// #{j : l_j > l_e or (l_j == l_e and j < e)}, i.e. larger logit first, equal
+// logits to the lower id -- and its float32 softmax probability.  Lanes of
+// rank < topk write ridx/rw[rank]; gap = l_(k) - l_(k+1) (0 when k == E).
+// sc is 68 floats of wave-private, 16-byte aligned LDS.
+__device__ __forceinline__ void lane_topk(float lv, int E, int topk, float* sc, int32_t* ridx,
+                                          float* rw, float* gap, int32_t* ridx_out, int* sel,
+                                          float* selw) {
+  const int lane = threadIdx.x & 63;
+  sc[lane] = lane < E ? lv : -INFINITY;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_s_waitcnt(0);
+  float mx = -INFINITY;
+  int rank = 0;
 #pragma unroll
-  for (int i = 0; i < ATT_ROWS; ++i) {
-    int r = b * C + i0 + i;
-    lim[i] = (i < nr && row_valid[r]) ? row_pos[r] : -1;
-    maxpos = max(maxpos, lim[i]);
-  }
-  for (int e = threadIdx.x; e < ATT_ROWS * DH; e += 256) {
-    int i = e / DH, d = e % DH;
-    qs[i][d] = i < nr ? q[(size_t)(b * C + i0 + i) * D + h * DH + d] : 0.f;
-  }
-  __syncthreads();
-  const int k0 = s * ATT_SPL;
-  const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
-  const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
-  float m[ATT_ROWS], l[ATT_ROWS], o[ATT_ROWS][DPL];
+  for (int j4 = 0; j4 < 16; ++j4) {
+    const float4 v = *(const float4*)(sc + 4 * j4);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-  for (int i = 0; i < ATT_ROWS; ++i) {
-    m[i] = -INFINITY;
-    l[i] = 0.f;
-#pragma unroll
-    for (int d = 0; d < DPL; ++d) o[i][d] = 0.f;
-  }
-  // each wave: 64 consecutive keys per pass
-  for (int kb = k0 + wv * 64; kb < k0 + ATT_SPL && kb <= maxpos; kb += NW * 64) {
-    const int j = kb + lane;
-    float sc[ATT_ROWS];
-#pragma unroll
-    for (int i = 0; i < ATT_ROWS; ++i) sc[i] = 0.f;
-    if (j <= maxpos) {
-      const uint4* kr = (const uint4*)(Kc + (size_t)j * DH);
-#pragma unroll
-      for (int c = 0; c < DH / 8; ++c) {
-        uint4 v = kr[c];
-        float kf[8] = {__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
-                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u),
-                       __uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
-                       __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u)};
-#pragma unroll
-        for (int i = 0; i < ATT_ROWS; ++i) {
-          if (i < nr) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) sc[i] += qs[i][c * 8 + e] * kf[e];
-          }
-        }
+    for (int q = 0; q < 4; ++q) {
+      const int j = 4 * j4 + q;
+      if (j < E) {
+        mx = fmaxf(mx, vv[q]);
+        rank += (vv[q] > lv) || (vv[q] == lv && j < lane);
       }
     }
-#pragma unroll
-    for (int i = 0; i < ATT_ROWS; ++i) {
-      float si = (j <= lim[i]) ? sc[i] * scale : -INFINITY;
-      float mx = wave_max(si);
-      float mn = fmaxf(m[i], mx);
-      float p = (mn == -INFINITY) ? 0.f : __expf(si - mn);
-      float corr = (mn == -INFINITY) ? 1.f : __expf(m[i] - mn);
-      l[i] = l[i] * corr + wave_sum(p);
-#pragma unroll
-      for (int d = 0; d < DPL; ++d) o[i][d] *= corr;
-      m[i] = mn;
-      ps[wv][i][lane] = p;
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    const int nk = min(64, maxpos - kb + 1);
-    for (int jj = 0; jj < nk; ++jj) {
-      const uint16_t* vr = Vc + (size_t)(kb + jj) * DH + lane * DPL;
-      float vf[DPL];
-      if (DPL == 2) {
-        uint32_t u = *(const uint32_t*)vr;
-        vf[0] = __uint_as_float(u << 16);
-        vf[DPL - 1] = __uint_as_float(u & 0xffff0000u);
-      } else {
-        vf[0] = bf2f(vr[0]);
-      }
-#pragma unroll
-      for (int i = 0; i < ATT_ROWS; ++i) {
-        float p = ps[wv][i][jj];
-#pragma unroll
-        for (int d = 0; d < DPL; ++d) o[i][d] += p * vf[d];
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
   }
-  // combine the 4 waves of the block
+  float se = 0.f;
 #pragma unroll
-  for (int i = 0; i < ATT_ROWS; ++i) {
-    if (lane == 0) {
-      wm[wv][i] = m[i];
-      wl[wv][i] = l[i];
-    }
+  for (int j4 = 0; j4 < 16; ++j4) {
+    const float4 v = *(const float4*)(sc + 4 * j4);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int d = 0; d < DPL; ++d) wo[wv][i][lane * DPL + d] = o[i][d];
+    for (int q = 0; q < 4; ++q)
+      if (4 * j4 + q < E) se += __expf(vv[q] - mx);
   }
-  __syncthreads();
-  for (int e = threadIdx.x; e < nr * DH; e += 256) {
-    const int i = e / DH, d = e % DH;
-    float M = -INFINITY;
-    for (int x = 0; x < NW; ++x) M = fmaxf(M, wm[x][i]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-      for (int x = 0; x < NW; ++x) {
-        float f = wm[x][i] == -INFINITY ? 0.f : __expf(wm[x][i] - M);
-        L += wl[x][i] * f;
-        O += wo[x][i][d] * f;
-      }
-    }
-    const int r = b * C + i0 + i;
-    float* pp = part + (((size_t)r * nh + h) * n_split + s) * (DH + 2);
-    pp[d] = O;
-    if (d == 0) {
-      pp[DH] = M;
-      pp[DH + 1] = L;
+  const float p = __expf(lv - mx) / se;
+  __builtin_amdgcn_wave_barrier();
+  if (lane < E && rank < topk) {
+    ridx[rank] = lane;
+    rw[rank] = p;
+    if (ridx_out) ridx_out[rank] = lane;
+    if (sel) {
+      sel[rank] = lane;
+      selw[rank] = p;
     }
   }
-}
-
-// merge of the splits: out[r][h*dh + d] = bf16(sum_s o_s e^{m_s-M} / L)
-__global__ void __launch_bounds__(256) k_attn_merge(int nh, int dh, int n_split,
-                                                    const float* __restrict__ part,
-                                                    const int32_t* __restrict__ row_valid,
-                                                    uint16_t* __restrict__ out) {
-  const int r = blockIdx.x;
-  const int D = nh * dh;
-  for (int e = threadIdx.x; e < D; e += blockDim.x) {
-    const int h = e / dh, d = e % dh;
-    float val = 0.f;
-    if (row_valid[r]) {
-      const float* pp = part + ((size_t)r * nh + h) * n_split * (dh + 2);
-      float M = -INFINITY;
-      for (int s = 0; s < n_split; ++s) M = fmaxf(M, pp[s * (dh + 2) + dh]);
-      float L = 0.f, O = 0.f;
-      for (int s = 0; s < n_split; ++s) {
-        const float ms = pp[s * (dh + 2) + dh];
-        if (ms == -INFINITY) continue;
-        const float f = __expf(ms - M);
-        L += pp[s * (dh + 2) + dh + 1] * f;
-        O += pp[s * (dh + 2) + d] * f;
-      }
-      val = L > 0.f ? O / L : 0.f;
-    }
-    out[(size_t)r * D + e] = f2bf(val);
-  }
+  if (lane < E && rank == topk - 1) sc[64] = lv;
+  if (lane < E && rank == topk) sc[65] = lv;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_s_waitcnt(0);
+  if (lane == 0 && gap) *gap = topk < E ? sc[64] - sc[65] : 0.f;
 }
 
 // ---------------------------------------------------------------- router + grouping
@@ -421,6 +305,7 @@ __global__ void __launch_bounds__(256) k_router(int R, int E, int topk, int nkt,
   }
   __syncthreads();
   // one wave per 4 rows: lane = expert
+  __shared__ __align__(16) float tsc[4][68];
   for (int rr = wv; rr < 16; rr += 4) {
     const int r = r0 + rr;
     if (r >= R) break;
@@ -429,37 +314,9 @@ __global__ void __launch_bounds__(256) k_router(int R, int E, int topk, int nkt,
       lv = lg[rr][lane];
       if (bias) lv += bias[lane];
     }
-    const float mx = wave_max(lv);
-    const float ex = lane < E ? __expf(lv - mx) : 0.f;
-    const float p = ex / wave_sum(ex);
-    bool taken = lane >= E;
-    float kth = 0.f;
-    for (int j = 0; j <= topk && j < E; ++j) {
-      float v = taken ? -INFINITY : lv;
-      int id = taken ? (1 << 30) : lane;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        float ov = __shfl_xor(v, o, MTP_WAVE);
-        int oi = __shfl_xor(id, o, MTP_WAVE);
-        if (ov > v || (ov == v && oi < id)) {
-          v = ov;
-          id = oi;
-        }
-      }
-      if (j == topk) {
-        if (lane == 0 && rgap) rgap[r] = kth - v;
-        break;
-      }
-      const float pid = __shfl(p, id, MTP_WAVE);
-      if (lane == id) taken = true;
-      if (lane == 0) {
-        ridx[(size_t)r * topk + j] = id;
-        rw[(size_t)r * topk + j] = pid;
-        if (ridx_out) ridx_out[(size_t)r * topk + j] = id;
-      }
-      kth = v;
-    }
-    if (topk >= E && lane == 0 && rgap) rgap[r] = 0.f;
+    lane_topk(lv, E, topk, tsc[wv], ridx + (size_t)r * topk, rw + (size_t)r * topk,
+              rgap ? rgap + r : nullptr, ridx_out ? ridx_out + (size_t)r * topk : nullptr,
+              nullptr, nullptr);
   }
   // last block: group by expert
   __threadfence();

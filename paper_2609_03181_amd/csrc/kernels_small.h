@@ -1,0 +1,772 @@
+// Small-batch kernels (R <= 16 rows in a pass: batch x (K+1) <= 16).
+// At this size every contraction is a weight stream, so the kernels aim at
+// memory-level parallelism and few launches:
+//   - a 16-feature strip is split along K over NW waves of one block; each
+//     wave issues all of its tile loads before its MFMAs and the partial
+//     accumulators are summed in LDS in wave order (deterministic);
+//   - RMSNorm is a prologue that recomputes the (few) normalised rows into
+//     LDS, which then feeds the MFMA B operand;
+//   - the MoE down projection is n-tile-major: one block owns 16 output
+//     features, its waves take the touched experts round-robin, and the
+//     block adds the sum straight into the residual stream.
+#pragma once
+#include "common.h"
+#include "kernels_mfma.h"
+
+namespace mtp {
+
+constexpr int SR_MAX = 16;  // rows of the small-batch path
+constexpr int XPAD = 8;     // LDS row padding (bf16 elements)
+
+// acc += tiles [t0, t1) of a packed strip against this lane's B row
+// (global or LDS).  Batches of 8 tiles, double-buffered: the loads of the
+// next batch are in flight while the current one is multiplied.
+__device__ __forceinline__ void sk_load8(const uint4* __restrict__ A, int t, int t1,
+                                         const uint16_t* xrow, int koff, uint4 (&a)[8],
+                                         uint4 (&b)[8]) {
+  const int lane = threadIdx.x & 63;
+  const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    if (t + u < t1) {
+      a[u] = A[(size_t)(t + u) * 64 + lane];
+      b[u] = xrow ? ldx(xrow + (t + u) * 32 + koff) : z;
+    }
+  }
+}
+
+__device__ __forceinline__ f32x4_t sk_range(const uint4* __restrict__ A, int t0, int t1,
+                                            const uint16_t* xrow, f32x4_t acc) {
+  const int koff = 8 * ((threadIdx.x & 63) >> 4);
+  const uint4 z = make_uint4(0, 0, 0, 0);
+  uint4 a[8], b[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) a[u] = b[u] = z;  // every staged register defined
+  if (t0 < t1) sk_load8(A, t0, t1, xrow, koff, a, b);
+  for (int t = t0; t < t1; t += 8) {
+    uint4 an[8], bn[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) an[u] = bn[u] = z;
+    if (t + 8 < t1) sk_load8(A, t + 8, t1, xrow, koff, an, bn);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (t + u < t1) acc = mfma16(a[u], b[u], acc);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      a[u] = an[u];
+      b[u] = bn[u];
+    }
+  }
+  return acc;
+}
+
+// up to MAXT tiles of a strip, loaded into registers ahead of their use
+template <int MAXT>
+__device__ __forceinline__ void preload(const uint4* __restrict__ A, int t0, int n,
+                                        uint4 (&a)[MAXT]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int u = 0; u < MAXT; ++u)
+    a[u] = u < n ? A[(size_t)(t0 + u) * 64 + lane] : make_uint4(0, 0, 0, 0);
+}
+
+template <int MAXT>
+__device__ __forceinline__ f32x4_t mma_pre(const uint4 (&a)[MAXT], int t0, int n,
+                                           const uint16_t* xrow, f32x4_t acc) {
+  const int koff = 8 * ((threadIdx.x & 63) >> 4);
+  const uint4 z = make_uint4(0, 0, 0, 0);
+  uint4 b[MAXT];
+#pragma unroll
+  for (int u = 0; u < MAXT; ++u)
+    b[u] = (u < n && xrow) ? ldx(xrow + (t0 + u) * 32 + koff) : z;
+#pragma unroll
+  for (int u = 0; u < MAXT; ++u)
+    if (u < n) acc = mfma16(a[u], b[u], acc);
+  return acc;
+}
+
+// sum of the NW per-wave accumulators in wave order; the result is valid
+// in wave 0.  red holds NW*64 f32x4.
+template <int NW>
+__device__ __forceinline__ f32x4_t block_acc_sum(f32x4_t acc, f32x4_t* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  red[w * 64 + lane] = acc;
+  __syncthreads();
+  f32x4_t s = red[lane];
+  if (w == 0) {
+#pragma unroll
+    for (int x = 1; x < NW; ++x) s += red[x * 64 + lane];
+  }
+  return s;
+}
+
+// RMSNorm of rows r < R of src (row idx[r] when idx, row stride H,
+// H % 256 == 0, H <= 2048) with gain g into LDS xs[r][ldl] (bf16);
+// optionally float32 copies to yf (row stride ldf) when write_f.  One wave
+// per row; each lane loads its (up to 8) float4 of the row and of g before
+// using any of them.
+__device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restrict__ src,
+                                              const int32_t* __restrict__ idx,
+                                              const float* __restrict__ g, float eps,
+                                              uint16_t* xs, int ldl, float* __restrict__ yf,
+                                              int ldf, bool write_f) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int n4 = H / 256;  // float4 per lane
+  float4 gv[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+    if (u < n4) gv[u] = ((const float4*)g)[u * 64 + lane];
+  for (int r = w; r < R; r += nw) {
+    const float4* x = (const float4*)(src + (size_t)(idx ? idx[r] : r) * H);
+    float4 xv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n4) xv[u] = x[u * 64 + lane];
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n4) ss += xv[u].x * xv[u].x + xv[u].y * xv[u].y + xv[u].z * xv[u].z + xv[u].w * xv[u].w;
+    ss = wave_sum(ss);
+    const float rinv = rsqrtf(ss / (float)H + eps);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (u < n4) {
+        const int j = (u * 64 + lane) * 4;
+        const float y0 = xv[u].x * rinv * gv[u].x, y1 = xv[u].y * rinv * gv[u].y;
+        const float y2 = xv[u].z * rinv * gv[u].z, y3 = xv[u].w * rinv * gv[u].w;
+        uint2 pk;
+        pk.x = (uint32_t)f2bf(y0) | ((uint32_t)f2bf(y1) << 16);
+        pk.y = (uint32_t)f2bf(y2) | ((uint32_t)f2bf(y3) << 16);
+        *(uint2*)(xs + r * ldl + j) = pk;
+        if (write_f) *(float4*)(yf + (size_t)r * ldf + j) = make_float4(y0, y1, y2, y3);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- dense split-K
+// Y[r][n] (=|+=) X[r] . W[n], one 16-feature strip per block, K split over
+// NW waves.  X bf16 rows in global memory.
+template <int NW, bool ADD>
+__global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
+                                                  const uint16_t* __restrict__ X, int ldx_,
+                                                  const uint4* __restrict__ Wp,
+                                                  float* __restrict__ Y, int ldy) {
+  __shared__ f32x4_t red[NW * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nt = blockIdx.x;
+  const int r = lane & 15;
+  const uint16_t* xrow = r < R ? X + (size_t)r * ldx_ : nullptr;
+  const int per = nkt / NW;
+  f32x4_t acc = sk_range(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per, xrow,
+                         f32x4_t{0.f, 0.f, 0.f, 0.f});
+  acc = block_acc_sum<NW>(acc, red);
+  if (w != 0 || r >= R) return;
+  const int n = nt * 16 + 4 * (lane >> 4);
+  if (n >= N) return;
+  float4* y = (float4*)(Y + (size_t)r * ldy + n);
+  float4 v = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  if (ADD) {
+    const float4 o = *y;
+    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+  }
+  *y = v;
+}
+
+// ---------------------------------------------------------------- QKV
+// Task = block: a q/k rotate-half pair of strips (RoPE in registers) or a v
+// strip; K split over 4 waves (<= 16 tiles each).  Each wave first issues
+// its weight-tile loads, then the block computes x = RMSNorm(h; g) of the R
+// rows into LDS (the prologue overlaps the weight fetch), then multiplies.
+// q -> q_out (float32), k/v -> cache at the row position.
+__global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int dh,
+                                               const float* __restrict__ h,
+                                               const float* __restrict__ g, float eps,
+                                               const uint4* __restrict__ Wp,
+                                               const float2* __restrict__ rope,
+                                               const int32_t* __restrict__ row_pos,
+                                               const int32_t* __restrict__ row_valid,
+                                               uint16_t* __restrict__ cache, size_t seq_stride,
+                                               int cap, float* __restrict__ q_out) {
+  extern __shared__ __align__(16) uint16_t xs[];  // [R][H + XPAD]
+  __shared__ f32x4_t red[2 * 4 * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ldl = H + XPAD, nkt = H / 32, per = nkt / 4;
+  const int D = nh * dh, half = dh / 2, tph = dh / 32;
+  const int task = blockIdx.x, n_pair = 2 * nh * tph;
+  const bool pair = task < n_pair;
+  int sec = 0, hh = 0, pt = 0, ta, tb;
+  if (pair) {
+    sec = task / (nh * tph);
+    const int rest = task % (nh * tph);
+    hh = rest / tph;
+    pt = rest % tph;
+    ta = (sec * D + hh * dh) / 16 + pt;
+    tb = ta + tph;
+  } else {
+    ta = 2 * D / 16 + (task - n_pair);
+    tb = ta;
+  }
+  uint4 a0[16], a1[16];
+  preload<16>(Wp + (size_t)ta * nkt * 64, w * per, per, a0);
+  if (pair) preload<16>(Wp + (size_t)tb * nkt * 64, w * per, per, a1);
+  // row bookkeeping loads, independent of everything above
+  const int r = lane & 15;
+  const int valid = r < R ? row_valid[r] : 0;
+  const int pos = r < R ? row_pos[r] : 0;
+  norm_rows_lds(R, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+  __syncthreads();
+  const uint16_t* xrow = r < R ? xs + r * ldl : nullptr;
+  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t c0 = mma_pre<16>(a0, w * per, per, xrow, z4);
+  c0 = block_acc_sum<4>(c0, red);
+  if (pair) {
+    f32x4_t c1 = mma_pre<16>(a1, w * per, per, xrow, z4);
+    c1 = block_acc_sum<4>(c1, red + 4 * 64);
+    if (w != 0 || r >= R) return;
+    const int p = valid ? pos : 0;
+    const int b = r / C;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int i = pt * 16 + 4 * (lane >> 4) + t;
+      const float2 cs = rope[(size_t)p * half + i];
+      const float x0 = c0[t], x1 = c1[t];
+      const float y0 = x0 * cs.x - x1 * cs.y, y1 = x1 * cs.x + x0 * cs.y;
+      if (sec == 0) {
+        q_out[(size_t)r * D + hh * dh + i] = y0;
+        q_out[(size_t)r * D + hh * dh + i + half] = y1;
+      } else if (valid) {
+        uint16_t* kc = cache + (size_t)b * seq_stride + ((size_t)hh * cap + p) * dh;
+        kc[i] = f2bf(y0);
+        kc[i + half] = f2bf(y1);
+      }
+    }
+  } else {
+    if (w != 0 || r >= R || !valid) return;
+    const int b = r / C;
+    const int f = (ta - 2 * D / 16) * 16 + 4 * (lane >> 4);
+    const int hv = f / dh, d = f % dh;
+    uint16_t* vc = cache + (size_t)b * seq_stride + ((size_t)(nh + hv) * cap + pos) * dh + d;
+    uint2 pk;
+    pk.x = (uint32_t)f2bf(c0[0]) | ((uint32_t)f2bf(c0[1]) << 16);
+    pk.y = (uint32_t)f2bf(c0[2]) | ((uint32_t)f2bf(c0[3]) << 16);
+    *(uint2*)vc = pk;
+  }
+}
+
+// ---------------------------------------------------------------- attention
+// Split-K decode attention, merge fused.  Block (split s, head h,
+// z = b*ngroups + g) covers keys [s*spl, (s+1)*spl) of sequence b for the
+// NR query rows of group g.  Per 64-key tile the block loads K and V with
+// coalesced 16-byte loads (the next tile's loads are issued before the
+// current tile is used) into LDS; wave w owns rows w, w+4: lane = key for
+// the scores, lane = 2 (or 1) dims for P.V.  Float32 scores and softmax.
+// The last block of a (z, head) merges all splits and writes bf16.
+template <int DH, int NR>
+__global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int spl,
+                                                const float* __restrict__ q,
+                                                const uint16_t* __restrict__ cache,
+                                                size_t seq_stride, int cap,
+                                                const int32_t* __restrict__ row_pos,
+                                                const int32_t* __restrict__ row_valid,
+                                                float scale, float* __restrict__ part,
+                                                int32_t* __restrict__ counters,
+                                                uint16_t* __restrict__ out) {
+  constexpr int KL = DH + 8;            // padded LDS row of K (bf16)
+  constexpr int VPT = 64 * DH / 8 / 256;  // uint4 per thread per tile (K or V)
+  constexpr int DPL = DH / 64;
+  constexpr int RPW = (NR + 3) / 4;     // rows per wave
+  __shared__ __align__(16) uint16_t Ks[64 * KL];
+  __shared__ __align__(16) uint16_t Vs[64 * DH];
+  __shared__ __align__(16) float qs[NR][DH];
+  __shared__ __align__(16) float ps[4][64];
+  __shared__ int last;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int s = blockIdx.x, h = blockIdx.y;
+  const int ngroups = (C + NR - 1) / NR;
+  const int b = blockIdx.z / ngroups, g = blockIdx.z % ngroups;
+  const int i0 = g * NR, nr = min(NR, C - i0);
+  const int D = nh * DH;
+  int lim[NR];
+  {
+    int rv[NR], rp[NR];
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const int r = b * C + i0 + min(i, nr - 1);
+      rv[i] = row_valid[r];
+      rp[i] = row_pos[r];
+    }
+#pragma unroll
+    for (int i = 0; i < NR; ++i) lim[i] = (i < nr && rv[i]) ? rp[i] : -1;
+  }
+  int maxpos = -1;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) maxpos = max(maxpos, lim[i]);
+  const int k0 = s * spl, k1 = min(k0 + spl, maxpos + 1);
+  const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
+  const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
+  // first tile's loads
+  uint4 kreg[VPT], vreg[VPT];
+  auto load_tile = [&](int t0) {
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int c = threadIdx.x + 256 * u;  // 16-byte chunk of the tile
+      const int key = c / (DH / 8), part8 = c % (DH / 8);
+      const int j = min(t0 + key, cap - 1);
+      kreg[u] = *(const uint4*)(Kc + (size_t)j * DH + part8 * 8);
+      vreg[u] = *(const uint4*)(Vc + (size_t)j * DH + part8 * 8);
+    }
+  };
+  if (k0 < k1) load_tile(k0);
+  for (int e = threadIdx.x; e < NR * DH; e += 256) {
+    const int i = e / DH, d = e % DH;
+    qs[i][d] = i < nr ? q[(size_t)(b * C + i0 + i) * D + h * DH + d] : 0.f;
+  }
+  float m[RPW], l[RPW], o[RPW][DPL];
+#pragma unroll
+  for (int x = 0; x < RPW; ++x) {
+    m[x] = -INFINITY;
+    l[x] = 0.f;
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) o[x][d] = 0.f;
+  }
+  for (int t0 = k0; t0 < k1; t0 += 64) {
+    __syncthreads();  // previous tile fully consumed
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int c = threadIdx.x + 256 * u;
+      const int key = c / (DH / 8), part8 = c % (DH / 8);
+      *(uint4*)(Ks + key * KL + part8 * 8) = kreg[u];
+      *(uint4*)(Vs + key * DH + part8 * 8) = vreg[u];
+    }
+    __syncthreads();
+    if (t0 + 64 < k1) load_tile(t0 + 64);  // next tile in flight
+    const int j = t0 + lane;
+#pragma unroll
+    for (int x = 0; x < RPW; ++x) {
+      const int i = wv + 4 * x;
+      if (i >= NR) break;
+      // score of key j for row i
+      float sc = 0.f;
+      const uint16_t* kr = Ks + lane * KL;
+#pragma unroll
+      for (int c = 0; c < DH / 8; ++c) {
+        const uint4 v = *(const uint4*)(kr + c * 8);
+        const float4 qa = *(const float4*)&qs[i][c * 8];
+        const float4 qb = *(const float4*)&qs[i][c * 8 + 4];
+        sc += qa.x * __uint_as_float(v.x << 16) + qa.y * __uint_as_float(v.x & 0xffff0000u) +
+              qa.z * __uint_as_float(v.y << 16) + qa.w * __uint_as_float(v.y & 0xffff0000u) +
+              qb.x * __uint_as_float(v.z << 16) + qb.y * __uint_as_float(v.z & 0xffff0000u) +
+              qb.z * __uint_as_float(v.w << 16) + qb.w * __uint_as_float(v.w & 0xffff0000u);
+      }
+      const float si = (j <= lim[i]) ? sc * scale : -INFINITY;
+      const float mn = fmaxf(m[x], wave_max(si));
+      const float p = (mn == -INFINITY) ? 0.f : __expf(si - mn);
+      const float corr = (mn == -INFINITY) ? 1.f : __expf(m[x] - mn);
+      l[x] = l[x] * corr + wave_sum(p);
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) o[x][d] *= corr;
+      m[x] = mn;
+      // P.V over the 64 keys of the tile (p broadcast from LDS; keys past
+      // the end of the split have p = 0)
+      ps[wv][lane] = p;
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+      for (int j4 = 0; j4 < 16; ++j4) {
+        const float4 p4 = *(const float4*)&ps[wv][4 * j4];
+        const float pp[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+        for (int q2 = 0; q2 < 4; ++q2) {
+          const int jj = 4 * j4 + q2;
+          if (DPL == 2) {
+            const uint32_t uu = *(const uint32_t*)(Vs + jj * DH + lane * 2);
+            o[x][0] += pp[q2] * __uint_as_float(uu << 16);
+            o[x][DPL - 1] += pp[q2] * __uint_as_float(uu & 0xffff0000u);
+          } else {
+            o[x][0] += pp[q2] * bf2f(Vs[jj * DH + lane]);
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  // partial of each owned row
+#pragma unroll
+  for (int x = 0; x < RPW; ++x) {
+    const int i = wv + 4 * x;
+    if (i >= nr) break;
+    const int r = b * C + i0 + i;
+    float* pp = part + (((size_t)r * nh + h) * n_split + s) * (DH + 2);
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) pp[lane * DPL + d] = o[x][d];
+    if (lane == 0) {
+      pp[DH] = m[x];
+      pp[DH + 1] = l[x];
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  int32_t* ctr = counters + (size_t)blockIdx.z * nh + h;
+  if (threadIdx.x == 0) last = atomicAdd(ctr, 1) == n_split - 1;
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  if (threadIdx.x == 0) *ctr = 0;
+  // merge: wave w merges rows w, w+4 (lane = dims)
+#pragma unroll
+  for (int x = 0; x < RPW; ++x) {
+    const int i = wv + 4 * x;
+    if (i >= nr) break;
+    const int r = b * C + i0 + i;
+    const float* pp = part + ((size_t)r * nh + h) * n_split * (DH + 2);
+    float M = -INFINITY;
+    for (int y = 0; y < n_split; ++y) M = fmaxf(M, pp[y * (DH + 2) + DH]);
+    float L = 0.f, O[DPL];
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) O[d] = 0.f;
+    for (int y = 0; y < n_split; ++y) {
+      const float ms = pp[y * (DH + 2) + DH];
+      if (ms == -INFINITY) continue;
+      const float f = __expf(ms - M);
+      L += pp[y * (DH + 2) + DH + 1] * f;
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) O[d] += pp[y * (DH + 2) + lane * DPL + d] * f;
+    }
+    const bool ok = row_valid[r] && L > 0.f;
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) out[(size_t)r * D + h * DH + lane * DPL + d] = f2bf(ok ? O[d] / L : 0.f);
+  }
+}
+
+// ---------------------------------------------------------------- router
+// One block (16 waves) for all R <= 16 rows.  Prologue: y = RMSNorm(h; g)
+// into LDS and to xout (bf16, for the experts).  Router logits by MFMA
+// (strip x K-quarter per wave), bias, float32 softmax, top-k (larger logit
+// first, equal -> lower id), k-th vs (k+1)-th gap; then the grouping of
+// (row, slot) pairs by expert (rows ascending) and the list of touched
+// experts (ascending id).
+__global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk,
+                                                   const float* __restrict__ h,
+                                                   const float* __restrict__ g, float eps,
+                                                   uint16_t* __restrict__ xout,
+                                                   const uint4* __restrict__ Wp,
+                                                   const float* __restrict__ bias,
+                                                   int32_t* __restrict__ ridx,
+                                                   float* __restrict__ rw,
+                                                   float* __restrict__ rgap,
+                                                   int32_t* __restrict__ ridx_out,
+                                                   int32_t* __restrict__ cnt,
+                                                   int32_t* __restrict__ off,
+                                                   int32_t* __restrict__ ent_row,
+                                                   int32_t* __restrict__ ent_slot,
+                                                   float* __restrict__ ent_w,
+                                                   int32_t* __restrict__ touched,
+                                                   int32_t* __restrict__ n_touched) {
+  extern __shared__ __align__(16) uint16_t xs[];  // [R][H + XPAD]
+  __shared__ f32x4_t red[16 * 64];
+  __shared__ float lg[SR_MAX][65];
+  __shared__ int sel[SR_MAX * 8];
+  __shared__ float selw[SR_MAX * 8];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ldl = H + XPAD, nkt = H / 32;
+  // 16 waves = 4 strips x 4 K-quarters; weight tiles first
+  const int strip = w >> 2, qk = w & 3, per = nkt / 4;
+  const bool live = strip * 16 < E;
+  uint4 a[16];
+  if (live) preload<16>(Wp + (size_t)strip * nkt * 64, qk * per, per, a);
+  const float bl = (bias && lane < E) ? bias[lane] : 0.f;
+  norm_rows_lds(R, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+  __syncthreads();
+  for (int e = threadIdx.x; e < R * H / 8; e += blockDim.x) {
+    const int rr = e / (H / 8), c8 = e % (H / 8);
+    *(uint4*)(xout + (size_t)rr * H + c8 * 8) = *(const uint4*)(xs + rr * ldl + c8 * 8);
+  }
+  const int r = lane & 15;
+  const uint16_t* xrow = r < R ? xs + r * ldl : nullptr;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if (live) acc = mma_pre<16>(a, qk * per, per, xrow, acc);
+  red[w * 64 + lane] = acc;
+  __syncthreads();
+  if (qk == 0 && live) {
+    f32x4_t sacc = red[w * 64 + lane];
+    for (int x = 1; x < 4; ++x) sacc += red[(w + x) * 64 + lane];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) lg[r][strip * 16 + 4 * (lane >> 4) + t] = sacc[t];
+  }
+  __syncthreads();
+  // top-k, one wave per row
+  __shared__ __align__(16) float tsc[16][68];
+  if (w < R) {
+    const float lv = lane < E ? lg[w][lane] + bl : -INFINITY;
+    lane_topk(lv, E, topk, tsc[w], ridx + (size_t)w * topk, rw + (size_t)w * topk,
+              rgap ? rgap + w : nullptr, ridx_out ? ridx_out + (size_t)w * topk : nullptr,
+              sel + w * topk, selw + w * topk);
+  }
+  __syncthreads();
+  // grouping: one thread per expert counts, one thread per entry places
+  __shared__ int l_cnt[64], l_off[64];
+  const int nent = R * topk;
+  if (threadIdx.x < 64) {
+    const int e = threadIdx.x;
+    int c = 0;
+#pragma unroll 8
+    for (int x = 0; x < nent; ++x) c += sel[x] == e;
+    l_cnt[e] = e < E ? c : 0;
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int e = threadIdx.x;
+    int o = 0;
+    for (int x = 0; x < e; ++x) o += l_cnt[x];
+    if (e < E) {
+      cnt[e] = l_cnt[e];
+      off[e] = o;
+    }
+    l_off[e] = o;
+  }
+  __syncthreads();
+  if (threadIdx.x < nent) {
+    const int x = threadIdx.x, e = sel[x];
+    int before = 0;
+    for (int y = 0; y < x; ++y) before += sel[y] == e;
+    const int t = l_off[e] + before;
+    ent_row[t] = x / topk;
+    ent_slot[t] = x % topk;
+    ent_w[t] = selw[x];
+  }
+  if (threadIdx.x == 0) {  // touched-expert list (ascending id)
+    int n = 0;
+    for (int e = 0; e < E; ++e)
+      if (l_cnt[e] > 0) touched[n++] = e;
+    *n_touched = n;
+  }
+}
+
+// ---------------------------------------------------------------- MoE gate/up
+// Block = (16-wide intermediate tile, expert y): routed expert y < E over
+// its cnt[y] entries (blocks of untouched experts exit after one load), or
+// y == E: the dense SwiGLU over all rows (the shared experts as one
+// width-SI SwiGLU, or the draft FFN).  K split over 4 waves; weight tiles
+// are loaded first.  With g != NULL the B rows are RMSNorm(h; g) computed
+// into LDS (dense mode), else the bf16 rows xg.
+__global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI,
+                                              const uint16_t* __restrict__ xg,
+                                              const float* __restrict__ h,
+                                              const float* __restrict__ g, float eps,
+                                              const uint4* __restrict__ egu, size_t e_stride,
+                                              const uint4* __restrict__ sgu,
+                                              const int32_t* __restrict__ cnt,
+                                              const int32_t* __restrict__ off,
+                                              const int32_t* __restrict__ ent_row,
+                                              uint16_t* __restrict__ act,
+                                              uint16_t* __restrict__ act_sh) {
+  extern __shared__ __align__(16) uint16_t xs[];
+  __shared__ f32x4_t red[2 * 4 * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int it = blockIdx.x, e = blockIdx.y;
+  const bool dense = e == E;
+  const int width = dense ? SI : I;
+  if (it * 16 >= width) return;
+  int n = R, o = 0;
+  if (!dense) {
+    n = cnt[e];
+    o = off[e];
+    if (n == 0) return;
+  }
+  const int nkt = H / 32, per = nkt / 4, ldl = H + XPAD;
+  const uint4 *G, *U;
+  if (dense) {
+    G = sgu + (size_t)it * nkt * 64;
+    U = sgu + (size_t)(SI / 16 + it) * nkt * 64;
+  } else {
+    const uint4* base = egu + (size_t)e * e_stride;
+    G = base + (size_t)it * nkt * 64;
+    U = base + (size_t)(I / 16 + it) * nkt * 64;
+  }
+  uint4 ag_[16], au_[16];
+  preload<16>(G, w * per, per, ag_);
+  preload<16>(U, w * per, per, au_);
+  const int t = lane & 15;
+  const uint16_t* xrow = nullptr;
+  if (g) {
+    norm_rows_lds(R, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+    __syncthreads();
+    if (t < n) xrow = xs + t * ldl;
+  } else if (t < n) {
+    xrow = xg + (size_t)(dense ? t : ent_row[o + t]) * H;
+  }
+  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t cg = mma_pre<16>(ag_, w * per, per, xrow, z4);
+  f32x4_t cu = mma_pre<16>(au_, w * per, per, xrow, z4);
+  cg = block_acc_sum<4>(cg, red);
+  cu = block_acc_sum<4>(cu, red + 4 * 64);
+  if (w != 0 || t >= n) return;
+  const int i = it * 16 + 4 * (lane >> 4);
+  uint2 pk;
+  pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
+  pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
+  if (dense)
+    *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
+  else
+    *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
+}
+
+// ---------------------------------------------------------------- MoE down
+// Block = 16 output features (one strip of every down matrix); its 16 waves
+// take the virtual experts round-robin -- the touched routed experts in
+// ascending id, then the S shared experts (width I each) -- and accumulate
+// w_t * (Wd[n] . act_t) into per-wave LDS rows; the block then adds the
+// wave-ordered sum into h (only this block writes these 16 columns).  The
+// expert lists are staged in LDS first so no wave chains index loads.
+__global__ void __launch_bounds__(1024) k_s_down(int R, int H, int E, int I, int S,
+                                                 const uint16_t* __restrict__ act,
+                                                 const uint16_t* __restrict__ act_sh,
+                                                 const uint4* __restrict__ edn, size_t e_stride,
+                                                 const uint4* __restrict__ sdn,
+                                                 const int32_t* __restrict__ cnt,
+                                                 const int32_t* __restrict__ off,
+                                                 const int32_t* __restrict__ ent_row,
+                                                 const float* __restrict__ ent_w,
+                                                 float* __restrict__ h) {
+  constexpr int NW = 16;
+  __shared__ float acc_l[NW][SR_MAX][17];
+  __shared__ int l_cnt[64], l_off[64], l_list[64], l_n;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nt = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const int e = threadIdx.x;
+    l_cnt[e] = e < E ? cnt[e] : 0;
+    l_off[e] = e < E ? off[e] : 0;
+  }
+  for (int e = threadIdx.x; e < NW * SR_MAX * 17; e += blockDim.x) (&acc_l[0][0][0])[e] = 0.f;
+  __syncthreads();
+  if (w == 0) {  // compact list of touched experts, ascending id
+    const int has = l_cnt[lane] > 0;
+    int pre = has;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(pre, d, MTP_WAVE);
+      if (lane >= d) pre += v;
+    }
+    if (has) l_list[pre - 1] = lane;
+    if (lane == 63) l_n = pre;
+  }
+  __syncthreads();
+  const int n_routed = l_n, nvirt = n_routed + S;
+  const int nkt = I / 32;
+  const int t = lane & 15;
+  for (int v = w; v < nvirt; v += NW) {
+    const uint4* A;
+    const uint16_t* xrow = nullptr;
+    int row = -1;
+    float wt = 1.f;
+    if (v < n_routed) {
+      const int e = l_list[v];
+      const int n = l_cnt[e], o = l_off[e];
+      A = edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
+      if (t < n) {
+        xrow = act + (size_t)(o + t) * I;
+        row = ent_row[o + t];
+        wt = ent_w[o + t];
+      }
+    } else {
+      const int sx = v - n_routed;
+      // shared expert sx: columns sx*I.. of the [H][S*I] down matrix, whose
+      // packed strip nt has S*nkt tiles
+      A = sdn + (size_t)nt * S * nkt * 64 + (size_t)sx * nkt * 64;
+      if (t < R) {
+        xrow = act_sh + (size_t)t * S * I + (size_t)sx * I;
+        row = t;
+      }
+    }
+    const f32x4_t a = sk_range(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    if (row >= 0) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += wt * a[q];
+    }
+  }
+  __syncthreads();
+  const int rr = threadIdx.x >> 4, f = threadIdx.x & 15;
+  if (rr < R) {
+    float sum = 0.f;
+    for (int x = 0; x < NW; ++x) sum += acc_l[x][rr][f];
+    h[(size_t)rr * H + nt * 16 + f] += sum;
+  }
+}
+
+// ---------------------------------------------------------------- LM head
+// Block = 4 vocabulary strips (64 rows) x the nr <= 16 input rows X (bf16);
+// per row the best logit, its id (lowest on ties) and the second best.
+__global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16_t* __restrict__ X,
+                                              const uint4* __restrict__ Wp,
+                                              float* __restrict__ logits, size_t ldl,
+                                              float* __restrict__ pv, int32_t* __restrict__ pi,
+                                              float* __restrict__ p2) {
+  __shared__ float bv[4][SR_MAX], sv[4][SR_MAX];
+  __shared__ int bi[4][SR_MAX];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int nkt = H / 32;
+  const int nt = blockIdx.x * 4 + wv;
+  const int r = lane & 15;
+  const uint16_t* xrow = r < nr ? X + (size_t)r * H : nullptr;
+  const bool live = nt * 16 < V;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if (live) acc = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow, acc);
+  const int v0 = nt * 16 + 4 * (lane >> 4);
+  float b1 = -INFINITY, b2 = -INFINITY;
+  int id = 1 << 30;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int v = v0 + t;
+    const float x = (live && v < V) ? acc[t] : -INFINITY;
+    if (logits && r < nr && live && v < V) logits[(size_t)r * ldl + v] = x;
+    if (x > b1) {
+      b2 = b1;
+      b1 = x;
+      id = v;
+    } else if (x > b2) {
+      b2 = x;
+    }
+  }
+#pragma unroll
+  for (int o = 16; o <= 32; o <<= 1) {
+    const float ob1 = __shfl_xor(b1, o, MTP_WAVE), ob2 = __shfl_xor(b2, o, MTP_WAVE);
+    const int oid = __shfl_xor(id, o, MTP_WAVE);
+    if (ob1 > b1 || (ob1 == b1 && oid < id)) {
+      b2 = fmaxf(b1, ob2);
+      b1 = ob1;
+      id = oid;
+    } else {
+      b2 = fmaxf(b2, ob1);
+    }
+  }
+  if (lane < 16) {
+    bv[wv][lane] = b1;
+    sv[wv][lane] = b2;
+    bi[wv][lane] = id;
+  }
+  __syncthreads();
+  if (threadIdx.x < nr) {
+    const int rr = threadIdx.x;
+    float c1 = bv[0][rr], c2 = sv[0][rr];
+    int cid = bi[0][rr];
+    for (int x = 1; x < 4; ++x) {
+      const float ob1 = bv[x][rr], ob2 = sv[x][rr];
+      const int oid = bi[x][rr];
+      if (ob1 > c1 || (ob1 == c1 && oid < cid)) {
+        c2 = fmaxf(c1, ob2);
+        c1 = ob1;
+        cid = oid;
+      } else {
+        c2 = fmaxf(c2, ob1);
+      }
+    }
+    const size_t o = (size_t)rr * gridDim.x + blockIdx.x;
+    pv[o] = c1;
+    pi[o] = cid;
+    p2[o] = c2;
+  }
+}
+
+}  // namespace mtp

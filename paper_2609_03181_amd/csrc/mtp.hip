@@ -11,6 +11,7 @@
 #include "kernels_generic.h"
 #include "kernels_rows.h"
 #include "kernels_mfma.h"
+#include "kernels_small.h"
 #include "kernels_spec.h"
 
 using namespace mtp;
@@ -29,7 +30,8 @@ struct mtp_ctx {
   mtp_weights w;
   float2* rope;  // [max_ctx][head_dim/2] (cos, sin)
   Packed pk;     // bf16 models only
-  int n_split;   // attention key splits of ATT_SPL positions
+  int n_split;   // attention key splits ...
+  int spl;       // ... of spl positions each (multiple of 64)
 };
 
 namespace {
@@ -48,7 +50,7 @@ struct Ws {
   void *xin, *attn, *act, *xhead;
   // bf16 fast path
   float *part, *slot, *ent_w;
-  int32_t *cnt, *off, *ent_row, *ent_slot;
+  int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr;
   uint16_t* act_sh;
   size_t bytes;
 };
@@ -104,11 +106,14 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.off = (int32_t*)take((size_t)c.n_routed * 4);
     w.ent_row = (int32_t*)take(R * k * 4);
     w.ent_slot = (int32_t*)take(R * k * 4);
+    w.touched = (int32_t*)take((size_t)c.n_routed * 4);
+    w.n_touched = (int32_t*)take(4);
+    w.att_ctr = (int32_t*)take(R * c.n_heads * 4);
     const size_t shw = (size_t)(SI > c.draft_inter ? SI : c.draft_inter);
     w.act_sh = (uint16_t*)take(R * shw * 2);
   } else {
     w.part = w.slot = w.ent_w = nullptr;
-    w.cnt = w.off = w.ent_row = w.ent_slot = nullptr;
+    w.cnt = w.off = w.ent_row = w.ent_slot = w.touched = w.n_touched = w.att_ctr = nullptr;
     w.act_sh = nullptr;
   }
   w.bytes = off;
@@ -126,6 +131,7 @@ struct Model {
   hipStream_t s;
   const Packed& pk;
   int n_split;
+  int spl;
 
   const T* wp(const void* p, size_t off_elems) const { return (const T*)p + off_elems; }
 
@@ -165,8 +171,12 @@ struct Model {
                 float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
                 float* margin, int32_t* route_idx, float* route_gap) {
     if constexpr (BF) {
-      verifier_fast(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
-                    logits, margin, route_idx, route_gap);
+      if (B * C <= SR_MAX && c.top_k <= 8 && small_ok())
+        verifier_small(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
+                       logits, margin, route_idx, route_gap);
+      else
+        verifier_fast(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
+                      logits, margin, route_idx, route_gap);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -215,8 +225,12 @@ struct Model {
              int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
              size_t ldl) {
     if constexpr (BF) {
-      draft_fast(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
-                 logits, ldl);
+      if (B * C <= SR_MAX && small_ok())
+        draft_small(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
+                    logits, ldl);
+      else
+        draft_fast(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
+                   logits, ldl);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -271,16 +285,8 @@ struct Model {
       k_qkv_rope<4><<<dim3(cdiv(tasks, 4), cdiv(R, 64)), 256, 0, s>>>(
           R, C, nh, dh, H / 32, (const uint16_t*)ws.xin, wqkv, rope, ws.row_pos, ws.row_valid,
           cache, seq_stride, c.max_ctx, ws.q);
-    const int ng = (C + ATT_ROWS - 1) / ATT_ROWS;
-    dim3 ag(n_split, nh, B * ng);
-    const float scale = 1.0f / sqrtf((float)dh);
-    if (dh == 128)
-      k_attn_split<128><<<ag, 256, 0, s>>>(C, nh, n_split, ws.q, cache, seq_stride, c.max_ctx,
-                                           ws.row_pos, ws.row_valid, scale, ws.part);
-    else
-      k_attn_split<64><<<ag, 256, 0, s>>>(C, nh, n_split, ws.q, cache, seq_stride, c.max_ctx,
-                                          ws.row_pos, ws.row_valid, scale, ws.part);
-    k_attn_merge<<<R, 256, 0, s>>>(nh, dh, n_split, ws.part, ws.row_valid, (uint16_t*)ws.attn);
+    if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
+    else sattn<64>(ws, B, C, cache, seq_stride);
     mmr(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
   }
 
@@ -297,6 +303,133 @@ struct Model {
                                                             logits, ldl, ws.pv, ws.pi, ws.p2);
     k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
+  }
+
+  // ------------------------------------------------------------ small-batch path
+  // shapes the small-batch kernels cover: per-wave tile counts <= 16 and
+  // whole float4 rows per lane
+  bool small_ok() const {
+    return c.hidden % 256 == 0 && c.hidden <= 2048 && c.n_routed <= 64;
+  }
+  static int nw_for(int nkt) {
+    if (nkt % 16 == 0 && nkt >= 128) return 16;
+    if (nkt % 8 == 0 && nkt >= 64) return 8;
+    return 4;
+  }
+  void smm(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
+           bool add) {
+    const int nkt = K / 32, nw = nw_for(nkt);
+    const unsigned g = cdiv(N, 16);
+#define MTP_SMM(NW)                                                                       \
+  if (add) k_s_mm<NW, true><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);        \
+  else k_s_mm<NW, false><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);
+    if (nw == 16) { MTP_SMM(16) } else if (nw == 8) { MTP_SMM(8) } else { MTP_SMM(4) }
+#undef MTP_SMM
+  }
+
+  template <int DH, int NR>
+  void sattn_launch(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
+    const int ng = (C + NR - 1) / NR;
+    k_s_attn<DH, NR><<<dim3(n_split, c.n_heads, B * ng), 256, 0, s>>>(
+        C, c.n_heads, n_split, spl, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
+        1.0f / sqrtf((float)DH), ws.part, ws.att_ctr, (uint16_t*)ws.attn);
+  }
+  template <int DH>
+  void sattn(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
+    if (C <= 1) sattn_launch<DH, 1>(ws, B, C, cache, seq_stride);
+    else if (C <= 2) sattn_launch<DH, 2>(ws, B, C, cache, seq_stride);
+    else if (C <= 4) sattn_launch<DH, 4>(ws, B, C, cache, seq_stride);
+    else sattn_launch<DH, 8>(ws, B, C, cache, seq_stride);
+  }
+
+  // pre-norm attention sub-layer: h += Wo attn(RMSNorm(h; g)), small batch
+  void attn_small(const Ws& ws, int B, int C, const float* g, const uint4* wqkv, const uint4* wo,
+                  uint16_t* cache, size_t seq_stride) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    const size_t lds = (size_t)R * (H + XPAD) * 2;
+    k_s_qkv<<<D / 8, 256, lds, s>>>(R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, wqkv, rope,
+                                    ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q);
+    if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
+    else sattn<64>(ws, B, C, cache, seq_stride);
+    smm(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
+  }
+
+  // LM head over nr rows of ws.xhead (bf16, already normalised)
+  void lm_small(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
+                int32_t* tok, float* margin) {
+    const int V = c.vocab, H = c.hidden;
+    const unsigned nblk = cdiv(cdiv(V, 16), 4);
+    k_s_lm<<<nblk, 256, 0, s>>>(nr, V, H, (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv,
+                                ws.pi, ws.p2);
+    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
+                                               tok, margin);
+  }
+
+  void verifier_small(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
+                      float* hid, bool head_all, int32_t* tok, int per, int ostride,
+                      float* logits, float* margin, int32_t* route_idx, float* route_gap) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
+    const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter, S = c.n_shared;
+    const int SI = S * I;
+    const float eps = (float)c.rms_eps;
+    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
+    const size_t layer_stride = (size_t)B * seq_stride;
+    const size_t lds = (size_t)R * (H + XPAD) * 2;
+    k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok,
+                                                  (const T*)w.embed, vision, vis_ld, vis_off, ws.h,
+                                                  ws.status);
+    for (int l = 0; l < L; ++l) {
+      attn_small(ws, B, C, w.attn_norm + (size_t)l * H, pk.wqkv + l * pk.wqkv_s,
+                 pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
+      k_s_router<<<1, 1024, lds, s>>>(
+          R, H, E, k, ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin,
+          pk.router + l * pk.router_s, w.router_bias ? w.router_bias + (size_t)l * E : nullptr,
+          ws.ridx, ws.rw, route_gap ? route_gap + (size_t)l * R : ws.rgap,
+          route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.cnt, ws.off, ws.ent_row,
+          ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched);
+      k_s_gu<<<dim3(cdiv(SI > I ? SI : I, 16), E + 1), 256, 0, s>>>(
+          R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,
+          pk.exp_gu + (size_t)l * E * pk.exp_gu_s, pk.exp_gu_s, pk.sh_gu + l * pk.sh_gu_s, ws.cnt,
+          ws.off, ws.ent_row, (uint16_t*)ws.act, ws.act_sh);
+      k_s_down<<<H / 16, 1024, 0, s>>>(R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh,
+                                       pk.exp_down + (size_t)l * E * pk.exp_down_s,
+                                       pk.exp_down_s, pk.sh_down + l * pk.sh_down_s, ws.cnt,
+                                       ws.off, ws.ent_row, ws.ent_w, ws.h);
+    }
+    k_combine_norm<<<R, 256, 0, s>>>(H, 0, nullptr, ws.h, w.final_norm, eps, hid,
+                                     (tok && head_all) ? (uint16_t*)ws.xhead : nullptr);
+    if (!tok) return;
+    if (head_all) {
+      lm_small(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
+    } else {
+      k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, nullptr, 0,
+                                      (T*)ws.xhead, H, 0);
+      lm_small(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
+    }
+  }
+
+  void draft_small(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
+                   int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride,
+                   int ooff, float* logits, size_t ldl) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    const int F = c.draft_inter;
+    const float eps = (float)c.rms_eps;
+    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
+    k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok,
+                                                         (const T*)w.embed, vision, vis_ld,
+                                                         vis_off, a, a_ld, w.d_enorm, w.d_hnorm,
+                                                         eps, (T*)ws.xin, ws.status);
+    smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
+    attn_small(ws, B, C, w.d_attn_norm, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
+    k_s_gu<<<dim3(F / 16, 1), 256, (size_t)R * (H + XPAD) * 2, s>>>(
+        R, H, 0, F, F, nullptr, ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr,
+        nullptr, nullptr, ws.act_sh);
+    smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
+    (void)D;
+    if (!head) return;
+    k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
+                                    (T*)ws.xhead, H, 0);
+    lm_small(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
   }
 
   void verifier_fast(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
@@ -477,7 +610,11 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   ctx->w = *w;
   ctx->rope = nullptr;
   ctx->pk = Packed{};
-  ctx->n_split = (c.max_ctx + ATT_SPL - 1) / ATT_SPL;
+  // key splits for decode attention: about 128 positions each, at most 64
+  ctx->n_split = (c.max_ctx + 127) / 128;
+  if (ctx->n_split > 64) ctx->n_split = 64;
+  ctx->spl = ((c.max_ctx + ctx->n_split - 1) / ctx->n_split + 63) / 64 * 64;
+  ctx->n_split = (c.max_ctx + ctx->spl - 1) / ctx->spl;
   const int half = c.head_dim / 2;
   const size_t n = (size_t)c.max_ctx * half;
   float2* host = new (std::nothrow) float2[n];
@@ -558,7 +695,7 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl};
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     for (int c0 = 0; c0 < n_rows; c0 += C) {
       const int Cc = n_rows - c0 < C ? n_rows - c0 : C;
@@ -607,7 +744,7 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_draft_len<<<cdiv(batch, 256), 256, 0, s>>>(batch, n_rows, row_pos, draft_len, w.status);
@@ -650,7 +787,7 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, kv_len, 0, nullptr, c.max_ctx, w.row_pos,
