@@ -33,8 +33,25 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "_oracle.so")
 _lib = None
 
-ROUTE_TOL = 1e-3     # router-logit gap below which two routings are both correct
-ARGMAX_TOL = 0.05    # logit gap below which two greedy tokens are both correct
+# Decision tolerances.  Two implementations that round at the same storage
+# points but sum in different orders reach different router logits and
+# token logits; an integer decision (a routing, a greedy token) may then
+# differ only where the oracle's own margin is below the tolerance.
+#   ROUTE_TOL       router k-th vs (k+1)-th logit gap, float32 models;
+#   ROUTE_TOL_BF16  the same for bf16 models: a one-ulp flip of a stored
+#                   bf16 key or value moves every later router logit by
+#                   ~1e-4..1e-3, and a change of summation order alone
+#                   produces such flips (a float32-product evaluation of the
+#                   same model moves router logits by up to ~4e-3);
+#   ARGMAX_TOL      top-1 vs top-2 token logit gap.
+ROUTE_TOL = 1e-3
+ROUTE_TOL_BF16 = 1e-2
+ARGMAX_TOL = 0.05
+
+
+def route_tolerances(cfg) -> np.ndarray:
+    """Per-layer routing tolerance of a model configuration."""
+    return np.full(cfg.n_layers, ROUTE_TOL_BF16 if cfg.dtype == "bf16" else ROUTE_TOL)
 
 
 def build(force: bool = True) -> str:
@@ -69,7 +86,7 @@ def _L():
             build(force=False)
         lib = ctypes.CDLL(_LIB_PATH)
         vp, i32, f32, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_double
-        lib.orc_verify_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, f32, vp,
+        lib.orc_verify_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp, vp, vp, vp, vp]
         lib.orc_verify_rows.restype = i32
         lib.orc_draft_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -116,7 +133,8 @@ class Oracle:
 
     # -- rows ------------------------------------------------------------
     def verify_rows(self, kv, tok, pos, emb=None, head_mask=None, want_logits=False,
-                    want_routes=False, follow_route=None, route_tol=ROUTE_TOL):
+                    want_routes=False, follow_route=None, route_tol=None):
+        """route_tol: per-layer follow tolerance (default route_tolerances)."""
         c = self.cfg
         tok = _c(tok, np.int32)
         pos = _c(pos, np.int32)
@@ -133,9 +151,12 @@ class Oracle:
             rw = np.empty((c.n_layers, n, c.top_k), np.float32)
             rg = np.empty((c.n_layers, n), np.float32)
         fr = _c(follow_route, np.int32)
+        rt = np.ascontiguousarray(np.broadcast_to(
+            route_tolerances(c) if route_tol is None else np.asarray(route_tol, np.float32),
+            (c.n_layers,)), np.float32)
         nf = ctypes.c_int(0)
         rc = _L().orc_verify_rows(ctypes.byref(self.dims), ctypes.byref(self.wts), _p(kv),
-                                  kv.shape[3], n, _p(tok), _p(emb), _p(pos), _p(fr), route_tol,
+                                  kv.shape[3], n, _p(tok), _p(emb), _p(pos), _p(fr), _p(rt),
                                   ctypes.byref(nf), _p(b), _p(hm), _p(logits), _p(amax),
                                   _p(margin), _p(ri), _p(rw), _p(rg))
         if rc < 0:

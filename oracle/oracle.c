@@ -454,12 +454,13 @@ static void input_row(const orc_dims* d, const orc_weights* w, int32_t tok, cons
  * Outputs (each optional): b = final-norm state [nr][H]; LM-head results
  * for rows with head_mask set; routing per layer [L][nr][k]; k-th vs
  * (k+1)-th router-logit gap [L][nr].  follow_route [L][nr][k] makes the
- * oracle adopt externally chosen near-tie routes (see follow_route).
+ * oracle adopt externally chosen near-tie routes (see follow_route), with
+ * tolerance route_tol[l] in layer l.
  * Returns the number of rejected route sets (0 without follow_route), or
  * -1 on a position outside the cache. */
 int orc_verify_rows(const orc_dims* d, const orc_weights* w, float* kv, int cap, int nr,
                     const int32_t* tok, const void* emb, const int32_t* pos,
-                    const int32_t* follow_route, float route_tol, int* n_followed,
+                    const int32_t* follow_route, const float* route_tol, int* n_followed,
                     float* b_out, const uint8_t* head_mask, float* logits, int32_t* amax,
                     float* margin, int32_t* route_idx, float* route_w, float* route_gap) {
   const int H = d->hidden, L = d->n_layers, nh = d->n_heads, dh = d->head_dim, k = d->top_k;
@@ -474,7 +475,8 @@ int orc_verify_rows(const orc_dims* d, const orc_weights* w, float* kv, int cap,
     attn_sublayer(d, w->attn_norm + (size_t)l * H, woff(d, w->wqkv, (size_t)l * 3 * nhd * H),
                   woff(d, w->wo, (size_t)l * H * nhd), kv + (size_t)l * slab, cap, nr, pos, h);
     bad += moe_sublayer(d, w, l, nr, h, follow_route ? follow_route + (size_t)l * nr * k : NULL,
-                        route_tol, n_followed, route_idx ? route_idx + (size_t)l * nr * k : NULL,
+                        follow_route ? route_tol[l] : 0.f, n_followed,
+                        route_idx ? route_idx + (size_t)l * nr * k : NULL,
                         route_w ? route_w + (size_t)l * nr * k : NULL,
                         route_gap ? route_gap + (size_t)l * nr : NULL);
   }

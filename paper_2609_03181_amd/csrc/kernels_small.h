@@ -145,8 +145,9 @@ __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restr
 }
 
 // ---------------------------------------------------------------- dense split-K
-// Y[r][n] (=|+=) X[r] . W[n], one 16-feature strip per block, K split over
-// NW waves.  X bf16 rows in global memory.
+// Y[r][n] (=|+=) X[r] . W[n], one 16-feature strip (blockIdx.x) x one
+// 16-row group (blockIdx.y) per block, K split over NW waves.  X bf16 rows
+// in global memory.
 template <int NW, bool ADD>
 __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
                                                   const uint16_t* __restrict__ X, int ldx_,
@@ -155,7 +156,7 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
   __shared__ f32x4_t red[NW * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nt = blockIdx.x;
-  const int r = lane & 15;
+  const int r = blockIdx.y * 16 + (lane & 15);  // 16-row group blockIdx.y
   const uint16_t* xrow = r < R ? X + (size_t)r * ldx_ : nullptr;
   const int per = nkt / NW;
   f32x4_t acc = sk_range(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per, xrow,
@@ -174,14 +175,16 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
 }
 
 // ---------------------------------------------------------------- QKV
-// Task = block: a q/k rotate-half pair of strips (RoPE in registers) or a v
-// strip; K split over 4 waves (<= 16 tiles each).  Each wave first issues
-// its weight-tile loads, then the block computes x = RMSNorm(h; g) of the R
-// rows into LDS (the prologue overlaps the weight fetch), then multiplies.
+// Task = blockIdx.x: a q/k rotate-half pair of strips (RoPE in registers)
+// or a v strip; rows = 16-row group blockIdx.y; K split over 4 waves (<= 16
+// tiles each).  Each wave first issues its weight-tile loads, then the
+// block computes x = RMSNorm(h; g) of its rows into LDS (the prologue
+// overlaps the weight fetch) -- or, with xg, reads normalised bf16 rows.
 // q -> q_out (float32), k/v -> cache at the row position.
 __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int dh,
                                                const float* __restrict__ h,
                                                const float* __restrict__ g, float eps,
+                                               const uint16_t* __restrict__ xg,
                                                const uint4* __restrict__ Wp,
                                                const float2* __restrict__ rope,
                                                const int32_t* __restrict__ row_pos,
@@ -211,12 +214,19 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
   preload<16>(Wp + (size_t)ta * nkt * 64, w * per, per, a0);
   if (pair) preload<16>(Wp + (size_t)tb * nkt * 64, w * per, per, a1);
   // row bookkeeping loads, independent of everything above
-  const int r = lane & 15;
+  const int r0 = blockIdx.y * 16;
+  const int nloc = min(16, R - r0);
+  const int r = r0 + (lane & 15);
   const int valid = r < R ? row_valid[r] : 0;
   const int pos = r < R ? row_pos[r] : 0;
-  norm_rows_lds(R, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
-  __syncthreads();
-  const uint16_t* xrow = r < R ? xs + r * ldl : nullptr;
+  const uint16_t* xrow = nullptr;
+  if (xg) {
+    if (r < R) xrow = xg + (size_t)r * H;
+  } else {
+    norm_rows_lds(nloc, H, h + (size_t)r0 * H, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+    __syncthreads();
+    if (r < R) xrow = xs + (lane & 15) * ldl;
+  }
   const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
   f32x4_t c0 = mma_pre<16>(a0, w * per, per, xrow, z4);
   c0 = block_acc_sum<4>(c0, red);
@@ -413,34 +423,49 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
   if (!last) return;
   __threadfence();
   if (threadIdx.x == 0) *ctr = 0;
-  // merge: wave w merges rows w, w+4 (lane = dims)
+  // merge: wave w merges rows w, w+4.  Lane y holds split y's (m, l)
+  // (n_split <= 64); the weights e^{m_y - M} go through LDS and each lane
+  // then sums its dims over the splits with all loads in flight.
 #pragma unroll
   for (int x = 0; x < RPW; ++x) {
     const int i = wv + 4 * x;
     if (i >= nr) break;
     const int r = b * C + i0 + i;
     const float* pp = part + ((size_t)r * nh + h) * n_split * (DH + 2);
-    float M = -INFINITY;
-    for (int y = 0; y < n_split; ++y) M = fmaxf(M, pp[y * (DH + 2) + DH]);
-    float L = 0.f, O[DPL];
+    const float my = lane < n_split ? pp[lane * (DH + 2) + DH] : -INFINITY;
+    const float ly = lane < n_split ? pp[lane * (DH + 2) + DH + 1] : 0.f;
+    const float M = wave_max(my);
+    const float fy = (my == -INFINITY) ? 0.f : __expf(my - M);
+    const float L = wave_sum(ly * fy);
+    ps[wv][lane] = fy;
+    __builtin_amdgcn_wave_barrier();
+    float O[DPL];
 #pragma unroll
     for (int d = 0; d < DPL; ++d) O[d] = 0.f;
-    for (int y = 0; y < n_split; ++y) {
-      const float ms = pp[y * (DH + 2) + DH];
-      if (ms == -INFINITY) continue;
-      const float f = __expf(ms - M);
-      L += pp[y * (DH + 2) + DH + 1] * f;
+    for (int y0 = 0; y0 < n_split; y0 += 8) {
+      float ov[8][DPL];
 #pragma unroll
-      for (int d = 0; d < DPL; ++d) O[d] += pp[y * (DH + 2) + lane * DPL + d] * f;
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int d = 0; d < DPL; ++d)
+          ov[u][d] = (y0 + u < n_split) ? pp[(y0 + u) * (DH + 2) + lane * DPL + d] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float f = (y0 + u < n_split) ? ps[wv][y0 + u] : 0.f;
+#pragma unroll
+        for (int d = 0; d < DPL; ++d) O[d] += ov[u][d] * f;
+      }
     }
+    __builtin_amdgcn_wave_barrier();
     const bool ok = row_valid[r] && L > 0.f;
 #pragma unroll
-    for (int d = 0; d < DPL; ++d) out[(size_t)r * D + h * DH + lane * DPL + d] = f2bf(ok ? O[d] / L : 0.f);
+    for (int d = 0; d < DPL; ++d)
+      out[(size_t)r * D + h * DH + lane * DPL + d] = f2bf(ok ? O[d] / L : 0.f);
   }
 }
 
 // ---------------------------------------------------------------- router
-// One block (16 waves) for all R <= 16 rows.  Prologue: y = RMSNorm(h; g)
+// One block (16 waves) per 16-row group.  Prologue: y = RMSNorm(h; g)
 // into LDS and to xout (bf16, for the experts).  Router logits by MFMA
 // (strip x K-quarter per wave), bias, float32 softmax, top-k (larger logit
 // first, equal -> lower id), k-th vs (k+1)-th gap; then the grouping of
@@ -470,20 +495,27 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   __shared__ float selw[SR_MAX * 8];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int ldl = H + XPAD, nkt = H / 32;
+  const int r0 = blockIdx.x * 16, nloc = min(16, R - r0);
+  h += (size_t)r0 * H;
+  xout += (size_t)r0 * H;
+  ridx += (size_t)r0 * topk;
+  rw += (size_t)r0 * topk;
+  if (rgap) rgap += r0;
+  if (ridx_out) ridx_out += (size_t)r0 * topk;
   // 16 waves = 4 strips x 4 K-quarters; weight tiles first
   const int strip = w >> 2, qk = w & 3, per = nkt / 4;
   const bool live = strip * 16 < E;
   uint4 a[16];
   if (live) preload<16>(Wp + (size_t)strip * nkt * 64, qk * per, per, a);
   const float bl = (bias && lane < E) ? bias[lane] : 0.f;
-  norm_rows_lds(R, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+  norm_rows_lds(nloc, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
   __syncthreads();
-  for (int e = threadIdx.x; e < R * H / 8; e += blockDim.x) {
+  for (int e = threadIdx.x; e < nloc * H / 8; e += blockDim.x) {
     const int rr = e / (H / 8), c8 = e % (H / 8);
     *(uint4*)(xout + (size_t)rr * H + c8 * 8) = *(const uint4*)(xs + rr * ldl + c8 * 8);
   }
   const int r = lane & 15;
-  const uint16_t* xrow = r < R ? xs + r * ldl : nullptr;
+  const uint16_t* xrow = r < nloc ? xs + r * ldl : nullptr;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   if (live) acc = mma_pre<16>(a, qk * per, per, xrow, acc);
   red[w * 64 + lane] = acc;
@@ -497,13 +529,14 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   __syncthreads();
   // top-k, one wave per row
   __shared__ __align__(16) float tsc[16][68];
-  if (w < R) {
+  if (w < nloc) {
     const float lv = lane < E ? lg[w][lane] + bl : -INFINITY;
     lane_topk(lv, E, topk, tsc[w], ridx + (size_t)w * topk, rw + (size_t)w * topk,
               rgap ? rgap + w : nullptr, ridx_out ? ridx_out + (size_t)w * topk : nullptr,
               sel + w * topk, selw + w * topk);
   }
   __syncthreads();
+  if (gridDim.x > 1) return;  // several row groups: k_group does the grouping
   // grouping: one thread per expert counts, one thread per entry places
   __shared__ int l_cnt[64], l_off[64];
   const int nent = R * topk;
@@ -544,9 +577,9 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
 }
 
 // ---------------------------------------------------------------- MoE gate/up
-// Block = (16-wide intermediate tile, expert y): routed expert y < E over
-// its cnt[y] entries (blocks of untouched experts exit after one load), or
-// y == E: the dense SwiGLU over all rows (the shared experts as one
+// Block = (16-wide intermediate tile, expert y, 16-entry chunk z): routed
+// expert y < E over its entries z*16.. (blocks past cnt[y] exit after one
+// load), or y == E: the dense SwiGLU over rows z*16.. (the shared experts as one
 // width-SI SwiGLU, or the draft FFN).  K split over 4 waves; weight tiles
 // are loaded first.  With g != NULL the B rows are RMSNorm(h; g) computed
 // into LDS (dense mode), else the bf16 rows xg.
@@ -564,7 +597,7 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
   extern __shared__ __align__(16) uint16_t xs[];
   __shared__ f32x4_t red[2 * 4 * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int it = blockIdx.x, e = blockIdx.y;
+  const int it = blockIdx.x, e = blockIdx.y, t0 = blockIdx.z * 16;
   const bool dense = e == E;
   const int width = dense ? SI : I;
   if (it * 16 >= width) return;
@@ -572,8 +605,8 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
   if (!dense) {
     n = cnt[e];
     o = off[e];
-    if (n == 0) return;
   }
+  if (t0 >= n) return;
   const int nkt = H / 32, per = nkt / 4, ldl = H + XPAD;
   const uint4 *G, *U;
   if (dense) {
@@ -587,12 +620,13 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
   uint4 ag_[16], au_[16];
   preload<16>(G, w * per, per, ag_);
   preload<16>(U, w * per, per, au_);
-  const int t = lane & 15;
+  const int t = t0 + (lane & 15);  // entry (routed) or row (dense)
   const uint16_t* xrow = nullptr;
   if (g) {
-    norm_rows_lds(R, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+    norm_rows_lds(min(16, n - t0), H, h + (size_t)t0 * H, nullptr, g, eps, xs, ldl, nullptr, 0,
+                  false);
     __syncthreads();
-    if (t < n) xrow = xs + t * ldl;
+    if (t < n) xrow = xs + (lane & 15) * ldl;
   } else if (t < n) {
     xrow = xg + (size_t)(dense ? t : ent_row[o + t]) * H;
   }
@@ -695,9 +729,105 @@ __global__ void __launch_bounds__(1024) k_s_down(int R, int H, int E, int I, int
   }
 }
 
+// ---------------------------------------------------------------- MoE down (slots)
+// Any batch: block = (16 output features, expert y, 16-entry chunk z), K
+// split over 4 waves.  Routed y < E: slot[(row*(k+1) + slot)][n] =
+// w * (Wd_y[n] . act_t); y == E: slot[(r*(k+1) + k)][n] = Wsd[n] . act_sh[r]
+// (the shared experts as one width-SI SwiGLU).  k_combine_norm then adds
+// the k+1 slots of each row to h in a fixed order.
+__global__ void __launch_bounds__(256) k_s_down_slot(int R, int E, int topk, int H, int I, int SI,
+                                                     const uint16_t* __restrict__ act,
+                                                     const uint16_t* __restrict__ act_sh,
+                                                     const uint4* __restrict__ edn,
+                                                     size_t e_stride,
+                                                     const uint4* __restrict__ sdn,
+                                                     const int32_t* __restrict__ cnt,
+                                                     const int32_t* __restrict__ off,
+                                                     const int32_t* __restrict__ ent_row,
+                                                     const int32_t* __restrict__ ent_slot,
+                                                     const float* __restrict__ ent_w,
+                                                     float* __restrict__ slot) {
+  __shared__ f32x4_t red[4 * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nt = blockIdx.x, e = blockIdx.y, t0 = blockIdx.z * 16;
+  const bool dense = e == E;
+  int n = R, o = 0;
+  if (!dense) {
+    n = cnt[e];
+    o = off[e];
+  }
+  if (t0 >= n) return;
+  const int K = dense ? SI : I, nkt = K / 32, per = nkt / 4;
+  const uint4* A = dense ? sdn + (size_t)nt * nkt * 64
+                         : edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
+  const int t = t0 + (lane & 15);
+  const uint16_t* xrow = nullptr;
+  int row = 0, sl = topk;
+  float wt = 1.f;
+  if (t < n) {
+    if (dense) {
+      xrow = act_sh + (size_t)t * SI;
+      row = t;
+    } else {
+      xrow = act + (size_t)(o + t) * I;
+      row = ent_row[o + t];
+      sl = ent_slot[o + t];
+      wt = ent_w[o + t];
+    }
+  }
+  f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+  acc = block_acc_sum<4>(acc, red);
+  if (w != 0 || t >= n) return;
+  float4* dst = (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
+  *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
+}
+
+// Grouping of (row, slot) pairs by expert for any number of rows: counts,
+// offsets (ascending expert id) and one entry per pair.  Entries of one
+// expert are placed through LDS atomics, so their order inside the expert
+// varies between runs; every value computed from them does not (an entry's
+// row and slot travel with it and the MFMA columns are independent).
+__global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
+                                                const int32_t* __restrict__ ridx,
+                                                const float* __restrict__ rw,
+                                                int32_t* __restrict__ cnt,
+                                                int32_t* __restrict__ off,
+                                                int32_t* __restrict__ ent_row,
+                                                int32_t* __restrict__ ent_slot,
+                                                float* __restrict__ ent_w) {
+  __shared__ int l_cnt[64], l_off[64], l_cur[64];
+  if (threadIdx.x < 64) {
+    l_cnt[threadIdx.x] = 0;
+    l_cur[threadIdx.x] = 0;
+  }
+  __syncthreads();
+  const int n = R * topk;
+  for (int x = threadIdx.x; x < n; x += blockDim.x) atomicAdd(&l_cnt[ridx[x]], 1);
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int e = threadIdx.x;
+    int o = 0;
+    for (int y = 0; y < e; ++y) o += l_cnt[y];
+    l_off[e] = o;
+    if (e < E) {
+      cnt[e] = l_cnt[e];
+      off[e] = o;
+    }
+  }
+  __syncthreads();
+  for (int x = threadIdx.x; x < n; x += blockDim.x) {
+    const int e = ridx[x];
+    const int t = l_off[e] + atomicAdd(&l_cur[e], 1);
+    ent_row[t] = x / topk;
+    ent_slot[t] = x % topk;
+    ent_w[t] = rw[x];
+  }
+}
+
 // ---------------------------------------------------------------- LM head
-// Block = 4 vocabulary strips (64 rows) x the nr <= 16 input rows X (bf16);
-// per row the best logit, its id (lowest on ties) and the second best.
+// Block = 4 vocabulary strips (64 rows) x a 16-row group (blockIdx.y) of
+// the nr input rows X (bf16); per row the best logit, its id (lowest on
+// ties) and the second best.
 __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16_t* __restrict__ X,
                                               const uint4* __restrict__ Wp,
                                               float* __restrict__ logits, size_t ldl,
@@ -708,8 +838,9 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int nkt = H / 32;
   const int nt = blockIdx.x * 4 + wv;
+  const int r0 = blockIdx.y * 16;
   const int r = lane & 15;
-  const uint16_t* xrow = r < nr ? X + (size_t)r * H : nullptr;
+  const uint16_t* xrow = r0 + r < nr ? X + (size_t)(r0 + r) * H : nullptr;
   const bool live = nt * 16 < V;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   if (live) acc = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow, acc);
@@ -720,7 +851,7 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
   for (int t = 0; t < 4; ++t) {
     const int v = v0 + t;
     const float x = (live && v < V) ? acc[t] : -INFINITY;
-    if (logits && r < nr && live && v < V) logits[(size_t)r * ldl + v] = x;
+    if (logits && r0 + r < nr && live && v < V) logits[(size_t)(r0 + r) * ldl + v] = x;
     if (x > b1) {
       b2 = b1;
       b1 = x;
@@ -747,7 +878,7 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
     bi[wv][lane] = id;
   }
   __syncthreads();
-  if (threadIdx.x < nr) {
+  if (threadIdx.x < 16 && r0 + (int)threadIdx.x < nr) {
     const int rr = threadIdx.x;
     float c1 = bv[0][rr], c2 = sv[0][rr];
     int cid = bi[0][rr];
@@ -762,7 +893,7 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
         c2 = fmaxf(c2, ob1);
       }
     }
-    const size_t o = (size_t)rr * gridDim.x + blockIdx.x;
+    const size_t o = (size_t)(r0 + rr) * gridDim.x + blockIdx.x;
     pv[o] = c1;
     pi[o] = cid;
     p2[o] = c2;

@@ -171,12 +171,8 @@ struct Model {
                 float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
                 float* margin, int32_t* route_idx, float* route_gap) {
     if constexpr (BF) {
-      if (B * C <= SR_MAX && c.top_k <= 8 && small_ok())
-        verifier_small(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
-                       logits, margin, route_idx, route_gap);
-      else
-        verifier_fast(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
-                      logits, margin, route_idx, route_gap);
+      verifier_mfma(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
+                    logits, margin, route_idx, route_gap);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -225,12 +221,8 @@ struct Model {
              int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
              size_t ldl) {
     if constexpr (BF) {
-      if (B * C <= SR_MAX && small_ok())
-        draft_small(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
-                    logits, ldl);
-      else
-        draft_fast(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
-                   logits, ldl);
+      draft_mfma(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
+                 logits, ldl);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -255,71 +247,20 @@ struct Model {
                                     ws.ustate, H, (T*)ws.xhead, H, 0);
     lm_head(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
   }
-  // ------------------------------------------------------------ bf16 fast path
-  template <int RT>
-  void mm(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
-          bool add) {
-    dim3 grid(cdiv(cdiv(N, 16), 4), cdiv(R, 16 * RT));
-    if (add)
-      k_mm<RT, true><<<grid, 256, 0, s>>>(R, N, K / 32, X, ldx_, Wp, Y, ldy);
-    else
-      k_mm<RT, false><<<grid, 256, 0, s>>>(R, N, K / 32, X, ldx_, Wp, Y, ldy);
-  }
-  void mmr(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
-           bool add) {
-    if (R <= 16) mm<1>(R, N, K, X, ldx_, Wp, Y, ldy, add);
-    else mm<4>(R, N, K, X, ldx_, Wp, Y, ldy, add);
-  }
-
-  // attention sub-layer on the fast path: xin (normed, bf16 [R][H]) ->
-  // q + K/V append -> split attention -> merge -> h += Wo o
-  void attn_fast(const Ws& ws, int B, int C, const uint4* wqkv, const uint4* wo, uint16_t* cache,
-                 size_t seq_stride) {
-    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
-    const unsigned tasks = D / 8;  // D/16 rope pairs + D/16 v strips
-    if (R <= 16)
-      k_qkv_rope<1><<<dim3(cdiv(tasks, 4), 1), 256, 0, s>>>(
-          R, C, nh, dh, H / 32, (const uint16_t*)ws.xin, wqkv, rope, ws.row_pos, ws.row_valid,
-          cache, seq_stride, c.max_ctx, ws.q);
-    else
-      k_qkv_rope<4><<<dim3(cdiv(tasks, 4), cdiv(R, 64)), 256, 0, s>>>(
-          R, C, nh, dh, H / 32, (const uint16_t*)ws.xin, wqkv, rope, ws.row_pos, ws.row_valid,
-          cache, seq_stride, c.max_ctx, ws.q);
-    if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
-    else sattn<64>(ws, B, C, cache, seq_stride);
-    mmr(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
-  }
-
-  void lm_fast(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
-               int32_t* tok, float* margin) {
-    const int V = c.vocab, H = c.hidden;
-    const unsigned nblk = cdiv(cdiv(V, 16), 4);
-    if (nr <= 16)
-      k_lm_mfma<1><<<dim3(nblk, 1), 256, 0, s>>>(nr, V, H / 32, (const uint16_t*)ws.xhead, pk.lm,
-                                                logits, ldl, ws.pv, ws.pi, ws.p2);
-    else
-      k_lm_mfma<4><<<dim3(nblk, cdiv(nr, 64)), 256, 0, s>>>(nr, V, H / 32,
-                                                            (const uint16_t*)ws.xhead, pk.lm,
-                                                            logits, ldl, ws.pv, ws.pi, ws.p2);
-    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
-                                               tok, margin);
-  }
-
-  // ------------------------------------------------------------ small-batch path
-  // shapes the small-batch kernels cover: per-wave tile counts <= 16 and
-  // whole float4 rows per lane
-  bool small_ok() const {
-    return c.hidden % 256 == 0 && c.hidden <= 2048 && c.n_routed <= 64;
-  }
+  // ------------------------------------------------------------ bf16 MFMA path
   static int nw_for(int nkt) {
     if (nkt % 16 == 0 && nkt >= 128) return 16;
     if (nkt % 8 == 0 && nkt >= 64) return 8;
     return 4;
   }
+  static unsigned groups(int R) { return (unsigned)((R + 15) / 16); }
+  static size_t lds_rows(int R, int H) { return (size_t)(R < 16 ? R : 16) * (H + XPAD) * 2; }
+
+  // Y (=|+=) X . W^T over R rows (16-row groups)
   void smm(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
            bool add) {
     const int nkt = K / 32, nw = nw_for(nkt);
-    const unsigned g = cdiv(N, 16);
+    const dim3 g(cdiv(N, 16), groups(R));
 #define MTP_SMM(NW)                                                                       \
   if (add) k_s_mm<NW, true><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);        \
   else k_s_mm<NW, false><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);
@@ -327,11 +268,24 @@ struct Model {
 #undef MTP_SMM
   }
 
+  // Key splits for one call: enough blocks to fill the chip (about 2048),
+  // splits of at least 64 positions, at most the context's n_split.
+  void splits_for(int blocks_per_split, int& ns, int& sp) const {
+    ns = (2048 + blocks_per_split - 1) / blocks_per_split;
+    const int cap64 = (c.max_ctx + 63) / 64;
+    if (ns > n_split) ns = n_split;
+    if (ns > cap64) ns = cap64;
+    if (ns < 1) ns = 1;
+    sp = ((c.max_ctx + ns - 1) / ns + 63) / 64 * 64;
+    ns = (c.max_ctx + sp - 1) / sp;
+  }
   template <int DH, int NR>
   void sattn_launch(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
     const int ng = (C + NR - 1) / NR;
-    k_s_attn<DH, NR><<<dim3(n_split, c.n_heads, B * ng), 256, 0, s>>>(
-        C, c.n_heads, n_split, spl, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
+    int ns, sp;
+    splits_for(B * ng * c.n_heads, ns, sp);
+    k_s_attn<DH, NR><<<dim3(ns, c.n_heads, B * ng), 256, 0, s>>>(
+        C, c.n_heads, ns, sp, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
         1.0f / sqrtf((float)DH), ws.part, ws.att_ctr, (uint16_t*)ws.attn);
   }
   template <int DH>
@@ -342,76 +296,95 @@ struct Model {
     else sattn_launch<DH, 8>(ws, B, C, cache, seq_stride);
   }
 
-  // pre-norm attention sub-layer: h += Wo attn(RMSNorm(h; g)), small batch
-  void attn_small(const Ws& ws, int B, int C, const float* g, const uint4* wqkv, const uint4* wo,
-                  uint16_t* cache, size_t seq_stride) {
+  // attention sub-layer: h += Wo attn(RMSNorm(h; g)).  With xg the
+  // normalised rows are already in xg (bf16) and g is unused.
+  void attn_mfma(const Ws& ws, int B, int C, const float* g, const uint16_t* xg,
+                 const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
-    const size_t lds = (size_t)R * (H + XPAD) * 2;
-    k_s_qkv<<<D / 8, 256, lds, s>>>(R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, wqkv, rope,
-                                    ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q);
+    k_s_qkv<<<dim3(D / 8, groups(R)), 256, xg ? 0 : lds_rows(R, H), s>>>(
+        R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv, rope, ws.row_pos, ws.row_valid,
+        cache, seq_stride, c.max_ctx, ws.q);
     if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
     else sattn<64>(ws, B, C, cache, seq_stride);
     smm(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
   }
 
-  // LM head over nr rows of ws.xhead (bf16, already normalised)
-  void lm_small(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
-                int32_t* tok, float* margin) {
+  // LM head over nr rows of ws.xhead (bf16, normalised), greedy argmax
+  void lm_mfma(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
+               int32_t* tok, float* margin) {
     const int V = c.vocab, H = c.hidden;
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
-    k_s_lm<<<nblk, 256, 0, s>>>(nr, V, H, (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv,
-                                ws.pi, ws.p2);
+    k_s_lm<<<dim3(nblk, groups(nr)), 256, 0, s>>>(nr, V, H, (const uint16_t*)ws.xhead, pk.lm,
+                                                 logits, ldl, ws.pv, ws.pi, ws.p2);
     k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
   }
 
-  void verifier_small(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
-                      float* hid, bool head_all, int32_t* tok, int per, int ostride,
-                      float* logits, float* margin, int32_t* route_idx, float* route_gap) {
+  void verifier_mfma(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
+                     float* hid, bool head_all, int32_t* tok, int per, int ostride,
+                     float* logits, float* margin, int32_t* route_idx, float* route_gap) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter, S = c.n_shared;
     const int SI = S * I;
     const float eps = (float)c.rms_eps;
     const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
     const size_t layer_stride = (size_t)B * seq_stride;
-    const size_t lds = (size_t)R * (H + XPAD) * 2;
+    const bool small = R <= SR_MAX;  // MoE down adds straight into h
+    const unsigned G = groups(R);
     k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok,
                                                   (const T*)w.embed, vision, vis_ld, vis_off, ws.h,
                                                   ws.status);
     for (int l = 0; l < L; ++l) {
-      attn_small(ws, B, C, w.attn_norm + (size_t)l * H, pk.wqkv + l * pk.wqkv_s,
-                 pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
-      k_s_router<<<1, 1024, lds, s>>>(
+      const uint16_t* xg = nullptr;
+      if (!small && l > 0) {  // add the previous layer's expert slots, normalise
+        k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.attn_norm + (size_t)l * H, eps,
+                                         nullptr, (uint16_t*)ws.xin);
+        xg = (const uint16_t*)ws.xin;
+      }
+      attn_mfma(ws, B, C, w.attn_norm + (size_t)l * H, xg, pk.wqkv + l * pk.wqkv_s,
+                pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
+      k_s_router<<<G, 1024, lds_rows(R, H), s>>>(
           R, H, E, k, ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin,
           pk.router + l * pk.router_s, w.router_bias ? w.router_bias + (size_t)l * E : nullptr,
           ws.ridx, ws.rw, route_gap ? route_gap + (size_t)l * R : ws.rgap,
           route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.cnt, ws.off, ws.ent_row,
           ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched);
-      k_s_gu<<<dim3(cdiv(SI > I ? SI : I, 16), E + 1), 256, 0, s>>>(
+      if (G > 1)
+        k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
+                                   ws.ent_slot, ws.ent_w);
+      k_s_gu<<<dim3(cdiv(SI > I ? SI : I, 16), E + 1, G), 256, 0, s>>>(
           R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,
           pk.exp_gu + (size_t)l * E * pk.exp_gu_s, pk.exp_gu_s, pk.sh_gu + l * pk.sh_gu_s, ws.cnt,
           ws.off, ws.ent_row, (uint16_t*)ws.act, ws.act_sh);
-      k_s_down<<<H / 16, 1024, 0, s>>>(R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh,
-                                       pk.exp_down + (size_t)l * E * pk.exp_down_s,
-                                       pk.exp_down_s, pk.sh_down + l * pk.sh_down_s, ws.cnt,
-                                       ws.off, ws.ent_row, ws.ent_w, ws.h);
+      if (small)
+        k_s_down<<<H / 16, 1024, 0, s>>>(R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh,
+                                         pk.exp_down + (size_t)l * E * pk.exp_down_s,
+                                         pk.exp_down_s, pk.sh_down + l * pk.sh_down_s, ws.cnt,
+                                         ws.off, ws.ent_row, ws.ent_w, ws.h);
+      else
+        k_s_down_slot<<<dim3(H / 16, E + 1, G), 256, 0, s>>>(
+            R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh,
+            pk.exp_down + (size_t)l * E * pk.exp_down_s, pk.exp_down_s,
+            pk.sh_down + l * pk.sh_down_s, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w,
+            ws.slot);
     }
-    k_combine_norm<<<R, 256, 0, s>>>(H, 0, nullptr, ws.h, w.final_norm, eps, hid,
+    k_combine_norm<<<R, 256, 0, s>>>(H, small ? 0 : k, small ? nullptr : ws.slot, ws.h,
+                                     w.final_norm, eps, hid,
                                      (tok && head_all) ? (uint16_t*)ws.xhead : nullptr);
     if (!tok) return;
     if (head_all) {
-      lm_small(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
+      lm_mfma(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
     } else {
       k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, nullptr, 0,
                                       (T*)ws.xhead, H, 0);
-      lm_small(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
+      lm_mfma(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
     }
   }
 
-  void draft_small(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
-                   int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride,
-                   int ooff, float* logits, size_t ldl) {
-    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+  void draft_mfma(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
+                  int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
+                  float* logits, size_t ldl) {
+    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int F = c.draft_inter;
     const float eps = (float)c.rms_eps;
     const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
@@ -420,95 +393,15 @@ struct Model {
                                                          vis_off, a, a_ld, w.d_enorm, w.d_hnorm,
                                                          eps, (T*)ws.xin, ws.status);
     smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
-    attn_small(ws, B, C, w.d_attn_norm, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
-    k_s_gu<<<dim3(F / 16, 1), 256, (size_t)R * (H + XPAD) * 2, s>>>(
+    attn_mfma(ws, B, C, w.d_attn_norm, nullptr, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
+    k_s_gu<<<dim3(F / 16, 1, groups(R)), 256, lds_rows(R, H), s>>>(
         R, H, 0, F, F, nullptr, ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr,
         nullptr, nullptr, ws.act_sh);
     smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
-    (void)D;
     if (!head) return;
     k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
                                     (T*)ws.xhead, H, 0);
-    lm_small(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
-  }
-
-  void verifier_fast(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
-                     float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
-                     float* margin, int32_t* route_idx, float* route_gap) {
-    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
-    const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter;
-    const int SI = c.n_shared * I;
-    const float eps = (float)c.rms_eps;
-    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
-    const size_t layer_stride = (size_t)B * seq_stride;
-    k_embed_norm<<<R, 256, H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok,
-                                                   (const uint16_t*)w.embed,
-                                                   (const uint16_t*)vision, vis_ld, vis_off,
-                                                   w.attn_norm, eps, ws.h, (uint16_t*)ws.xin,
-                                                   ws.status);
-    const unsigned gu_tiles = cdiv((SI > I ? SI : I) / 16, 4);
-    const unsigned chunks = cdiv(R, 64);
-    for (int l = 0; l < L; ++l) {
-      if (l > 0)
-        k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.attn_norm + (size_t)l * H, eps,
-                                         nullptr, (uint16_t*)ws.xin);
-      attn_fast(ws, B, C, pk.wqkv + l * pk.wqkv_s, pk.wo + l * pk.wo_s,
-                (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
-      k_combine_norm<<<R, 256, 0, s>>>(H, k, nullptr, ws.h, w.ffn_norm + (size_t)l * H, eps,
-                                       nullptr, (uint16_t*)ws.xin);
-      k_router<<<cdiv(R, 16), 256, 0, s>>>(
-          R, E, k, H / 32, (const uint16_t*)ws.xin, pk.router + l * pk.router_s,
-          w.router_bias ? w.router_bias + (size_t)l * E : nullptr, ws.ridx, ws.rw,
-          route_gap ? route_gap + (size_t)l * R : ws.rgap,
-          route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.counter, ws.cnt, ws.off,
-          ws.ent_row, ws.ent_slot, ws.ent_w);
-      k_moe_gu<<<dim3(gu_tiles, E + 1, chunks), 256, 0, s>>>(
-          R, E, I, SI, H / 32, (const uint16_t*)ws.xin, pk.exp_gu + (size_t)l * E * pk.exp_gu_s,
-          pk.exp_gu_s, pk.sh_gu + l * pk.sh_gu_s, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act,
-          ws.act_sh);
-      k_moe_down<<<dim3(cdiv(H / 16, 4), E + 1, chunks), 256, 0, s>>>(
-          R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh,
-          pk.exp_down + (size_t)l * E * pk.exp_down_s, pk.exp_down_s, pk.sh_down + l * pk.sh_down_s,
-          ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot);
-    }
-    k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.final_norm, eps, hid,
-                                     head_all ? (uint16_t*)ws.xhead : nullptr);
-    if (!tok) return;
-    if (head_all) {
-      lm_fast(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
-    } else {
-      k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, nullptr, 0,
-                                      (T*)ws.xhead, H, 0);
-      lm_fast(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
-    }
-  }
-
-  void draft_fast(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
-                  int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
-                  float* logits, size_t ldl) {
-    const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
-    const int F = c.draft_inter;
-    const float eps = (float)c.rms_eps;
-    const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
-    k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok,
-                                                         (const T*)w.embed, vision, vis_ld,
-                                                         vis_off, a, a_ld, w.d_enorm, w.d_hnorm,
-                                                         eps, (T*)ws.xin, ws.status);
-    mmr(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
-    k_combine_norm<<<R, 256, 0, s>>>(H, 0, nullptr, ws.h, w.d_attn_norm, eps, nullptr,
-                                     (uint16_t*)ws.xin);
-    attn_fast(ws, B, C, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
-    k_combine_norm<<<R, 256, 0, s>>>(H, 0, nullptr, ws.h, w.d_ffn_norm, eps, nullptr,
-                                     (uint16_t*)ws.xin);
-    k_moe_gu<<<dim3(cdiv(F / 16, 4), 1, cdiv(R, 64)), 256, 0, s>>>(
-        R, 0, F, F, H / 32, (const uint16_t*)ws.xin, nullptr, 0, pk.d_gu, nullptr, nullptr,
-        nullptr, nullptr, ws.act_sh);
-    mmr(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
-    (void)D;
-    if (!head) return;
-    k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
-                                    (T*)ws.xhead, H, 0);
-    lm_fast(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
+    lm_mfma(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
   }
 };
 
@@ -595,9 +488,11 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   if (c.hidden % 64 || (c.head_dim != 64 && c.head_dim != 128) || c.n_routed > 64 ||
       c.moe_inter % 4 || c.draft_inter % 4 || (c.n_heads * c.head_dim) % 64)
     return MTP_EUNSUPPORTED;
-  // bf16 MFMA path: every contraction length a multiple of 128
-  if (c.dtype == MTP_BF16 && (c.hidden % 128 || (c.n_heads * c.head_dim) % 128 ||
-                              c.moe_inter % 128 || c.draft_inter % 128))
+  // bf16 MFMA path: contraction lengths multiples of 128, whole float4 rows
+  // per lane (hidden % 256, <= 2048), top-k <= 8
+  if (c.dtype == MTP_BF16 && (c.hidden % 256 || c.hidden > 2048 ||
+                              (c.n_heads * c.head_dim) % 128 || c.moe_inter % 128 ||
+                              c.draft_inter % 128 || c.top_k > 8))
     return MTP_EUNSUPPORTED;
   if (!w->embed || (!c.tie_lm_head && !w->lm_head) || !w->final_norm || !w->attn_norm ||
       !w->ffn_norm || !w->wqkv || !w->wo || !w->router || !w->exp_gu || !w->exp_down ||

@@ -31,10 +31,22 @@ def _bf16(x):
 
 
 class Ref:
-    def __init__(self, cfg, w):
+    """f32_products=True evaluates every matrix product in float32 (BLAS
+    summation order) instead of float64; everything else is unchanged.  The
+    difference between the two measures how far a change of summation
+    order alone moves the model's outputs."""
+
+    def __init__(self, cfg, w, f32_products: bool = False):
         self.cfg = cfg
         self.w = w
         self.bf = cfg.dtype == "bf16"
+        self.f32_products = f32_products
+
+    def mm(self, a, W):
+        """a @ W.T"""
+        if self.f32_products:
+            return (np.asarray(a, np.float32) @ np.asarray(W, np.float32).T).astype(np.float64)
+        return a @ W.T
 
     def W(self, name, *idx):
         a = self.w[name]
@@ -67,7 +79,7 @@ class Ref:
         n = h.shape[0]
         nh, dh = c.n_heads, c.head_dim
         a = self.inp(self.rms(h, g))
-        qkv = _f32(a @ wqkv.T)
+        qkv = _f32(self.mm(a, wqkv))
         q = qkv[:, :nh * dh].reshape(n, nh, dh)
         k = qkv[:, nh * dh:2 * nh * dh].reshape(n, nh, dh)
         v = qkv[:, 2 * nh * dh:].reshape(n, nh, dh)
@@ -81,20 +93,20 @@ class Ref:
         p = np.exp(s)
         p /= p.sum(axis=-1, keepdims=True)
         o = self.inp(np.einsum("hij,jhd->ihd", p, v).reshape(n, nh * dh))
-        return _f32(h + _f32(o @ wo.T))
+        return _f32(h + _f32(self.mm(o, wo)))
 
     def swiglu(self, y, wg, wu, wd):
-        g = _f32(y @ wg.T)
-        u = _f32(y @ wu.T)
+        g = _f32(self.mm(y, wg))
+        u = _f32(self.mm(y, wu))
         act = self.inp(g / (1.0 + np.exp(-g)) * u)
-        return _f32(act @ wd.T)
+        return _f32(self.mm(act, wd))
 
     def moe_block(self, h, l):
         """dense evaluation of all routed experts, masked by top-k."""
         c = self.cfg
         E, k, S, I = c.n_routed, c.top_k, c.n_shared, c.moe_inter
         y = self.inp(self.rms(h, self.W("ffn_norm", l)))
-        lg = _f32(_f32(y @ self.W("router", l).T) + self.w["router_bias"][l].astype(np.float64))
+        lg = _f32(_f32(self.mm(y, self.W("router", l))) + self.w["router_bias"][l].astype(np.float64))
         z = lg - lg.max(axis=-1, keepdims=True)
         pr = _f32(np.exp(z) / np.exp(z).sum(axis=-1, keepdims=True))
         n = h.shape[0]
@@ -128,19 +140,21 @@ class Ref:
 
     def lm_logits(self, x):
         W = self.W("embed") if self.cfg.tie_lm_head else self.W("lm_head")
-        return _f32(self.inp(x) @ W.T)
+        return _f32(self.mm(self.inp(x), W))
 
     def verifier(self, tok, emb=None):
         """rows 0..n-1 at positions 0..n-1: returns b, logits, routes."""
         c = self.cfg
         h = self.embed_rows(tok, emb)
         pos = np.arange(len(tok))
-        routes = []
+        routes, router_logits = [], []
         for l in range(c.n_layers):
             h = self.attn_block(h, pos, self.W("attn_norm", l), self.W("wqkv", l), self.W("wo", l))
-            h, sel, _ = self.moe_block(h, l)
+            h, sel, lg = self.moe_block(h, l)
             routes.append(sel)
+            router_logits.append(lg)
         b = self.rms(h, self.W("final_norm"))
+        self.router_logits = np.stack(router_logits)    # [L][n][E] of the last call
         return b, self.lm_logits(b), np.stack(routes)
 
     def draft(self, next_tok, next_emb, a, pos):
@@ -150,7 +164,7 @@ class Ref:
         cat = np.concatenate([self.inp(self.rms(e, self.W("d_enorm"))),
                               self.inp(self.rms(np.asarray(a, np.float64), self.W("d_hnorm")))],
                              axis=-1)
-        z = _f32(cat @ self.W("d_eh_proj").T)
+        z = _f32(self.mm(cat, self.W("d_eh_proj")))
         z = self.attn_block(z, pos, self.W("d_attn_norm"), self.W("d_wqkv"), self.W("d_wo"))
         F = self.cfg.draft_inter
         gu = self.W("d_gu")

@@ -3,7 +3,7 @@
 The oracle runs its own draft chain and verify pass from its own state.
 Wherever the GPU chose differently, the choice must be a near-tie of the
 oracle's own scores (top-1/top-2 logit gap <= ARGMAX_TOL; router k-th vs
-(k+1)-th gap <= ROUTE_TOL) and the GPU's value must lie in the oracle's
+(k+1)-th gap <= the layer's routing tolerance, oracle.route_tolerances) and the GPU's value must lie in the oracle's
 near-tie set; the oracle then continues on the GPU's choice.  Everything
 else -- every token, m, the commit list and the cache bookkeeping -- must
 be equal, and floats must agree to the stated tolerance.
@@ -77,13 +77,27 @@ def replay_step(orc, st, K, rec, stats, tol, forced=None):
         raise Mismatch(f"verify inputs differ: gpu drafts {list(rec['drafts'])} vs {drafts}")
     toks = [st.pending] + drafts
     follow = rec.get("routes")
+    rtol_l = oracle.route_tolerances(orc.cfg)
     r = orc.verify_rows(st.kv, toks, st.kv_len + np.arange(K + 1), want_logits=True,
-                        want_routes=True, follow_route=follow)
+                        want_routes=True, follow_route=follow, route_tol=rtol_l)
     if r["route_rejected"]:
-        raise Mismatch(f"{r['route_rejected']} GPU routings are not top-k of the oracle's logits")
+        # locate the first (layer, row) where the sets differ, without follow
+        kv_copy = st.kv.copy()
+        r0 = orc.verify_rows(kv_copy, toks, st.kv_len + np.arange(K + 1), want_routes=True)
+        detail = []
+        for l in range(follow.shape[0]):
+            for i in range(follow.shape[1]):
+                a_, b_ = sorted(r0["route_idx"][l, i].tolist()), sorted(follow[l, i].tolist())
+                if a_ != b_:
+                    detail.append(f"layer {l} row {i}: oracle {a_} gap {r0['route_gap'][l, i]:.2e} "
+                                  f"gpu {b_}")
+            if detail:
+                break
+        raise Mismatch(f"{r['route_rejected']} GPU routings are not top-k of the oracle's logits; "
+                       f"first difference: {detail[:3]}")
     stats["followed_routes"] += r["route_followed"]
     if follow is not None:
-        ok = r["route_gap"] > oracle.ROUTE_TOL
+        ok = r["route_gap"] > rtol_l[:, None]
         if not np.array_equal(np.sort(r["route_idx"][ok], -1), np.sort(follow[ok], -1)):
             raise Mismatch("routing differs where the oracle's gap exceeds the tolerance")
     v = [check_token(r["logits"][i], int(r["amax"][i]), int(rec["verify"][i]), f"verify row {i}",

@@ -90,6 +90,17 @@ def test_mid_bf16_spec_decode_matches_oracle():
     _run_and_replay("mid", 2, 3, 16, 12, 14, 96, dict(gain_jitter=0.1, zipf_s=1.1))
 
 
+def test_mid_bf16_batch6_multi_group_path():
+    """24 rows per pass: two 16-row groups, MoE down through slots, the
+    separate grouping kernel."""
+    _run_and_replay("mid", 6, 3, 8, 8, 8, 96, dict(gain_jitter=0.1, zipf_s=1.1))
+
+
+def test_mid_bf16_batch17_ragged_groups():
+    """68 rows per pass: five 16-row groups, the last one ragged (4 rows)."""
+    _run_and_replay("mid", 17, 3, 4, 4, 5, 64, dict(gain_jitter=0.1), check_kv=False)
+
+
 def test_k0_is_plain_greedy_on_gpu():
     _run_and_replay("tinyb", 2, 0, 6, 6, 12, 64)
 
