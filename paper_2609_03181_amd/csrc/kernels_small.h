@@ -19,15 +19,18 @@ constexpr int SR_MAX = 16;  // rows of the small-batch path
 constexpr int XPAD = 8;     // LDS row padding (bf16 elements)
 
 // acc += tiles [t0, t1) of a packed strip against this lane's B row
-// (global or LDS).  Batches of 8 tiles, double-buffered: the loads of the
-// next batch are in flight while the current one is multiplied.
-__device__ __forceinline__ void sk_load8(const uint4* __restrict__ A, int t, int t1,
-                                         const uint16_t* xrow, int koff, uint4 (&a)[8],
-                                         uint4 (&b)[8]) {
+// (global or LDS).  Batches of BT tiles, double-buffered: the loads of the
+// next batch are in flight while the current one is multiplied.  The
+// staging costs 4*BT uint4 registers per lane: BT = 8 for 256-thread blocks,
+// 4 for 1024-thread blocks (128 VGPRs per lane at most).
+template <int BT>
+__device__ __forceinline__ void sk_load(const uint4* __restrict__ A, int t, int t1,
+                                        const uint16_t* xrow, int koff, uint4 (&a)[BT],
+                                        uint4 (&b)[BT]) {
   const int lane = threadIdx.x & 63;
   const uint4 z = make_uint4(0, 0, 0, 0);
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
+  for (int u = 0; u < BT; ++u) {
     if (t + u < t1) {
       a[u] = A[(size_t)(t + u) * 64 + lane];
       b[u] = xrow ? ldx(xrow + (t + u) * 32 + koff) : z;
@@ -35,24 +38,25 @@ __device__ __forceinline__ void sk_load8(const uint4* __restrict__ A, int t, int
   }
 }
 
+template <int BT = 8>
 __device__ __forceinline__ f32x4_t sk_range(const uint4* __restrict__ A, int t0, int t1,
                                             const uint16_t* xrow, f32x4_t acc) {
   const int koff = 8 * ((threadIdx.x & 63) >> 4);
   const uint4 z = make_uint4(0, 0, 0, 0);
-  uint4 a[8], b[8];
+  uint4 a[BT], b[BT];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) a[u] = b[u] = z;  // every staged register defined
-  if (t0 < t1) sk_load8(A, t0, t1, xrow, koff, a, b);
-  for (int t = t0; t < t1; t += 8) {
-    uint4 an[8], bn[8];
+  for (int u = 0; u < BT; ++u) a[u] = b[u] = z;  // every staged register defined
+  if (t0 < t1) sk_load<BT>(A, t0, t1, xrow, koff, a, b);
+  for (int t = t0; t < t1; t += BT) {
+    uint4 an[BT], bn[BT];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) an[u] = bn[u] = z;
-    if (t + 8 < t1) sk_load8(A, t + 8, t1, xrow, koff, an, bn);
+    for (int u = 0; u < BT; ++u) an[u] = bn[u] = z;
+    if (t + BT < t1) sk_load<BT>(A, t + BT, t1, xrow, koff, an, bn);
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < BT; ++u)
       if (t + u < t1) acc = mfma16(a[u], b[u], acc);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < BT; ++u) {
       a[u] = an[u];
       b[u] = bn[u];
     }
@@ -70,18 +74,25 @@ __device__ __forceinline__ void preload(const uint4* __restrict__ A, int t0, int
     a[u] = u < n ? A[(size_t)(t0 + u) * 64 + lane] : make_uint4(0, 0, 0, 0);
 }
 
-template <int MAXT>
+// acc += preloaded tiles a[0..n) against this lane's B row; the B operands
+// are read CH at a time (CH = MAXT: all reads issued first, for a B row in
+// global memory; a small CH saves registers when the row is in LDS)
+template <int MAXT, int CH = MAXT>
 __device__ __forceinline__ f32x4_t mma_pre(const uint4 (&a)[MAXT], int t0, int n,
                                            const uint16_t* xrow, f32x4_t acc) {
+  static_assert(MAXT % CH == 0, "chunk must divide the tile count");
   const int koff = 8 * ((threadIdx.x & 63) >> 4);
   const uint4 z = make_uint4(0, 0, 0, 0);
-  uint4 b[MAXT];
 #pragma unroll
-  for (int u = 0; u < MAXT; ++u)
-    b[u] = (u < n && xrow) ? ldx(xrow + (t0 + u) * 32 + koff) : z;
+  for (int c0 = 0; c0 < MAXT; c0 += CH) {
+    uint4 b[CH];
 #pragma unroll
-  for (int u = 0; u < MAXT; ++u)
-    if (u < n) acc = mfma16(a[u], b[u], acc);
+    for (int u = 0; u < CH; ++u)
+      b[u] = (c0 + u < n && xrow) ? ldx(xrow + (t0 + c0 + u) * 32 + koff) : z;
+#pragma unroll
+    for (int u = 0; u < CH; ++u)
+      if (c0 + u < n) acc = mfma16(a[c0 + u], b[u], acc);
+  }
   return acc;
 }
 
@@ -103,8 +114,8 @@ __device__ __forceinline__ f32x4_t block_acc_sum(f32x4_t acc, f32x4_t* red) {
 // RMSNorm of rows r < R of src (row idx[r] when idx, row stride H,
 // H % 256 == 0, H <= 2048) with gain g into LDS xs[r][ldl] (bf16);
 // optionally float32 copies to yf (row stride ldf) when write_f.  One wave
-// per row; each lane loads its (up to 8) float4 of the row and of g before
-// using any of them.
+// per row; each lane loads its (up to 8) float4 of the row before using
+// any of them (the gain is re-read per row from cache).
 __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restrict__ src,
                                               const int32_t* __restrict__ idx,
                                               const float* __restrict__ g, float eps,
@@ -112,10 +123,6 @@ __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restr
                                               int ldf, bool write_f) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int n4 = H / 256;  // float4 per lane
-  float4 gv[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u)
-    if (u < n4) gv[u] = ((const float4*)g)[u * 64 + lane];
   for (int r = w; r < R; r += nw) {
     const float4* x = (const float4*)(src + (size_t)(idx ? idx[r] : r) * H);
     float4 xv[8];
@@ -132,8 +139,9 @@ __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restr
     for (int u = 0; u < 8; ++u) {
       if (u < n4) {
         const int j = (u * 64 + lane) * 4;
-        const float y0 = xv[u].x * rinv * gv[u].x, y1 = xv[u].y * rinv * gv[u].y;
-        const float y2 = xv[u].z * rinv * gv[u].z, y3 = xv[u].w * rinv * gv[u].w;
+        const float4 gv = ((const float4*)g)[u * 64 + lane];
+        const float y0 = xv[u].x * rinv * gv.x, y1 = xv[u].y * rinv * gv.y;
+        const float y2 = xv[u].z * rinv * gv.z, y3 = xv[u].w * rinv * gv.w;
         uint2 pk;
         pk.x = (uint32_t)f2bf(y0) | ((uint32_t)f2bf(y1) << 16);
         pk.y = (uint32_t)f2bf(y2) | ((uint32_t)f2bf(y3) << 16);
@@ -159,8 +167,8 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
   const int r = blockIdx.y * 16 + (lane & 15);  // 16-row group blockIdx.y
   const uint16_t* xrow = r < R ? X + (size_t)r * ldx_ : nullptr;
   const int per = nkt / NW;
-  f32x4_t acc = sk_range(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per, xrow,
-                         f32x4_t{0.f, 0.f, 0.f, 0.f});
+  f32x4_t acc = sk_range<(NW >= 16 ? 4 : 8)>(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per,
+                                            xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
   acc = block_acc_sum<NW>(acc, red);
   if (w != 0 || r >= R) return;
   const int n = nt * 16 + 4 * (lane >> 4);
@@ -265,6 +273,22 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
 }
 
 // ---------------------------------------------------------------- attention
+// One 64-key tile of K and V into registers: 16-byte chunk c = threadIdx.x
+// + 256u is key c / (DH/8), part c % (DH/8); keys past the capacity clamp
+// to the last row (their scores are masked).
+template <int DH, int VPT>
+__device__ __forceinline__ void attn_load_tile(const uint16_t* __restrict__ Kc,
+                                               const uint16_t* __restrict__ Vc, int t0, int cap,
+                                               uint4 (&kr)[VPT], uint4 (&vr)[VPT]) {
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int c = threadIdx.x + 256 * u;
+    const int j = min(t0 + c / (DH / 8), cap - 1);
+    kr[u] = *(const uint4*)(Kc + (size_t)j * DH + (c % (DH / 8)) * 8);
+    vr[u] = *(const uint4*)(Vc + (size_t)j * DH + (c % (DH / 8)) * 8);
+  }
+}
+
 // Split-K decode attention, merge fused.  Block (split s, head h,
 // z = b*ngroups + g) covers keys [s*spl, (s+1)*spl) of sequence b for the
 // NR query rows of group g.  Per 64-key tile the block loads K and V with
@@ -297,37 +321,30 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
   const int b = blockIdx.z / ngroups, g = blockIdx.z % ngroups;
   const int i0 = g * NR, nr = min(NR, C - i0);
   const int D = nh * DH;
-  int lim[NR];
-  {
-    int rv[NR], rp[NR];
-#pragma unroll
-    for (int i = 0; i < NR; ++i) {
-      const int r = b * C + i0 + min(i, nr - 1);
-      rv[i] = row_valid[r];
-      rp[i] = row_pos[r];
-    }
-#pragma unroll
-    for (int i = 0; i < NR; ++i) lim[i] = (i < nr && rv[i]) ? rp[i] : -1;
-  }
+  // key limit of every row of the group (block-uniform, for the split
+  // range) and of the rows this wave owns (rows wv + 4x)
   int maxpos = -1;
+  int lim[RPW];
 #pragma unroll
-  for (int i = 0; i < NR; ++i) maxpos = max(maxpos, lim[i]);
+  for (int x = 0; x < RPW; ++x) lim[x] = -1;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    if (i < nr) {
+      const int r = b * C + i0 + i;
+      const int li = row_valid[r] ? row_pos[r] : -1;
+      maxpos = max(maxpos, li);
+#pragma unroll
+      for (int x = 0; x < RPW; ++x)
+        if (i == wv + 4 * x) lim[x] = li;
+    }
+  }
   const int k0 = s * spl, k1 = min(k0 + spl, maxpos + 1);
   const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
   const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
-  // first tile's loads
   uint4 kreg[VPT], vreg[VPT];
-  auto load_tile = [&](int t0) {
 #pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int c = threadIdx.x + 256 * u;  // 16-byte chunk of the tile
-      const int key = c / (DH / 8), part8 = c % (DH / 8);
-      const int j = min(t0 + key, cap - 1);
-      kreg[u] = *(const uint4*)(Kc + (size_t)j * DH + part8 * 8);
-      vreg[u] = *(const uint4*)(Vc + (size_t)j * DH + part8 * 8);
-    }
-  };
-  if (k0 < k1) load_tile(k0);
+  for (int u = 0; u < VPT; ++u) kreg[u] = vreg[u] = make_uint4(0, 0, 0, 0);
+  if (k0 < k1) attn_load_tile<DH, VPT>(Kc, Vc, k0, cap, kreg, vreg);
   for (int e = threadIdx.x; e < NR * DH; e += 256) {
     const int i = e / DH, d = e % DH;
     qs[i][d] = i < nr ? q[(size_t)(b * C + i0 + i) * D + h * DH + d] : 0.f;
@@ -350,7 +367,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
       *(uint4*)(Vs + key * DH + part8 * 8) = vreg[u];
     }
     __syncthreads();
-    if (t0 + 64 < k1) load_tile(t0 + 64);  // next tile in flight
+    if (t0 + 64 < k1) attn_load_tile<DH, VPT>(Kc, Vc, t0 + 64, cap, kreg, vreg);  // in flight
     const int j = t0 + lane;
 #pragma unroll
     for (int x = 0; x < RPW; ++x) {
@@ -369,7 +386,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
               qb.x * __uint_as_float(v.z << 16) + qb.y * __uint_as_float(v.z & 0xffff0000u) +
               qb.z * __uint_as_float(v.w << 16) + qb.w * __uint_as_float(v.w & 0xffff0000u);
       }
-      const float si = (j <= lim[i]) ? sc * scale : -INFINITY;
+      const float si = (j <= lim[x]) ? sc * scale : -INFINITY;
       const float mn = fmaxf(m[x], wave_max(si));
       const float p = (mn == -INFINITY) ? 0.f : __expf(si - mn);
       const float corr = (mn == -INFINITY) ? 1.f : __expf(m[x] - mn);
@@ -506,7 +523,7 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   const int strip = w >> 2, qk = w & 3, per = nkt / 4;
   const bool live = strip * 16 < E;
   uint4 a[16];
-  if (live) preload<16>(Wp + (size_t)strip * nkt * 64, qk * per, per, a);
+  preload<16>(Wp + (size_t)(live ? strip : 0) * nkt * 64, qk * per, live ? per : 0, a);
   const float bl = (bias && lane < E) ? bias[lane] : 0.f;
   norm_rows_lds(nloc, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
   __syncthreads();
@@ -517,7 +534,7 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   const int r = lane & 15;
   const uint16_t* xrow = r < nloc ? xs + r * ldl : nullptr;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  if (live) acc = mma_pre<16>(a, qk * per, per, xrow, acc);
+  if (live) acc = mma_pre<16, 4>(a, qk * per, per, xrow, acc);
   red[w * 64 + lane] = acc;
   __syncthreads();
   if (qk == 0 && live) {
@@ -714,7 +731,7 @@ __global__ void __launch_bounds__(1024) k_s_down(int R, int H, int E, int I, int
         row = t;
       }
     }
-    const f32x4_t a = sk_range(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    const f32x4_t a = sk_range<4>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
     if (row >= 0) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += wt * a[q];
