@@ -101,6 +101,29 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   return t;
 }
 
+// Wait for this wave's outstanding LDS operations only (lgkmcnt(0); vmcnt
+// and expcnt at their maxima, so global loads in flight keep flying).
+// Used with a wave barrier when a wave reads back LDS it has just written.
+__device__ __forceinline__ void lds_wait() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
+// Cross-workgroup publication without cache maintenance.  The L2 of one
+// XCD is not coherent with the others, and a device-scope fence
+// (__threadfence) writes back and invalidates the whole L2.  Data that one
+// workgroup hands to another inside a kernel is therefore stored and
+// loaded with agent-scope atomic accesses (write-through stores and loads
+// that do not hit stale L2 lines); vmem_release() orders those stores
+// before a following flag atomic by waiting for their completion.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void vmem_release() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+}
+
 // sticky status: the first error code wins
 __device__ __forceinline__ void set_status(int32_t* status, int32_t code) {
   atomicCAS(status, 0, code);

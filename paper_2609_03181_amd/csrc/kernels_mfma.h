@@ -56,7 +56,7 @@ __device__ __forceinline__ void lane_topk(float lv, int E, int topk, float* sc, 
   const int lane = threadIdx.x & 63;
   sc[lane] = lane < E ? lv : -INFINITY;
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_s_waitcnt(0);
+  lds_wait();
   float mx = -INFINITY;
   int rank = 0;
 #pragma unroll
@@ -95,7 +95,7 @@ __device__ __forceinline__ void lane_topk(float lv, int E, int topk, float* sc, 
   if (lane < E && rank == topk - 1) sc[64] = lv;
   if (lane < E && rank == topk) sc[65] = lv;
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_s_waitcnt(0);
+  lds_wait();
   if (lane == 0 && gap) *gap = topk < E ? sc[64] - sc[65] : 0.f;
 }
 

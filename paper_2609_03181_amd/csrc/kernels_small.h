@@ -398,7 +398,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
       // the end of the split have p = 0)
       ps[wv][lane] = p;
       __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_s_waitcnt(0);
+      lds_wait();
 #pragma unroll
       for (int j4 = 0; j4 < 16; ++j4) {
         const float4 p4 = *(const float4*)&ps[wv][4 * j4];
@@ -426,20 +426,21 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
     const int r = b * C + i0 + i;
     float* pp = part + (((size_t)r * nh + h) * n_split + s) * (DH + 2);
 #pragma unroll
-    for (int d = 0; d < DPL; ++d) pp[lane * DPL + d] = o[x][d];
+    for (int d = 0; d < DPL; ++d) st_agent(pp + lane * DPL + d, o[x][d]);
     if (lane == 0) {
-      pp[DH] = m[x];
-      pp[DH + 1] = l[x];
+      st_agent(pp + DH, m[x]);
+      st_agent(pp + DH + 1, l[x]);
     }
   }
-  __threadfence();
+  vmem_release();
   __syncthreads();
   int32_t* ctr = counters + (size_t)blockIdx.z * nh + h;
-  if (threadIdx.x == 0) last = atomicAdd(ctr, 1) == n_split - 1;
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+           n_split - 1;
   __syncthreads();
   if (!last) return;
-  __threadfence();
-  if (threadIdx.x == 0) *ctr = 0;
+  if (threadIdx.x == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // merge: wave w merges rows w, w+4.  Lane y holds split y's (m, l)
   // (n_split <= 64); the weights e^{m_y - M} go through LDS and each lane
   // then sums its dims over the splits with all loads in flight.
@@ -449,8 +450,8 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
     if (i >= nr) break;
     const int r = b * C + i0 + i;
     const float* pp = part + ((size_t)r * nh + h) * n_split * (DH + 2);
-    const float my = lane < n_split ? pp[lane * (DH + 2) + DH] : -INFINITY;
-    const float ly = lane < n_split ? pp[lane * (DH + 2) + DH + 1] : 0.f;
+    const float my = lane < n_split ? ld_agent(pp + lane * (DH + 2) + DH) : -INFINITY;
+    const float ly = lane < n_split ? ld_agent(pp + lane * (DH + 2) + DH + 1) : 0.f;
     const float M = wave_max(my);
     const float fy = (my == -INFINITY) ? 0.f : __expf(my - M);
     const float L = wave_sum(ly * fy);
@@ -465,7 +466,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
       for (int u = 0; u < 8; ++u)
 #pragma unroll
         for (int d = 0; d < DPL; ++d)
-          ov[u][d] = (y0 + u < n_split) ? pp[(y0 + u) * (DH + 2) + lane * DPL + d] : 0.f;
+          ov[u][d] = (y0 + u < n_split) ? ld_agent(pp + (y0 + u) * (DH + 2) + lane * DPL + d) : 0.f;
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const float f = (y0 + u < n_split) ? ps[wv][y0 + u] : 0.f;

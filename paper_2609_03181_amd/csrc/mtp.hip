@@ -271,7 +271,7 @@ struct Model {
   // Key splits for one call: enough blocks to fill the chip (about 2048),
   // splits of at least 64 positions, at most the context's n_split.
   void splits_for(int blocks_per_split, int& ns, int& sp) const {
-    ns = (2048 + blocks_per_split - 1) / blocks_per_split;
+    ns = (4096 + blocks_per_split - 1) / blocks_per_split;
     const int cap64 = (c.max_ctx + 63) / 64;
     if (ns > n_split) ns = n_split;
     if (ns > cap64) ns = cap64;
