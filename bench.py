@@ -64,6 +64,142 @@ def verify_bytes(cfg, B, K, kv_len, routes):
     return w + kv + emb, U
 
 
+KERNEL_CLASSES = {  # timing-hook class -> kernel name as the profiler lists it
+    1: ("decode attention", "mtp::k_s_attn"),
+    2: ("verify MoE gate/up + SwiGLU", "mtp::k_s_gu<0>"),
+    3: ("verify MoE down", "mtp::k_s_down"),
+    4: ("LM head + partial argmax", "mtp::k_s_lm"),
+    5: ("RMSNorm + QKV + RoPE + KV append", "mtp::k_s_qkv"),
+    6: ("RMSNorm + router + top-k", "mtp::k_s_router"),
+    7: ("draft FFN gate/up + SwiGLU", "mtp::k_s_gu<1>"),
+}
+
+
+def class_cost(cfg, B, K, kv_len, draft_len, routes, kc):
+    """Algorithmic HBM bytes and FLOPs of one step's launches of kernel
+    class kc (every weight each launch touches read once, activations read
+    and written once, each sequence's K/V read once per launch)."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    H, D, I, S, E, k = (cfg.hidden, cfg.n_heads * cfg.head_dim, cfg.moe_inter, cfg.n_shared,
+                        cfg.n_routed, cfg.top_k)
+    L, V, F, R = cfg.n_layers, cfg.vocab, cfg.draft_inter, B * (K + 1)
+    U = [len(np.unique(routes[l])) for l in range(L)]
+    kv = sum(int(n) for n in kv_len)
+    dl = sum(int(n) for n in draft_len)
+    if kc == 1:   # verify: L launches over kv_len + K+1 keys; draft: K launches
+        b = L * ((kv + R) * 2 * D * es + R * D * (4 + es))
+        b += K * ((dl + B * K) * 2 * D * es + B * (K + 1) * D * (4 + es))
+        f = L * (kv + R) * (K + 1) * 4 * D + K * dl * 4 * D
+        return b, f, L + K
+    if kc == 2:
+        b = sum(U) * 2 * I * H * es + L * 2 * S * I * H * es + L * R * (H + k * I + S * I) * es
+        return b, L * R * (k + S) * 2 * I * H * 2, L
+    if kc == 3:
+        b = sum(U) * I * H * es + L * S * I * H * es + L * R * ((k + S) * I * es + 2 * H * 4)
+        return b, L * R * (k + S) * I * H * 2, L
+    if kc == 4:   # verifier head on B rows (timing mode) + K draft heads on B rows
+        return (1 + K) * (V * H * es + B * H * es), (1 + K) * B * V * H * 2, 1 + K
+    if kc == 5:
+        b = (L + K) * 3 * D * H * es + L * R * (H * 4 + 2 * D * es + D * 4)
+        return b, (L * R + K * B * (K + 1)) * 3 * D * H * 2, L + K
+    if kc == 6:
+        return L * (E * H * es + R * H * (4 + es)), L * R * E * H * 2, L
+    if kc == 7:
+        return K * 2 * F * H * es, K * B * (K + 1) * 2 * F * H * 2, K
+    raise ValueError(kc)
+
+
+def src_hash():
+    """sha256 of the library sources (kernels and C-ABI)."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2609_03181_amd", "csrc")
+    h = hashlib.sha256()
+    for n in sorted(os.listdir(d)):
+        if n.endswith((".h", ".hip")):
+            h.update(open(os.path.join(d, n), "rb").read())
+    h.update(open(os.path.join(ROOT, "include", "mtp.h"), "rb").read())
+    return h.hexdigest()[:16]
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+COPY_BYTES = 1 << 30
+
+
+def _traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` measured by the FETCH_SIZE and
+    WRITE_SIZE counters (profiles/traffic.json, written by --traffic-from),
+    or None when none were taken for this workload or the library sources
+    changed since."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))[workload]
+    except (OSError, KeyError, ValueError):
+        return None
+    if t.get("src_hash") != src_hash() or t.get("kernel") != kernel:
+        return None
+    return t["bytes_per_launch"]
+
+
+def _pmc_per_dispatch(path, counter, match):
+    """Mean per-dispatch value of `counter` over dispatches whose kernel
+    name starts with `match` (rocprofv3 counter_collection.csv)."""
+    import csv
+    per = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter or not r["Kernel_Name"].startswith(match):
+            continue
+        per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    if not per:
+        raise SystemExit(f"no {counter} samples for {match} in {path}")
+    return sum(per.values()) / len(per), len(per)
+
+
+def _largest_kernel(path, counter):
+    import csv
+    best = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] == counter:
+            best[r["Kernel_Name"]] = max(best.get(r["Kernel_Name"], 0.0), float(r["Counter_Value"]))
+    return max(best, key=best.get)
+
+
+def traffic_from(workload, kernel, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+    """Record measured HBM traffic of `kernel` (per launch) for `workload`:
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) from two counter runs of
+    the bench, each scaled by what the same counter reads for a plain copy
+    of COPY_BYTES (the --copy-calibration run)."""
+    cname = _largest_kernel(copy_fetch_csv, "FETCH_SIZE")
+    cf, _ = _pmc_per_dispatch(copy_fetch_csv, "FETCH_SIZE", cname)
+    cw, _ = _pmc_per_dispatch(copy_write_csv, "WRITE_SIZE", cname)
+    sf, sw = COPY_BYTES / (cf * 1024), COPY_BYTES / (cw * 1024)
+    f, nf = _pmc_per_dispatch(fetch_csv, "FETCH_SIZE", kernel)
+    wv, nw = _pmc_per_dispatch(write_csv, "WRITE_SIZE", kernel)
+    entry = {"kernel": kernel, "src_hash": src_hash(),
+             "fetch_kib_per_dispatch": round(f, 1), "write_kib_per_dispatch": round(wv, 1),
+             "dispatches": [nf, nw], "copy_kernel": cname[:60],
+             "copy_scale": [round(sf, 4), round(sw, 4)],
+             "bytes_per_launch": int(f * 1024 * sf + wv * 1024 * sw)}
+    try:
+        d = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        d = {}
+    d[workload] = entry
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(d, fh, indent=1)
+    print(json.dumps({workload: entry}))
+
+
+def copy_calibration():
+    """A plain device copy of COPY_BYTES, three times (for scaling the
+    FETCH_SIZE / WRITE_SIZE counters)."""
+    import torch
+    a = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES}))
+
+
 def draft_bytes(cfg, B, K, draft_len, n_rows):
     es = 2 if cfg.dtype == "bf16" else 4
     H, D, F = cfg.hidden, cfg.n_heads * cfg.head_dim, cfg.draft_inter
@@ -119,7 +255,18 @@ def main():
     ap.add_argument("--workload", default="b1", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches, not a HIP graph")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--traffic-from", nargs=5, metavar=("KERNEL", "FETCH_CSV", "WRITE_CSV",
+                                                        "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="record FETCH/WRITE_SIZE traffic of KERNEL for --workload")
     args = ap.parse_args()
+    if args.traffic_from:
+        traffic_from(args.workload, *args.traffic_from)
+        return
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the decode step has no "
               "cross-GPU path in this build", file=sys.stderr)
@@ -127,7 +274,7 @@ def main():
 
     import torch
     import synth
-    from paper_2609_03181_amd import metrics
+    from paper_2609_03181_amd import _lib
     from paper_2609_03181_amd.session import Model, Session
 
     wl = WORKLOADS[args.workload]
@@ -187,19 +334,21 @@ def main():
     ms_step = 1e3 * dt / args.steps
     value = accepted / dt
 
-    # ---- per-call breakdown (eager, events on the launch stream)
+    # ---- per-call breakdown (eager, events on the launch stream) and the
+    # routing / cache state each measured step ran on
     stream = torch.cuda.current_stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)
     nb = 8
     times = {"draft": [], "verify": [], "accept+commit": []}
-    route_sets = []
-    s_rec = s
-    s_rec.route_idx = torch.zeros((cfg.n_layers, B * (K + 1), cfg.top_k), dtype=torch.int32,
-                                  device="cuda")
-    kv_lens, d_lens, n_rows = [], [], []
+    s.route_idx = torch.zeros((cfg.n_layers, B * (K + 1), cfg.top_k), dtype=torch.int32,
+                              device="cuda")
+    state = []   # (kv_len, draft_len, routes) per measured step
+
+    def snap():
+        return (s.kv_len.cpu().numpy().copy(), s.row_pos.cpu().numpy() + s.n_rows.cpu().numpy())
+
     for _ in range(nb):
-        kv_lens.append(s.kv_len.cpu().numpy().copy())
-        d_lens.append(s.row_pos.cpu().numpy() + s.n_rows.cpu().numpy())
+        kvl, dl = snap()
         e = [ev() for _ in range(4)]
         e[0].record(stream)
         s.draft()
@@ -213,13 +362,44 @@ def main():
         times["draft"].append(e[0].elapsed_time(e[1]))
         times["verify"].append(e[1].elapsed_time(e[2]))
         times["accept+commit"].append(e[2].elapsed_time(e[3]))
-        route_sets.append(s.route_idx.cpu().numpy().copy())
-    s_rec.route_idx = None
-    vb, U = zip(*[verify_bytes(cfg, B, K, kv_lens[i], route_sets[i]) for i in range(nb)])
+        state.append((kvl, dl, s.route_idx.cpu().numpy().copy()))
+    vb, U = zip(*[verify_bytes(cfg, B, K, st[0], st[2]) for st in state])
     verify_ms = float(np.median(times["verify"]))
     vbytes = float(np.mean(vb))
-    dbytes = float(np.mean([draft_bytes(cfg, B, K, d_lens[i], None) for i in range(nb)]))
-    achieved = vbytes / (verify_ms * 1e-3) / 1e9
+    dbytes = float(np.mean([draft_bytes(cfg, B, K, st[1], None) for st in state]))
+
+    # ---- launch durations of each kernel class (HIP events recorded by the
+    # library around each launch of the class, eager steps on the same
+    # stream), with the class's algorithmic bytes and FLOPs
+    kernels = {}
+    for kc, (what, kname) in KERNEL_CLASSES.items():
+        tot_ms = tot_b = tot_f = 0.0
+        n_l = 0
+        for _ in range(4):
+            kvl, dl = snap()
+            _lib.mtp_timing_start(model.ctx, kc, 4096)
+            s.step()
+            ms, n = _lib.mtp_timing_stop(model.ctx)
+            b, f, _ = class_cost(cfg, B, K, kvl, dl, s.route_idx.cpu().numpy(), kc)
+            tot_ms, tot_b, tot_f, n_l = tot_ms + ms, tot_b + b, tot_f + f, n_l + n
+        if n_l == 0:
+            continue
+        kernels[kname] = {"what": what, "launches_per_step": n_l // 4,
+                          "us_per_launch": round(1e3 * tot_ms / n_l, 2),
+                          "us_per_step": round(1e3 * tot_ms / 4, 1),
+                          "bytes_per_launch": int(tot_b / n_l),
+                          "GB_s": round(tot_b / (tot_ms * 1e-3) / 1e9, 1),
+                          "TFLOP_s": round(tot_f / (tot_ms * 1e-3) / 1e12, 2)}
+    s.route_idx = None
+    if kernels:
+        dom = max(kernels, key=lambda n: kernels[n]["us_per_step"])
+        kd = kernels[dom]
+    else:   # float32 path: no per-kernel hook; the verify pass is the unit
+        dom = "moe_verify_step (whole verify pass)"
+        kd = {"what": "verify pass", "bytes_per_launch": int(vbytes),
+              "us_per_launch": round(1e3 * verify_ms, 2),
+              "GB_s": round(vbytes / (verify_ms * 1e-3) / 1e9, 1)}
+    achieved = kd["GB_s"]
     assert s.status() == 0
 
     out = {
@@ -239,13 +419,19 @@ def main():
                    "mode": "eager" if args.eager else "hipgraph",
                    "tau": round(accepted / (args.steps * B), 4),
                    "verify_steps_per_s": round(args.steps / dt, 2)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": "moe_verify_step (whole verify pass)",
-                     "bytes_per_launch": int(vbytes), "ms_per_launch": round(verify_ms, 4),
-                     "experts_touched_per_layer": round(float(np.mean(U)), 2)},
+                     "traffic": _traffic(args.workload, dom),
+                     "kernel": dom, "what": kd["what"],
+                     "bytes_per_launch": kd["bytes_per_launch"],
+                     "us_per_launch": kd["us_per_launch"]},
+        "verify_pass": {"ms": round(verify_ms, 4), "bytes": int(vbytes),
+                        "GB_s": round(vbytes / (verify_ms * 1e-3) / 1e9, 1),
+                        "experts_touched_per_layer": round(float(np.mean(U)), 2)},
+        "kernels": kernels,
         "breakdown_ms": {k: round(float(np.median(v)), 4) for k, v in times.items()},
         "draft_bytes_per_step": int(dbytes),
+        "src_hash": src_hash(),
     }
     if not args.no_cpu_baseline:
         ctx_cpu = int(min(int(ctx[0]), 768))

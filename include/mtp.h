@@ -188,6 +188,31 @@ mtp_status mtp_bench_override_drafts(int32_t batch, int32_t k, const int32_t* ta
                                      int32_t n_steps, int32_t* step_ctr, int32_t* draft_tok,
                                      void* stream);
 
+/* Measurement only (not part of the method): per-launch timing of one
+ * kernel class.  Between mtp_timing_start and mtp_timing_stop, every
+ * launch of the class made by this context's calls is bracketed by a pair
+ * of HIP events recorded on the call's stream (at most max_launches
+ * launches; later ones are not timed).  Do not start timing while a stream
+ * is being captured into a graph.  Timed launches are made with
+ * hipExtLaunchKernelGGL, whose event pair the runtime stamps at the start
+ * and the end of the dispatch itself.  mtp_timing_stop waits for the last
+ * event and returns the summed launch durations (ms) and the number of
+ * timed launches.  The context creates and destroys the events itself.
+ * Errors: MTP_EINVAL (bad class, max_launches < 1, already started / not
+ * started), MTP_EHIP. */
+typedef enum {
+  MTP_KC_ATTN = 1,       /* decode attention, split-K with fused merge */
+  MTP_KC_MOE_GU = 2,     /* verifier MoE gate/up + SwiGLU (routed + shared) */
+  MTP_KC_MOE_DOWN = 3,   /* verifier MoE down projection */
+  MTP_KC_LM_HEAD = 4,    /* LM head partial argmax (verifier and draft) */
+  MTP_KC_QKV = 5,        /* fused RMSNorm + QKV + RoPE + K/V append */
+  MTP_KC_ROUTER = 6,     /* fused RMSNorm + router + top-k */
+  MTP_KC_DRAFT_FFN = 7   /* draft block FFN gate/up + SwiGLU */
+} mtp_kernel_class;
+mtp_status mtp_timing_start(mtp_ctx* ctx, int32_t kernel_class, int32_t max_launches);
+mtp_status mtp_timing_stop(mtp_ctx* ctx, float* total_ms /* (host) */,
+                           int32_t* n_launches /* (host) */);
+
 #ifdef __cplusplus
 }
 #endif

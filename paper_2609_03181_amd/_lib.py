@@ -17,7 +17,11 @@ STATUS_NAMES = {0: "MTP_OK", -1: "MTP_EINVAL", -2: "MTP_ECAPACITY", -3: "MTP_EHI
 # every symbol include/mtp.h declares
 EXPORTS = ("mtp_create", "mtp_destroy", "mtp_workspace_bytes", "mtp_status_read",
            "mtp_status_clear", "mtp_prefill", "mtp_draft_k", "moe_verify_step",
-           "greedy_accept", "kv_commit_rollback", "mtp_bench_override_drafts")
+           "greedy_accept", "kv_commit_rollback", "mtp_bench_override_drafts",
+           "mtp_timing_start", "mtp_timing_stop")
+
+# kernel classes of the timing hook (mtp_kernel_class)
+KC_ATTN, KC_MOE_GU, KC_MOE_DOWN, KC_LM_HEAD, KC_QKV, KC_ROUTER, KC_DRAFT_FFN = range(1, 8)
 
 
 class MtpError(RuntimeError):
@@ -70,6 +74,8 @@ def load():
         "greedy_accept": ([I32, I32, P, P, P, P, P], I32),
         "kv_commit_rollback": ([P, I32, I32, P, P, P, P, P, P, P, P, P, I32, P, P], I32),
         "mtp_bench_override_drafts": ([I32, I32, P, I32, P, P, P], I32),
+        "mtp_timing_start": ([P, I32, I32], I32),
+        "mtp_timing_stop": ([P, P, P], I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -145,3 +151,14 @@ def kv_commit_rollback(ctx, batch, k, accept_len, commit_tok, kv_len, n_rows, ro
 def mtp_bench_override_drafts(batch, k, table, n_steps, step_ctr, draft_tok, stream):
     _check("mtp_bench_override_drafts", load().mtp_bench_override_drafts(
         batch, k, table, n_steps, step_ctr, draft_tok, stream))
+
+
+def mtp_timing_start(ctx, kernel_class, max_launches):
+    _check("mtp_timing_start", load().mtp_timing_start(ctx, kernel_class, max_launches))
+
+
+def mtp_timing_stop(ctx):
+    """-> (summed launch durations in ms, number of timed launches)"""
+    ms, n = ctypes.c_float(0.0), ctypes.c_int32(0)
+    _check("mtp_timing_stop", load().mtp_timing_stop(ctx, ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)

@@ -600,7 +600,11 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
 // load), or y == E: the dense SwiGLU over rows z*16.. (the shared experts as one
 // width-SI SwiGLU, or the draft FFN).  K split over 4 waves; weight tiles
 // are loaded first.  With g != NULL the B rows are RMSNorm(h; g) computed
-// into LDS (dense mode), else the bf16 rows xg.
+// into LDS (dense mode), else the bf16 rows xg.  ROLE only names the
+// instance (so profiles separate decode from prefill launches); the draft
+// roles are the dense-only form (the draft block's FFN, launched with E = 0).
+enum { GU_VERIFY = 0, GU_DRAFT = 1, GU_PREFILL = 2, GU_DRAFT_PREFILL = 3 };
+template <int ROLE>
 __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI,
                                               const uint16_t* __restrict__ xg,
                                               const float* __restrict__ h,
@@ -616,7 +620,7 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
   __shared__ f32x4_t red[2 * 4 * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int it = blockIdx.x, e = blockIdx.y, t0 = blockIdx.z * 16;
-  const bool dense = e == E;
+  const bool dense = (ROLE & 1) || e == E;
   const int width = dense ? SI : I;
   if (it * 16 >= width) return;
   int n = R, o = 0;

@@ -1,6 +1,7 @@
 // C-ABI implementation of the MI355X FastMTP greedy speculative-decode
 // step (declarations and contracts in include/mtp.h).
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <cmath>
 #include <cstdio>
@@ -25,6 +26,14 @@ struct Packed {
   size_t wqkv_s, wo_s, router_s, exp_gu_s, exp_down_s, sh_gu_s, sh_down_s;
 };
 
+// Launch timing of one kernel class (measurement hook): launches of the
+// class go through hipExtLaunchKernelGGL with a start/stop event pair,
+// which the runtime stamps at the dispatch's start and end.
+struct Timing {
+  int kclass = 0, cap = 0, n = 0;
+  hipEvent_t* ev = nullptr;  // [2 * cap]: start, stop per launch
+};
+
 struct mtp_ctx {
   mtp_config cfg;
   mtp_weights w;
@@ -32,7 +41,21 @@ struct mtp_ctx {
   Packed pk;     // bf16 models only
   int n_split;   // attention key splits ...
   int spl;       // ... of spl positions each (multiple of 64)
+  Timing tm;
 };
+
+// Launch of kernel k on stream s; timed when its class kc is being timed.
+template <typename... KA, typename... Args>
+inline void launch_k(Timing* tm, int kc, void (*k)(KA...), dim3 grid, dim3 block, size_t shmem,
+                     hipStream_t s, Args... args) {
+  if (tm && tm->kclass == kc && tm->n < tm->cap) {
+    const int i = tm->n++;
+    hipExtLaunchKernelGGL(k, grid, block, (uint32_t)shmem, s, tm->ev[2 * i], tm->ev[2 * i + 1], 0,
+                          static_cast<KA>(args)...);
+  } else {
+    k<<<grid, block, shmem, s>>>(static_cast<KA>(args)...);
+  }
+}
 
 namespace {
 
@@ -132,6 +155,8 @@ struct Model {
   const Packed& pk;
   int n_split;
   int spl;
+  Timing* tm;
+  bool prefill = false;  // prefill calls launch the prefill-tagged kernel instances
 
   const T* wp(const void* p, size_t off_elems) const { return (const T*)p + off_elems; }
 
@@ -284,9 +309,9 @@ struct Model {
     const int ng = (C + NR - 1) / NR;
     int ns, sp;
     splits_for(B * ng * c.n_heads, ns, sp);
-    k_s_attn<DH, NR><<<dim3(ns, c.n_heads, B * ng), 256, 0, s>>>(
-        C, c.n_heads, ns, sp, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
-        1.0f / sqrtf((float)DH), ws.part, ws.att_ctr, (uint16_t*)ws.attn);
+    launch_k(tm, MTP_KC_ATTN, k_s_attn<DH, NR>, dim3(ns, c.n_heads, B * ng), dim3(256), 0, s, C,
+             c.n_heads, ns, sp, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
+             1.0f / sqrtf((float)DH), ws.part, ws.att_ctr, (uint16_t*)ws.attn);
   }
   template <int DH>
   void sattn(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
@@ -301,9 +326,9 @@ struct Model {
   void attn_mfma(const Ws& ws, int B, int C, const float* g, const uint16_t* xg,
                  const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
-    k_s_qkv<<<dim3(D / 8, groups(R)), 256, xg ? 0 : lds_rows(R, H), s>>>(
-        R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv, rope, ws.row_pos, ws.row_valid,
-        cache, seq_stride, c.max_ctx, ws.q);
+    launch_k(tm, MTP_KC_QKV, k_s_qkv, dim3(D / 8, groups(R)), dim3(256),
+             xg ? 0 : lds_rows(R, H), s, R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv,
+             rope, ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q);
     if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
     else sattn<64>(ws, B, C, cache, seq_stride);
     smm(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
@@ -314,8 +339,8 @@ struct Model {
                int32_t* tok, float* margin) {
     const int V = c.vocab, H = c.hidden;
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
-    k_s_lm<<<dim3(nblk, groups(nr)), 256, 0, s>>>(nr, V, H, (const uint16_t*)ws.xhead, pk.lm,
-                                                 logits, ldl, ws.pv, ws.pi, ws.p2);
+    launch_k(tm, MTP_KC_LM_HEAD, k_s_lm, dim3(nblk, groups(nr)), dim3(256), 0, s, nr, V, H,
+             (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
     k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
   }
@@ -343,30 +368,35 @@ struct Model {
       }
       attn_mfma(ws, B, C, w.attn_norm + (size_t)l * H, xg, pk.wqkv + l * pk.wqkv_s,
                 pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
-      k_s_router<<<G, 1024, lds_rows(R, H), s>>>(
-          R, H, E, k, ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin,
-          pk.router + l * pk.router_s, w.router_bias ? w.router_bias + (size_t)l * E : nullptr,
-          ws.ridx, ws.rw, route_gap ? route_gap + (size_t)l * R : ws.rgap,
-          route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.cnt, ws.off, ws.ent_row,
-          ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched);
+      launch_k(tm, MTP_KC_ROUTER, k_s_router, dim3(G), dim3(1024), lds_rows(R, H), s, R, H, E,
+               k, ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin,
+               pk.router + l * pk.router_s,
+               w.router_bias ? w.router_bias + (size_t)l * E : nullptr, ws.ridx, ws.rw,
+               route_gap ? route_gap + (size_t)l * R : ws.rgap,
+               route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.cnt, ws.off, ws.ent_row,
+               ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched);
       if (G > 1)
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
                                    ws.ent_slot, ws.ent_w);
-      k_s_gu<<<dim3(cdiv(SI > I ? SI : I, 16), E + 1, G), 256, 0, s>>>(
-          R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,
-          pk.exp_gu + (size_t)l * E * pk.exp_gu_s, pk.exp_gu_s, pk.sh_gu + l * pk.sh_gu_s, ws.cnt,
-          ws.off, ws.ent_row, (uint16_t*)ws.act, ws.act_sh);
+      {
+        const dim3 grid(cdiv(SI > I ? SI : I, 16), E + 1, G);
+        const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
+        const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
+        launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL> : k_s_gu<GU_VERIFY>, grid,
+                 dim3(256), 0, s, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,
+                 egu, pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act,
+                 ws.act_sh);
+      }
+      const uint4* edn = pk.exp_down + (size_t)l * E * pk.exp_down_s;
+      const uint4* sdn = pk.sh_down + l * pk.sh_down_s;
       if (small)
-        k_s_down<<<H / 16, 1024, 0, s>>>(R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh,
-                                         pk.exp_down + (size_t)l * E * pk.exp_down_s,
-                                         pk.exp_down_s, pk.sh_down + l * pk.sh_down_s, ws.cnt,
-                                         ws.off, ws.ent_row, ws.ent_w, ws.h);
+        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down, dim3(H / 16), dim3(1024), 0, s, R, H, E, I, S,
+                 (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn, ws.cnt, ws.off,
+                 ws.ent_row, ws.ent_w, ws.h);
       else
-        k_s_down_slot<<<dim3(H / 16, E + 1, G), 256, 0, s>>>(
-            R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh,
-            pk.exp_down + (size_t)l * E * pk.exp_down_s, pk.exp_down_s,
-            pk.sh_down + l * pk.sh_down_s, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w,
-            ws.slot);
+        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot, dim3(H / 16, E + 1, G), dim3(256), 0, s, R,
+                 E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn,
+                 ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot);
     }
     k_combine_norm<<<R, 256, 0, s>>>(H, small ? 0 : k, small ? nullptr : ws.slot, ws.h,
                                      w.final_norm, eps, hid,
@@ -394,9 +424,10 @@ struct Model {
                                                          eps, (T*)ws.xin, ws.status);
     smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
     attn_mfma(ws, B, C, w.d_attn_norm, nullptr, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
-    k_s_gu<<<dim3(F / 16, 1, groups(R)), 256, lds_rows(R, H), s>>>(
-        R, H, 0, F, F, nullptr, ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr,
-        nullptr, nullptr, ws.act_sh);
+    launch_k(tm, MTP_KC_DRAFT_FFN, prefill ? k_s_gu<GU_DRAFT_PREFILL> : k_s_gu<GU_DRAFT>,
+             dim3(F / 16, 1, groups(R)), dim3(256), lds_rows(R, H), s, R, H, 0, F, F, nullptr,
+             ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr, nullptr, nullptr,
+             ws.act_sh);
     smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
     if (!head) return;
     k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
@@ -542,8 +573,18 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   return MTP_OK;
 }
 
+static void timing_release(Timing& t) {
+  if (t.ev) {
+    for (int i = 0; i < 2 * t.cap; ++i)
+      if (t.ev[i]) (void)hipEventDestroy(t.ev[i]);
+    delete[] t.ev;
+  }
+  t = Timing{};
+}
+
 void mtp_destroy(mtp_ctx* ctx) {
   if (!ctx) return;
+  timing_release(ctx->tm);
   if (ctx->rope) (void)hipFree(ctx->rope);
   if (ctx->pk.base) (void)hipFree(ctx->pk.base);
   delete ctx;
@@ -590,7 +631,8 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
+    m.prefill = true;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     for (int c0 = 0; c0 < n_rows; c0 += C) {
       const int Cc = n_rows - c0 < C ? n_rows - c0 : C;
@@ -639,7 +681,7 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_draft_len<<<cdiv(batch, 256), 256, 0, s>>>(batch, n_rows, row_pos, draft_len, w.status);
@@ -682,7 +724,7 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, kv_len, 0, nullptr, c.max_ctx, w.row_pos,
@@ -729,6 +771,41 @@ mtp_status mtp_bench_override_drafts(int32_t batch, int32_t k, const int32_t* ta
   if (batch < 1 || k < 1 || !table || n_steps < 1 || !step_ctr || !draft_tok) return MTP_EINVAL;
   k_override<<<1, 256, 0, (hipStream_t)stream>>>(batch, k, table, n_steps, step_ctr, draft_tok);
   return launch_status();
+}
+
+mtp_status mtp_timing_start(mtp_ctx* ctx, int32_t kernel_class, int32_t max_launches) {
+  if (!ctx || kernel_class < MTP_KC_ATTN || kernel_class > MTP_KC_DRAFT_FFN || max_launches < 1 ||
+      ctx->tm.kclass != 0)
+    return MTP_EINVAL;
+  Timing t;
+  t.ev = new (std::nothrow) hipEvent_t[2 * (size_t)max_launches]();
+  if (!t.ev) return MTP_EHIP;
+  t.cap = max_launches;
+  for (int i = 0; i < 2 * max_launches; ++i)
+    if (hipEventCreateWithFlags(&t.ev[i], hipEventDisableSystemFence) != hipSuccess) {
+      timing_release(t);
+      return MTP_EHIP;
+    }
+  t.kclass = kernel_class;
+  ctx->tm = t;
+  return MTP_OK;
+}
+
+mtp_status mtp_timing_stop(mtp_ctx* ctx, float* total_ms, int32_t* n_launches) {
+  if (!ctx || ctx->tm.kclass == 0 || !total_ms || !n_launches) return MTP_EINVAL;
+  Timing& t = ctx->tm;
+  mtp_status st = MTP_OK;
+  double sum = 0.0;
+  if (t.n > 0 && hipEventSynchronize(t.ev[2 * t.n - 1]) != hipSuccess) st = MTP_EHIP;
+  for (int i = 0; i < t.n && st == MTP_OK; ++i) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]) != hipSuccess) st = MTP_EHIP;
+    sum += ms;
+  }
+  *total_ms = (float)sum;
+  *n_launches = t.n;
+  timing_release(t);
+  return st;
 }
 
 }  // extern "C"
