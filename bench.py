@@ -97,8 +97,8 @@ def class_cost(cfg, B, K, kv_len, draft_len, routes, kc):
     if kc == 3:
         b = sum(U) * I * H * es + L * S * I * H * es + L * R * ((k + S) * I * es + 2 * H * 4)
         return b, L * R * (k + S) * I * H * 2, L
-    if kc == 4:   # verifier head on B rows (timing mode) + K draft heads on B rows
-        return (1 + K) * (V * H * es + B * H * es), (1 + K) * B * V * H * 2, 1 + K
+    if kc == 4:   # verifier head on all R rows + K draft heads on B rows
+        return ((1 + K) * V * H * es + (R + K * B) * H * es, (R + K * B) * V * H * 2, 1 + K)
     if kc == 5:
         b = (L + K) * 3 * D * H * es + L * R * (H * 4 + 2 * D * es + D * 4)
         return b, (L * R + K * B * (K + 1)) * 3 * D * H * 2, L + K
@@ -145,7 +145,8 @@ def _pmc_per_dispatch(path, counter, match):
     import csv
     per = {}
     for r in csv.DictReader(open(path)):
-        if r["Counter_Name"] != counter or not r["Kernel_Name"].startswith(match):
+        name = r["Kernel_Name"].removeprefix("void ")
+        if r["Counter_Name"] != counter or not name.startswith(match):
             continue
         per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
     if not per:
@@ -167,12 +168,22 @@ def traffic_from(workload, kernel, fetch_csv, write_csv, copy_fetch_csv, copy_wr
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) from two counter runs of
     the bench, each scaled by what the same counter reads for a plain copy
     of COPY_BYTES (the --copy-calibration run)."""
-    cname = _largest_kernel(copy_fetch_csv, "FETCH_SIZE")
-    cf, _ = _pmc_per_dispatch(copy_fetch_csv, "FETCH_SIZE", cname)
-    cw, _ = _pmc_per_dispatch(copy_write_csv, "WRITE_SIZE", cname)
+    def num(x):
+        try:
+            return float(x)
+        except ValueError:
+            return None
+    # each source is a counter_collection.csv, or a KiB-per-dispatch value
+    # already reduced from one
+    cname = "copy" if num(copy_fetch_csv) is not None else _largest_kernel(copy_fetch_csv,
+                                                                           "FETCH_SIZE")
+    cf = num(copy_fetch_csv) or _pmc_per_dispatch(copy_fetch_csv, "FETCH_SIZE", cname)[0]
+    cw = num(copy_write_csv) or _pmc_per_dispatch(copy_write_csv, "WRITE_SIZE", cname)[0]
     sf, sw = COPY_BYTES / (cf * 1024), COPY_BYTES / (cw * 1024)
-    f, nf = _pmc_per_dispatch(fetch_csv, "FETCH_SIZE", kernel)
-    wv, nw = _pmc_per_dispatch(write_csv, "WRITE_SIZE", kernel)
+    f, nf = ((num(fetch_csv), None) if num(fetch_csv) is not None else
+             _pmc_per_dispatch(fetch_csv, "FETCH_SIZE", kernel))
+    wv, nw = ((num(write_csv), None) if num(write_csv) is not None else
+              _pmc_per_dispatch(write_csv, "WRITE_SIZE", kernel))
     entry = {"kernel": kernel, "src_hash": src_hash(),
              "fetch_kib_per_dispatch": round(f, 1), "write_kib_per_dispatch": round(wv, 1),
              "dispatches": [nf, nw], "copy_kernel": cname[:60],
