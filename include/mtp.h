@@ -128,12 +128,15 @@ mtp_status mtp_status_clear(const mtp_ctx* ctx, void* ws, void* stream);
  *   = the greedy token, out_tok[b][0] = that token, n_out = 1.
  * k is the draft depth the following steps use: hid is [B][k+1][H] f32,
  * next_tok [B][k+1]; tok is [B][n_rows]; vision [B][n_rows][H] (storage
- * dtype) or NULL when every tok >= 0; out_tok [B][max_out]. */
+ * dtype) or NULL when every tok >= 0; out_tok [B][max_out].  route_idx,
+ * when not NULL, receives the top-k experts of every row and layer,
+ * [L][B][n_rows][top_k] (for checks). */
 mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, const int32_t* tok,
                        const void* vision, void* kv_cache, void* draft_kv, int32_t* kv_len,
                        int32_t* draft_len, float* hid, int32_t* next_tok, int32_t* n_rows_out,
                        int32_t* row_pos, int32_t* pending, int32_t* out_tok, int32_t max_out,
-                       int32_t* n_out, void* ws, size_t ws_bytes, void* stream);
+                       int32_t* n_out, int32_t* route_idx, void* ws, size_t ws_bytes,
+                       void* stream);
 
 /* Draft (state-shift equation).  Depth 1 runs the catch-up rows
  * i = 0..n_rows[b]-1 at positions row_pos[b]+i, each with state

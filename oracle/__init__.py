@@ -41,11 +41,18 @@ _lib = None
 #   ROUTE_TOL_BF16  the same for bf16 models: a one-ulp flip of a stored
 #                   bf16 key or value moves every later router logit by
 #                   ~1e-4..1e-3, and a change of summation order alone
-#                   produces such flips (a float32-product evaluation of the
-#                   same model moves router logits by up to ~4e-3);
+#                   produces such flips.  Measured with float32 instead of
+#                   float64 dot products: router logits move by up to 2.8e-3
+#                   in a 2-layer model over 32 rows; over the full-shape
+#                   768-row prefix by up to 2.9e-3 in layer 0 and a median
+#                   1.3e-2 / 99th percentile 5.4e-2 in layer 11 (sequential
+#                   float32 sums, routing differences left to cascade).  The
+#                   GPU path's routings lie within 2.5e-2 of the oracle's
+#                   top-k there (oracle following them), so 5e-2 is twice
+#                   that;
 #   ARGMAX_TOL      top-1 vs top-2 token logit gap.
 ROUTE_TOL = 1e-3
-ROUTE_TOL_BF16 = 1e-2
+ROUTE_TOL_BF16 = 5e-2
 ARGMAX_TOL = 0.05
 
 
@@ -87,7 +94,7 @@ def _L():
         lib = ctypes.CDLL(_LIB_PATH)
         vp, i32, f32, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_double
         lib.orc_verify_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp,
-                                        vp, vp, vp, vp, vp, vp, vp, vp]
+                                        vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.orc_verify_rows.restype = i32
         lib.orc_draft_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.orc_draft_rows.restype = i32
@@ -96,6 +103,7 @@ def _L():
         lib.orc_attend.argtypes = [vp, vp, vp, i32, i32, vp]
         lib.orc_router.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp]
         lib.orc_moe_sublayer.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp]
+        lib.orc_set_sum32.argtypes = [i32]
         lib.orc_bf16_round.argtypes = [f32]
         lib.orc_bf16_round.restype = f32
         _lib = lib
@@ -133,7 +141,8 @@ class Oracle:
 
     # -- rows ------------------------------------------------------------
     def verify_rows(self, kv, tok, pos, emb=None, head_mask=None, want_logits=False,
-                    want_routes=False, follow_route=None, route_tol=None):
+                    want_routes=False, follow_route=None, route_tol=None,
+                    want_router_logits=False):
         """route_tol: per-layer follow tolerance (default route_tolerances)."""
         c = self.cfg
         tok = _c(tok, np.int32)
@@ -150,6 +159,8 @@ class Oracle:
             ri = np.empty((c.n_layers, n, c.top_k), np.int32)
             rw = np.empty((c.n_layers, n, c.top_k), np.float32)
             rg = np.empty((c.n_layers, n), np.float32)
+        rl = (np.empty((c.n_layers, n, c.n_routed), np.float32) if want_router_logits
+              else None)
         fr = _c(follow_route, np.int32)
         rt = np.ascontiguousarray(np.broadcast_to(
             route_tolerances(c) if route_tol is None else np.asarray(route_tol, np.float32),
@@ -158,11 +169,11 @@ class Oracle:
         rc = _L().orc_verify_rows(ctypes.byref(self.dims), ctypes.byref(self.wts), _p(kv),
                                   kv.shape[3], n, _p(tok), _p(emb), _p(pos), _p(fr), _p(rt),
                                   ctypes.byref(nf), _p(b), _p(hm), _p(logits), _p(amax),
-                                  _p(margin), _p(ri), _p(rw), _p(rg))
+                                  _p(margin), _p(ri), _p(rw), _p(rg), _p(rl))
         if rc < 0:
             raise ValueError("oracle: position outside the KV capacity")
         return dict(b=b, amax=amax, margin=margin, logits=logits, route_idx=ri, route_w=rw,
-                    route_gap=rg, route_rejected=rc, route_followed=nf.value)
+                    route_gap=rg, route_rejected=rc, route_followed=nf.value, router_logits=rl)
 
     def draft_rows(self, dkv, tok, a, pos, emb=None, head_mask=None, want_logits=False):
         c = self.cfg
@@ -229,6 +240,13 @@ def attend(q, K, V):
     return o
 
 
+def set_sum32(on: bool) -> None:
+    """Sensitivity measurement only: weight dot products in float32
+    (sequential) instead of float64 while on.  Reference values are always
+    computed with it off."""
+    _L().orc_set_sum32(int(bool(on)))
+
+
 def bf16_round(x: float) -> float:
     return float(_L().orc_bf16_round(float(x)))
 
@@ -270,16 +288,21 @@ class SeqState:
     out: list               # generated tokens
     max_new: int = 1 << 30
     last_logits: np.ndarray | None = None   # logits of the last prefill row
+    prefill_routes_followed: int = 0        # near-tie routes adopted from follow_route
+    prefill_routes_rejected: int = 0        # given routes that were not near-ties
 
     @property
     def finished(self) -> bool:
         return len(self.out) >= self.max_new
 
 
-def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30) -> SeqState:
+def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30,
+            follow_route=None) -> SeqState:
     """Verifier over the prefix (vision rows then text tokens), greedy token
     of the last row, and the draft prefill: rows p = 0..P-2 in base form
-    (state b_p, input row p+1 -- a vision row inside the visual prefix)."""
+    (state b_p, input row p+1 -- a vision row inside the visual prefix).
+    follow_route [L][P][k]: routes chosen elsewhere, adopted where they are
+    near-ties of the oracle's own (see Oracle.verify_rows)."""
     c = orc.cfg
     nv = 0 if vision is None else len(vision)
     tokens = np.asarray(tokens, dtype=np.int32)
@@ -291,14 +314,17 @@ def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30) -> Se
     kv, dkv = orc.new_kv(cap), orc.new_dkv(cap)
     hm = np.zeros(P, np.uint8)
     hm[P - 1] = 1
-    r = orc.verify_rows(kv, tok, np.arange(P), emb=emb, head_mask=hm, want_logits=True)
+    r = orc.verify_rows(kv, tok, np.arange(P), emb=emb, head_mask=hm, want_logits=True,
+                        want_routes=follow_route is not None, follow_route=follow_route)
     pending = int(r["amax"][P - 1])
     if P >= 2:
         orc.draft_rows(dkv, tok[1:], r["b"][:P - 1], np.arange(P - 1), emb=emb[1:])
     return SeqState(kv=kv, dkv=dkv, kv_len=P, pending=pending, hid=r["b"][P - 1:P].copy(),
                     next_tok=np.array([pending], np.int32), n_rows=1, row_pos=P - 1,
                     draft_len=P - 1, out=[pending], max_new=max_new,
-                    last_logits=r["logits"][P - 1].copy())
+                    last_logits=r["logits"][P - 1].copy(),
+                    prefill_routes_followed=r["route_followed"],
+                    prefill_routes_rejected=r["route_rejected"])
 
 
 def draft_chain(orc: Oracle, st: SeqState, K: int):

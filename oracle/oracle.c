@@ -93,9 +93,23 @@ static inline const void* woff(const orc_dims* d, const void* base, size_t elems
   return (const char*)base + elems * wsize(d);
 }
 
+/* Sensitivity-measurement switch (never set for reference values): when
+ * nonzero, weight dot products accumulate in float32 (sequentially) instead
+ * of float64, a different but equally valid summation that shows how far
+ * rounding alone moves the outputs. */
+static int g_sum32 = 0;
+void orc_set_sum32(int on) { g_sum32 = on; }
+
+static double wdot32(const orc_dims* d, const void* w, const float* x, int n) {
+  float s = 0.f;
+  for (int k = 0; k < n; ++k) s += wload(d, w, (size_t)k) * x[k];
+  return s;
+}
+
 /* dot product of weight row w[0..n) with float vector x, in float64
  * with four interleaved partial sums combined in a fixed order. */
 static double wdot(const orc_dims* d, const void* w, const float* x, int n) {
+  if (g_sum32) return wdot32(d, w, x, n);
   double s0 = 0, s1 = 0, s2 = 0, s3 = 0;
   int k = 0;
   if (d->bf16) {
@@ -335,7 +349,7 @@ static int follow_route(const orc_dims* d, const float* logits, int32_t* topk,
  * with y_r = RMSNorm(h[r]; ffn_norm).  Routing outputs are optional. */
 static int moe_sublayer(const orc_dims* d, const orc_weights* w, int layer, int nr, float* h,
                         const int32_t* follow, float tol, int* n_followed, int32_t* route_idx,
-                        float* route_w, float* route_gap) {
+                        float* route_w, float* route_gap, float* router_logits) {
   const int H = d->hidden, E = d->n_routed, k = d->top_k, S = d->n_shared, I = d->moe_inter;
   int bad = 0;
   float* y = (float*)malloc(sizeof(float) * (size_t)nr * H);
@@ -352,6 +366,7 @@ static int moe_sublayer(const orc_dims* d, const orc_weights* w, int layer, int 
     orc_router(d, w, layer, y + (size_t)r * H, lg, pr + (size_t)r * E, sel + (size_t)r * k, &gap);
     if (follow) bad += follow_route(d, lg, sel + (size_t)r * k, follow + (size_t)r * k, tol, n_followed);
     if (route_gap) route_gap[r] = gap;
+    if (router_logits) memcpy(router_logits + (size_t)r * E, lg, sizeof(float) * (size_t)E);
   }
   free(lg);
   /* delta[r] accumulates the FFN output of row r in float64 */
@@ -453,7 +468,7 @@ static void input_row(const orc_dims* d, const orc_weights* w, int32_t tok, cons
  * below pos[r] must already hold K/V (earlier rows of the call count).
  * Outputs (each optional): b = final-norm state [nr][H]; LM-head results
  * for rows with head_mask set; routing per layer [L][nr][k]; k-th vs
- * (k+1)-th router-logit gap [L][nr].  follow_route [L][nr][k] makes the
+ * (k+1)-th router-logit gap [L][nr]; router logits [L][nr][E].  follow_route [L][nr][k] makes the
  * oracle adopt externally chosen near-tie routes (see follow_route), with
  * tolerance route_tol[l] in layer l.
  * Returns the number of rejected route sets (0 without follow_route), or
@@ -462,7 +477,8 @@ int orc_verify_rows(const orc_dims* d, const orc_weights* w, float* kv, int cap,
                     const int32_t* tok, const void* emb, const int32_t* pos,
                     const int32_t* follow_route, const float* route_tol, int* n_followed,
                     float* b_out, const uint8_t* head_mask, float* logits, int32_t* amax,
-                    float* margin, int32_t* route_idx, float* route_w, float* route_gap) {
+                    float* margin, int32_t* route_idx, float* route_w, float* route_gap,
+                    float* router_logits) {
   const int H = d->hidden, L = d->n_layers, nh = d->n_heads, dh = d->head_dim, k = d->top_k;
   for (int r = 0; r < nr; ++r)
     if (pos[r] < 0 || pos[r] >= cap) return -1;
@@ -478,7 +494,8 @@ int orc_verify_rows(const orc_dims* d, const orc_weights* w, float* kv, int cap,
                         follow_route ? route_tol[l] : 0.f, n_followed,
                         route_idx ? route_idx + (size_t)l * nr * k : NULL,
                         route_w ? route_w + (size_t)l * nr * k : NULL,
-                        route_gap ? route_gap + (size_t)l * nr : NULL);
+                        route_gap ? route_gap + (size_t)l * nr : NULL,
+                        router_logits ? router_logits + (size_t)l * nr * d->n_routed : NULL);
   }
   float* b = (float*)malloc(sizeof(float) * (size_t)nr * H);
   for (int r = 0; r < nr; ++r)
@@ -545,5 +562,5 @@ void orc_moe_sublayer(const orc_dims* d, const orc_weights* w, int layer, int nr
                       const float* h_in, float* h_out, int32_t* route_idx, float* route_w,
                       float* route_gap) {
   memcpy(h_out, h_in, sizeof(float) * (size_t)nr * d->hidden);
-  moe_sublayer(d, w, layer, nr, h_out, NULL, 0.0f, NULL, route_idx, route_w, route_gap);
+  moe_sublayer(d, w, layer, nr, h_out, NULL, 0.0f, NULL, route_idx, route_w, route_gap, NULL);
 }

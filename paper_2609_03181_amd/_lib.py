@@ -67,8 +67,8 @@ def load():
         "mtp_workspace_bytes": ([P, I32, I32], SZ),
         "mtp_status_read": ([P, P, P], I32),
         "mtp_status_clear": ([P, P, P], I32),
-        "mtp_prefill": ([P, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, P, SZ, P],
-                        I32),
+        "mtp_prefill": ([P, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, P, P, SZ,
+                         P], I32),
         "mtp_draft_k": ([P, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "moe_verify_step": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "greedy_accept": ([I32, I32, P, P, P, P, P], I32),
@@ -115,11 +115,11 @@ def mtp_status_clear(ctx: int, ws: int, stream: int) -> None:
 
 
 def mtp_prefill(ctx, batch, k, n_rows, tok, vision, kv_cache, draft_kv, kv_len, draft_len, hid,
-                next_tok, n_rows_out, row_pos, pending, out_tok, max_out, n_out, ws, ws_bytes,
-                stream):
+                next_tok, n_rows_out, row_pos, pending, out_tok, max_out, n_out, route_idx, ws,
+                ws_bytes, stream):
     _check("mtp_prefill", load().mtp_prefill(
         ctx, batch, k, n_rows, tok, vision, kv_cache, draft_kv, kv_len, draft_len, hid, next_tok,
-        n_rows_out, row_pos, pending, out_tok, max_out, n_out, ws, ws_bytes, stream))
+        n_rows_out, row_pos, pending, out_tok, max_out, n_out, route_idx, ws, ws_bytes, stream))
 
 
 def mtp_draft_k(ctx, batch, k, hid, next_tok, n_rows, row_pos, draft_kv, draft_len, draft_tok,

@@ -109,4 +109,18 @@ __global__ void k_copy_rows(int B, int H, const int32_t* __restrict__ idx,
   for (int j = threadIdx.x; j < H; j += blockDim.x) dst[(size_t)b * dst_ld + j] = s[j];
 }
 
+// routes of one prefill chunk (stage [L][B*C][k], row b*C+i) into the
+// prefill layout out [L][B][n_rows][k] at rows c0+i
+__global__ void k_scatter_routes(int L, int B, int C, int k, int n_rows, int c0,
+                                 const int32_t* __restrict__ stage, int32_t* __restrict__ out) {
+  const size_t n = (size_t)L * B * C * k;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (size_t)gridDim.x * blockDim.x) {
+    const int t = (int)(e % k);
+    const size_t r = e / k;
+    const int i = (int)(r % C), b = (int)((r / C) % B), l = (int)(r / ((size_t)C * B));
+    out[(((size_t)l * B + b) * n_rows + c0 + i) * k + t] = stage[e];
+  }
+}
+
 }  // namespace mtp

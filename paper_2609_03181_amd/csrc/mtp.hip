@@ -69,7 +69,7 @@ struct Ws {
   int32_t* counter;  // self-resetting grid counter (router grouping)
   int32_t *row_pos, *row_valid, *row_tok, *head_row, *tok_stage, *chain_pos;
   float *h, *bbuf, *qkv, *q, *rw, *rgap, *gu, *ustate, *pv, *p2, *margin_stage;
-  int32_t *ridx, *pi;
+  int32_t *ridx, *pi, *route_stage;
   void *xin, *attn, *act, *xhead;
   // bf16 fast path
   float *part, *slot, *ent_w;
@@ -114,6 +114,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
   w.pi = (int32_t*)take(R * nblk * 4);
   w.p2 = (float*)take(R * nblk * 4);
   w.margin_stage = (float*)take(R * 4);
+  w.route_stage = (int32_t*)take(R * k * (size_t)c.n_layers * 4);
   w.xin = take(R * 2 * H * es);
   w.attn = take(R * D * es);
   size_t act_cols = (size_t)(k + 1) * SI;
@@ -611,7 +612,8 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
                        const void* vision, void* kv_cache, void* draft_kv, int32_t* kv_len,
                        int32_t* draft_len, float* hid, int32_t* next_tok, int32_t* n_rows_out,
                        int32_t* row_pos, int32_t* pending, int32_t* out_tok, int32_t max_out,
-                       int32_t* n_out, void* ws, size_t ws_bytes, void* stream) {
+                       int32_t* n_out, int32_t* route_idx, void* ws, size_t ws_bytes,
+                       void* stream) {
   if (!ctx) return MTP_EINVAL;
   const mtp_config& c = ctx->cfg;
   if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k || n_rows < 1 ||
@@ -642,7 +644,13 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
                                                  w.row_pos, w.row_valid, w.head_row, w.status);
       k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, tok, n_rows, c0, w.row_tok);
       m.verifier(w, batch, Cc, (const T*)vision, n_rows, c0, (T*)kv_cache, w.bbuf, false,
-                 last ? w.tok_stage : nullptr, 1, 1, nullptr, nullptr, nullptr, nullptr);
+                 last ? w.tok_stage : nullptr, 1, 1, nullptr, nullptr,
+                 route_idx ? w.route_stage : nullptr, nullptr);
+      if (route_idx) {
+        const size_t n = (size_t)c.n_layers * R * c.top_k;
+        k_scatter_routes<<<cdiv(n, 256) < 1024 ? cdiv(n, 256) : 1024, 256, 0, s>>>(
+            c.n_layers, batch, Cc, c.top_k, n_rows, c0, w.route_stage, route_idx);
+      }
       if (last)
         k_copy_rows<<<batch, 256, 0, s>>>(batch, c.hidden, w.head_row, w.bbuf, hid,
                                           (size_t)(k + 1) * c.hidden);

@@ -118,10 +118,15 @@ class Session:
         tok = tok.to(self.m.device, torch.int32).contiguous()
         if vision is not None:
             vision = vision.to(self.m.device).contiguous()
+        c = self.m.cfg
+        # record mode keeps the prefill's routing ([L][B][P][k]) for checks
+        self.prefill_routes = (torch.zeros((c.n_layers, B, P, c.top_k), dtype=torch.int32,
+                                           device=self.m.device) if self.record else None)
         _lib.mtp_prefill(self.m.ctx, B, self.K, P, _p(tok), _p(vision), _p(self.kv), _p(self.dkv),
                          _p(self.kv_len), _p(self.draft_len), _p(self.hid), _p(self.next_tok),
                          _p(self.n_rows), _p(self.row_pos), _p(self.pending), _p(self.out_tok),
-                         self.max_out, _p(self.n_out), _p(self.ws), self.ws_bytes, self.stream)
+                         self.max_out, _p(self.n_out), _p(self.prefill_routes), _p(self.ws),
+                         self.ws_bytes, self.stream)
 
     def set_forced_drafts(self, table: torch.Tensor):
         """Benchmark timing mode: table [n_steps][B][K] of draft tokens that

@@ -50,9 +50,16 @@ def gpu_prefill(model, B, K, tok, vis, max_out, record=True, prefill_rows=0):
     return s
 
 
-def oracle_prefill(orc, cfg, tok_b, vis_b, cap, max_new):
+def oracle_prefill(orc, cfg, tok_b, vis_b, cap, max_new, routes=None):
+    """The oracle's prefill of one sequence; routes [L][P][k] (the GPU's
+    prefill routing, Session.prefill_routes[:, b]) are followed at the
+    oracle's near-ties, and any other difference fails."""
     nv = int((tok_b < 0).sum())
-    return oracle.prefill(orc, cap, vis_b[:nv] if nv else None, tok_b[nv:], max_new=max_new)
+    st = oracle.prefill(orc, cap, vis_b[:nv] if nv else None, tok_b[nv:], max_new=max_new,
+                        follow_route=routes)
+    assert st.prefill_routes_rejected == 0, (
+        f"{st.prefill_routes_rejected} prefill routings are not near-ties of the oracle's")
+    return st
 
 
 def step_records(s: Session):
@@ -83,3 +90,53 @@ def step_records(s: Session):
 
 def finished(s: Session) -> bool:
     return bool((s.n_out >= s.max_new).all().item())
+
+
+def synthetic_context(cfg, B, ctx, seqs):
+    """Synthetic cached context (the batch-16/64 recipe): verifier and draft
+    K/V N(0,1) in the storage dtype (seed 15), last-commit states b N(0,1)
+    (seed 15, stream 72), pending tokens uniform (seed 15, stream 73).  Only
+    the sequences in `seqs` get K/V values (the others keep zero caches of
+    the same lengths).  Returns kv {b: [L][2][nh][ctx][dh]}, dkv {b: ...},
+    hid [B][H], pending [B]."""
+    kv, dkv = {}, {}
+    for b in seqs:
+        n = int(ctx[b])
+        kv[b] = np.stack([np.stack([synth.kv_values(cfg, l, b, c, n, 15, 70) for c in range(2)])
+                          for l in range(cfg.n_layers)])
+        dkv[b] = np.stack([synth.kv_values(cfg, 0, b, c, n - 1, 15, 71) for c in range(2)])
+    hid = synth.normal(15, 72, (B, cfg.hidden))
+    pend = synth.uniform_int(15, 73, B, 0, cfg.vocab)
+    return kv, dkv, hid, pend
+
+
+def load_synthetic(s: Session, cfg, ctx, kv, dkv, hid, pend):
+    """Put a synthetic_context into a GPU session (state after a commit of
+    one row at ctx-1)."""
+    for b, a in kv.items():
+        s.kv[:, b, :, :, :a.shape[3]] = to_dev_storage(a)
+    for b, a in dkv.items():
+        s.dkv[b, :, :, :a.shape[2]] = to_dev_storage(a)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    ctx = np.asarray(ctx, np.int32)
+    s.kv_len.copy_(t(ctx))
+    s.row_pos.copy_(t(ctx - 1))
+    s.draft_len.copy_(t(ctx - 1))
+    s.n_rows.fill_(1)
+    s.pending.copy_(t(pend))
+    s.next_tok[:, 0] = t(pend)
+    s.hid[:, 0] = torch.from_numpy(np.ascontiguousarray(hid, np.float32)).cuda()
+    s.n_out.fill_(0)
+
+
+def oracle_synthetic_state(orc, cfg, b, ctx_b, cap, kv, dkv, hid, pend):
+    """The oracle's state for sequence b of a synthetic_context."""
+    f = (lambda a: synth.bf16_bits_to_f32(a)) if cfg.dtype == "bf16" else (lambda a: a)
+    okv, odkv = orc.new_kv(cap), orc.new_dkv(cap)
+    okv[:, :, :, :ctx_b] = f(kv[b])
+    odkv[:, :, :ctx_b - 1] = f(dkv[b])
+    p = int(pend[b])
+    return oracle.SeqState(kv=okv, dkv=odkv, kv_len=ctx_b, pending=p,
+                           hid=np.ascontiguousarray(hid[b:b + 1], np.float32),
+                           next_tok=np.array([p], np.int32), n_rows=1, row_pos=ctx_b - 1,
+                           draft_len=ctx_b - 1, out=[p])

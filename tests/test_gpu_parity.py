@@ -42,7 +42,9 @@ def _run_and_replay(name, B, K, n_vis, n_txt, max_out, cap, wkw=None, check_kv=T
     log(f"[{name}] prefill B={B} P={n_vis + n_txt} K={K}")
     s = gpu_prefill(model, B, K, tok, vis, max_out)
     assert s.status() == 0
-    sts = [oracle_prefill(orc, cfg, tok[b], vis[b], cap, max_out) for b in range(B)]
+    pr = s.prefill_routes.cpu().numpy()
+    sts = [oracle_prefill(orc, cfg, tok[b], vis[b], cap, max_out, routes=pr[:, b])
+           for b in range(B)]
     hid0 = s.hid.cpu().numpy()
     for b in range(B):
         t = replay.check_token(sts[b].last_logits, sts[b].pending, int(s.pending[b]),
