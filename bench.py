@@ -44,6 +44,10 @@ WORKLOADS = {
     # tiny fp32 case
     "tiny": dict(model="tiny", B=1, K=3, n_vis=64, n_txt=16, synthetic=False, forced=False,
                  zipf=0.0),
+    # page loop: 32 pages (256 vision rows + 32 prompt tokens), 2048 new
+    # tokens each; timed: prefill + graph-replayed steps until every page is done
+    "pages": dict(model="full", B=32, K=3, n_vis=256, n_txt=32, synthetic=False, forced=False,
+                  zipf=0.0, new=2048),
 }
 
 
@@ -227,7 +231,7 @@ def cpu_baseline(cfg, w, K, ctx_len, budget_s=20.0):
     import oracle
     import synth
     orc = oracle.Oracle(cfg, w)
-    cap = ctx_len + 64 * (K + 1) + 8
+    cap = ctx_len + 1024 * (K + 1) + 8
     kv, dkv = orc.new_kv(cap), orc.new_dkv(cap)
     for l in range(cfg.n_layers):
         for c in range(2):
@@ -241,12 +245,13 @@ def cpu_baseline(cfg, w, K, ctx_len, budget_s=20.0):
                          draft_len=ctx_len - 1, out=[pend])
     t0 = time.perf_counter()
     steps = toks = 0
-    while time.perf_counter() - t0 < budget_s and steps < 64:
+    while time.perf_counter() - t0 < budget_s and steps < 1024:
         info = oracle.spec_step(orc, st, K)
         steps += 1
         toks += info["m"] + 1
     dt = time.perf_counter() - t0
-    return dict(value=toks / dt, unit="accepted tokens/s", cores=os.cpu_count(), kind="oracle",
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    return dict(value=toks / dt, unit="accepted tokens/s", cores=threads, kind="oracle",
                 sample=f"{steps} speculative steps (K={K}, B=1) of the same model from a "
                        f"synthetic {ctx_len}-position cache, {dt:.1f} s, "
                        f"OMP threads={os.environ.get('OMP_NUM_THREADS', 'all')}, "
@@ -296,6 +301,7 @@ def main():
     w = synth.make_weights(cfg, 0, 1, zipf_s=wl["zipf"])
     log(f"weights {time.time() - t0:.1f}s")
 
+    pages = "new" in wl
     if wl["synthetic"]:
         lo, hi, seed = wl["ctx"]
         ctx = synth.context_lengths(B, lo, hi, seed)
@@ -303,8 +309,8 @@ def main():
     else:
         P = wl["n_vis"] + wl["n_txt"]
         ctx = np.full(B, P, np.int32)
-        max_ctx = P + total_steps * (K + 1) + 8
-    max_out = total_steps * (K + 1) + 4
+        max_ctx = P + (wl["new"] + 4 * (K + 1) if pages else total_steps * (K + 1)) + 8
+    max_out = wl["new"] if pages else total_steps * (K + 1) + 4
     model = Model(cfg, w, B, max_ctx, K)
     s = Session(model, B, K, max_out, prefill_rows=64)
     log(f"upload {time.time() - t0:.1f}s")
@@ -312,11 +318,14 @@ def main():
     if wl["synthetic"]:
         _load_synthetic(s, cfg, ctx)
     else:
-        tok = np.full((B, P), -1, np.int32)
-        vis = np.zeros((B, P, cfg.hidden), cfg.wdtype)
-        for b in range(B):
-            vis[b, :wl["n_vis"]] = synth.vision_prefix(cfg, wl["n_vis"], seed=10 + b)
-            tok[b, wl["n_vis"]:] = synth.text_tokens(cfg, wl["n_txt"], seed=11 + b)
+        if pages:
+            tok, vis = synth.page_inputs(cfg, B, wl["n_vis"], wl["n_txt"])
+        else:
+            tok = np.full((B, P), -1, np.int32)
+            vis = np.zeros((B, P, cfg.hidden), cfg.wdtype)
+            for b in range(B):
+                vis[b, :wl["n_vis"]] = synth.vision_prefix(cfg, wl["n_vis"], seed=10 + b)
+                tok[b, wl["n_vis"]:] = synth.text_tokens(cfg, wl["n_txt"], seed=11 + b)
         vv = torch.from_numpy(vis.view(np.int16) if cfg.dtype == "bf16" else vis)
         torch.cuda.synchronize()
         tp = time.perf_counter()
@@ -334,16 +343,36 @@ def main():
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
-    n0 = s.n_out.clone()
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        run()
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t_start
-    accepted = int((s.n_out - n0).sum().item())
-    ms_step = 1e3 * dt / args.steps
-    value = accepted / dt
+    if pages:
+        # the whole page job: prefill, then steps until every page has its
+        # tokens (checked every 64 steps; finished pages stay frozen)
+        t_start = time.perf_counter()
+        s.prefill(torch.from_numpy(tok), vv)
+        n_steps = 0
+        while True:
+            for _ in range(64):
+                run()
+            n_steps += 64
+            if bool((s.n_out >= wl["new"]).all().item()):
+                break
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t_start
+        accepted = int(s.n_out.sum().item())
+        args.steps = n_steps
+        ms_step = 1e3 * dt / n_steps
+        value = accepted / dt
+        n0 = None
+    else:
+        n0 = s.n_out.clone()
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        for _ in range(args.steps):
+            run()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t_start
+        accepted = int((s.n_out - n0).sum().item())
+        ms_step = 1e3 * dt / args.steps
+        value = accepted / dt
 
     # ---- per-call breakdown (eager, events on the launch stream) and the
     # routing / cache state each measured step ran on
@@ -444,7 +473,12 @@ def main():
         "draft_bytes_per_step": int(dbytes),
         "src_hash": src_hash(),
     }
-    if not args.no_cpu_baseline:
+    if pages:
+        out["config"]["pages_per_s"] = round(B / dt, 4)
+        out["config"]["new_tokens_per_page"] = wl["new"]
+        out["config"]["job_s"] = round(dt, 3)
+        out["config"]["tau"] = None   # finished pages stay frozen while others finish
+    if not args.no_cpu_baseline and not pages:
         ctx_cpu = int(min(int(ctx[0]), 768))
         out["cpu_baseline"] = cpu_baseline(cfg, w, K, ctx_cpu)
     print(json.dumps(out), flush=True)
@@ -458,6 +492,9 @@ def _wl_name(name, wl):
         return "full shape, batch 16, cached ctx U{1024..2048}, forced acceptance 0.2/0.2/0.25/0.35"
     if name == "b64":
         return "full shape, batch 64, cached ctx U{512..4096}, Zipf(1.1) router bias"
+    if name == "pages":
+        return ("full shape, page loop: 32 pages x (256 vision rows + 32 prompt tokens), "
+                "2048 new tokens per page, K=3; timed = prefill + steps until all pages finish")
     return "tiny fp32 case (2 layers, d=256, 8 experts top-2, V=4096), K=3, batch 1"
 
 

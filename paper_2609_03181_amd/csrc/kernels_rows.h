@@ -11,8 +11,12 @@ namespace mtp {
 __global__ void k_rows_setup(int B, int C, const int32_t* __restrict__ pos0, int off,
                              const int32_t* __restrict__ nvalid, int cap,
                              int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
-                             int32_t* __restrict__ head_row, int32_t* __restrict__ status) {
+                             int32_t* __restrict__ head_row, int32_t* __restrict__ status,
+                             int32_t* __restrict__ zero = nullptr, int n_zero = 0) {
   int r = blockIdx.x * blockDim.x + threadIdx.x;
+  // counters that later kernels of the call expect at zero (the workspace
+  // is carved differently by calls with other row counts)
+  for (int z = r; z < n_zero; z += gridDim.x * blockDim.x) zero[z] = 0;
   if (r >= B * C) return;
   int b = r / C, i = r - b * C;
   int p = (pos0 ? pos0[b] : 0) + off + i;

@@ -75,6 +75,7 @@ struct Ws {
   float *part, *slot, *ent_w;
   int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr;
   uint16_t* act_sh;
+  int n_ctr;  // entries of att_ctr (zeroed at the start of each call)
   size_t bytes;
 };
 
@@ -92,7 +93,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     off += align_up(bytes);
     return r;
   };
-  Ws w;
+  Ws w{};
   w.status = (int32_t*)take(128);
   w.counter = (int32_t*)take(128);
   w.row_pos = (int32_t*)take(R * 4);
@@ -133,6 +134,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.touched = (int32_t*)take((size_t)c.n_routed * 4);
     w.n_touched = (int32_t*)take(4);
     w.att_ctr = (int32_t*)take(R * c.n_heads * 4);
+    w.n_ctr = (int)(R * c.n_heads);
     const size_t shw = (size_t)(SI > c.draft_inter ? SI : c.draft_inter);
     w.act_sh = (uint16_t*)take(R * shw * 2);
   } else {
@@ -641,7 +643,8 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
       const int R = batch * Cc;
       const bool last = c0 + Cc == n_rows;
       k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, nullptr, c0, nullptr, c.max_ctx,
-                                                 w.row_pos, w.row_valid, w.head_row, w.status);
+                                                 w.row_pos, w.row_valid, w.head_row, w.status,
+                                                 w.att_ctr, w.n_ctr);
       k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, tok, n_rows, c0, w.row_tok);
       m.verifier(w, batch, Cc, (const T*)vision, n_rows, c0, (T*)kv_cache, w.bbuf, false,
                  last ? w.tok_stage : nullptr, 1, 1, nullptr, nullptr,
@@ -695,7 +698,8 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
     k_draft_len<<<cdiv(batch, 256), 256, 0, s>>>(batch, n_rows, row_pos, draft_len, w.status);
     // depth 1 over the catch-up rows; the last valid row starts the chain
     k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, 0, n_rows, c.max_ctx, w.row_pos,
-                                               w.row_valid, w.head_row, w.status);
+                                               w.row_valid, w.head_row, w.status, w.att_ctr,
+                                               w.n_ctr);
     k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, C, next_tok, C, 0, w.row_tok);
     m.draft(w, batch, C, hid, (size_t)C * H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k, 0,
             draft_logits, (size_t)k * V);
@@ -736,7 +740,8 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, kv_len, 0, nullptr, c.max_ctx, w.row_pos,
-                                               w.row_valid, nullptr, w.status);
+                                               w.row_valid, nullptr, w.status, w.att_ctr,
+                                               w.n_ctr);
     k_row_tokens_verify<<<cdiv(R, 256), 256, 0, s>>>(batch, k, pending, draft_tok, w.row_tok);
     m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
                margin, route_idx, route_gap);

@@ -241,6 +241,21 @@ def text_tokens(cfg: ModelCfg, n: int, seed: int = 11, stream: int = 61) -> np.n
     return uniform_int(seed, stream, n, 0, cfg.vocab)
 
 
+def page_inputs(cfg: ModelCfg, pages: int, n_vis: int = 256, n_txt: int = 32):
+    """The page-loop prefixes: page q is n_vis vision rows N(0,1) (seed
+    20+q) followed by the same n_txt prompt tokens (seed 21).  Returns tok
+    [pages][P] int32 (-1 = vision row) and vision [pages][P][H] (model
+    dtype, zero at prompt rows)."""
+    P = n_vis + n_txt
+    tok = np.full((pages, P), -1, np.int32)
+    vis = np.zeros((pages, P, cfg.hidden), cfg.wdtype)
+    prompt = text_tokens(cfg, n_txt, seed=21)
+    for q in range(pages):
+        vis[q, :n_vis] = vision_prefix(cfg, n_vis, seed=20 + q)
+        tok[q, n_vis:] = prompt
+    return tok, vis
+
+
 def context_lengths(b: int, lo: int, hi: int, seed: int) -> np.ndarray:
     """b lengths uniform over the integers lo..hi inclusive."""
     return uniform_int(seed, 62, b, lo, hi - lo + 1)

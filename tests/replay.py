@@ -119,3 +119,23 @@ def replay_step(orc, st, K, rec, stats, tol, forced=None, state_tol=None):
 
 def new_stats():
     return dict(steps=0, followed_tokens=0, followed_routes=0)
+
+
+def teacher_forced_check(orc, tok_prefix, vis_prefix, gen, stats):
+    """One causal oracle pass over the prefix and the generated tokens (the
+    tokens the GPU produced are fed back in); the greedy token of the row
+    before each generated token must be that token, or a near-tie of it
+    (reading of several correct results).  Returns the number checked."""
+    c = orc.cfg
+    P, n = len(tok_prefix), len(gen)
+    toks = np.concatenate([np.asarray(tok_prefix, np.int32), np.asarray(gen[:-1], np.int32)])
+    emb = np.zeros((P + n - 1, c.hidden), c.wdtype)
+    emb[:P] = vis_prefix
+    hm = np.zeros(P + n - 1, np.uint8)
+    hm[P - 1:] = 1
+    kv = orc.new_kv(P + n)
+    r = orc.verify_rows(kv, toks, np.arange(P + n - 1), emb=emb, head_mask=hm, want_logits=True)
+    for i in range(n):
+        check_token(r["logits"][P - 1 + i], int(r["amax"][P - 1 + i]), int(gen[i]),
+                    f"generated token {i}", stats)
+    return n

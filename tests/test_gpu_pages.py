@@ -1,0 +1,64 @@
+"""The page loop at the full model shape: 32 synthetic pages (256 vision
+rows N(0,1), seed 20+page, and the same 32 prompt tokens, seed 21), greedy
+speculative decoding with K=3 to 2048 new tokens per page, the whole step
+captured once in a HIP graph and replayed.  Pages 0-3 are checked token for
+token against the oracle's greedy decode by a teacher-forced causal pass
+over the GPU's tokens (near-ties followed).  The check covers the first
+MTP_PAGES_CHECK_TOKENS tokens of each page (default 256; 2048 checks all of
+them, about a minute of CPU per page)."""
+import os
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2609_03181_amd.session import Model, Session
+from tests import replay
+from tests.gpu_util import log, to_dev_storage
+import torch
+
+pytestmark = pytest.mark.gpu
+
+PAGES, N_VIS, N_TXT, N_NEW, K = 32, 256, 32, 2048, 3
+
+
+def run_pages(model, tok, vis):
+    s = Session(model, PAGES, K, N_NEW, prefill_rows=64)
+    s.prefill(torch.from_numpy(tok), to_dev_storage(vis))
+    s.capture()
+    steps = 0
+    while True:
+        for _ in range(64):
+            s.replay()
+        steps += 64
+        if bool((s.n_out >= N_NEW).all().item()):
+            break
+        assert steps < 4 * N_NEW
+    assert s.status() == 0
+    return s, steps
+
+
+def test_page_loop_matches_oracle_greedy_decode():
+    cfg = synth.FULL
+    n_check = int(os.environ.get("MTP_PAGES_CHECK_TOKENS", "256"))
+    log(f"[pages] weights; {PAGES} pages x {N_NEW} new tokens, checking {n_check} on pages 0-3")
+    w = synth.make_weights(cfg, 0, 1)
+    tok, vis = synth.page_inputs(cfg, PAGES, N_VIS, N_TXT)
+    model = Model(cfg, w, PAGES, N_VIS + N_TXT + N_NEW + 4 * (K + 1) + 8, K)
+    try:
+        t0 = time.time()
+        s, steps = run_pages(model, tok, vis)
+        outs = s.outputs()
+        log(f"[pages] {steps} graph steps in {time.time() - t0:.1f} s")
+        assert all(len(o) == N_NEW for o in outs)
+        orc = oracle.Oracle(cfg, w)
+        stats = replay.new_stats()
+        for q in range(4):
+            t1 = time.time()
+            n = replay.teacher_forced_check(orc, tok[q], vis[q], np.array(outs[q][:n_check]),
+                                            stats)
+            log(f"[pages] page {q}: {n} tokens match ({time.time() - t1:.1f} s), {stats}")
+    finally:
+        model.close()

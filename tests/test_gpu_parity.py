@@ -289,3 +289,25 @@ def test_host_argument_errors():
         _lib.moe_verify_step(model.ctx, 2, 3, s.pending.data_ptr(), s.draft_tok.data_ptr(),
                              s.kv_len.data_ptr(), s.kv.data_ptr(), s.verify_tok.data_ptr(),
                              s.hid.data_ptr(), None, None, None, None, s.ws.data_ptr(), 1024, 0)
+
+
+def test_steps_after_prefill_do_not_depend_on_workspace_history():
+    """The workspace is carved per call by its row count; a step after a
+    prefill with larger chunks (other carve) must equal one after a prefill
+    with the step's own row count, bit for bit (regression: attention
+    split counters left non-zero by a differently carved call)."""
+    cfg, w, model, orc = build_pair("mid", 1, 96, 3, gain_jitter=0.1)
+    tok, _ = prefix_inputs(cfg, 1, 0, 40)
+    res = []
+    for rows in (4, 8, 16):
+        s = Session(model, 1, 3, 16, prefill_rows=rows, record=True)
+        s.prefill(torch.from_numpy(tok))
+        for _ in range(2):
+            s.step()
+        torch.cuda.synchronize()
+        res.append((s.draft_logits.cpu().numpy().copy(), s.logits.cpu().numpy().copy(),
+                    s.outputs()))
+    for r in res[1:]:
+        assert np.array_equal(r[0], res[0][0])
+        assert np.array_equal(r[1], res[0][1])
+        assert r[2] == res[0][2]
