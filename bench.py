@@ -70,12 +70,12 @@ def verify_bytes(cfg, B, K, kv_len, routes):
 
 KERNEL_CLASSES = {  # timing-hook class -> kernel name as the profiler lists it
     1: ("decode attention", "mtp::k_s_attn"),
-    2: ("verify MoE gate/up + SwiGLU", "mtp::k_s_gu<0>"),
+    2: ("verify MoE gate/up + SwiGLU", "mtp::k_s_gu<0,"),
     3: ("verify MoE down", "mtp::k_s_down"),
     4: ("LM head + partial argmax", "mtp::k_s_lm"),
     5: ("RMSNorm + QKV + RoPE + KV append", "mtp::k_s_qkv"),
     6: ("RMSNorm + router + top-k", "mtp::k_s_router"),
-    7: ("draft FFN gate/up + SwiGLU", "mtp::k_s_gu<1>"),
+    7: ("draft FFN gate/up + SwiGLU", "mtp::k_s_gu<1,"),
 }
 
 

@@ -96,6 +96,37 @@ __device__ __forceinline__ f32x4_t mma_pre(const uint4 (&a)[MAXT], int t0, int n
   return acc;
 }
 
+// two preloaded strips against the same B row (one B read per tile)
+template <int MAXT, int CH = MAXT>
+__device__ __forceinline__ void mma_pre2(const uint4 (&a1)[MAXT], const uint4 (&a2)[MAXT], int t0,
+                                         int n, const uint16_t* xrow, f32x4_t& c1, f32x4_t& c2) {
+  static_assert(MAXT % CH == 0, "chunk must divide the tile count");
+  const int koff = 8 * ((threadIdx.x & 63) >> 4);
+  const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int c0 = 0; c0 < MAXT; c0 += CH) {
+    uint4 b[CH];
+#pragma unroll
+    for (int u = 0; u < CH; ++u)
+      b[u] = (c0 + u < n && xrow) ? ldx(xrow + (t0 + c0 + u) * 32 + koff) : z;
+#pragma unroll
+    for (int u = 0; u < CH; ++u)
+      if (c0 + u < n) {
+        c1 = mfma16(a1[c0 + u], b[u], c1);
+        c2 = mfma16(a2[c0 + u], b[u], c2);
+      }
+  }
+}
+
+// tiles per wave (K / 32 / 4 waves) -> register array size
+#define MTP_MAXT_DISPATCH(per, F)      \
+  do {                                 \
+    if ((per) <= 4) { F(4); }          \
+    else if ((per) <= 8) { F(8); }     \
+    else if ((per) <= 10) { F(10); }   \
+    else { F(16); }                    \
+  } while (0)
+
 // sum of the NW per-wave accumulators in wave order; the result is valid
 // in wave 0.  red holds NW*64 f32x4.
 template <int NW>
@@ -189,6 +220,7 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
 // block computes x = RMSNorm(h; g) of its rows into LDS (the prologue
 // overlaps the weight fetch) -- or, with xg, reads normalised bf16 rows.
 // q -> q_out (float32), k/v -> cache at the row position.
+template <int MAXT>
 __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int dh,
                                                const float* __restrict__ h,
                                                const float* __restrict__ g, float eps,
@@ -218,9 +250,9 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
     ta = 2 * D / 16 + (task - n_pair);
     tb = ta;
   }
-  uint4 a0[16], a1[16];
-  preload<16>(Wp + (size_t)ta * nkt * 64, w * per, per, a0);
-  if (pair) preload<16>(Wp + (size_t)tb * nkt * 64, w * per, per, a1);
+  uint4 a0[MAXT], a1[MAXT];
+  preload<MAXT>(Wp + (size_t)ta * nkt * 64, w * per, per, a0);
+  preload<MAXT>(Wp + (size_t)tb * nkt * 64, w * per, pair ? per : 0, a1);
   // row bookkeeping loads, independent of everything above
   const int r0 = blockIdx.y * 16;
   const int nloc = min(16, R - r0);
@@ -236,10 +268,11 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
     if (r < R) xrow = xs + (lane & 15) * ldl;
   }
   const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  f32x4_t c0 = mma_pre<16>(a0, w * per, per, xrow, z4);
+  f32x4_t c0 = z4, c1 = z4;
+  if (pair) mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(a0, a1, w * per, per, xrow, c0, c1);
+  else c0 = mma_pre<MAXT>(a0, w * per, per, xrow, z4);
   c0 = block_acc_sum<4>(c0, red);
   if (pair) {
-    f32x4_t c1 = mma_pre<16>(a1, w * per, per, xrow, z4);
     c1 = block_acc_sum<4>(c1, red + 4 * 64);
     if (w != 0 || r >= R) return;
     const int p = valid ? pos : 0;
@@ -555,42 +588,43 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   }
   __syncthreads();
   if (gridDim.x > 1) return;  // several row groups: k_group does the grouping
-  // grouping: one thread per expert counts, one thread per entry places
-  __shared__ int l_cnt[64], l_off[64];
+  // grouping (rows <= 16, each row picks an expert at most once): a row
+  // mask per expert (LDS atomics), then one wave derives counts, offsets
+  // (prefix sum) and the touched list (ballot); an entry's place within its
+  // expert is the number of earlier rows in the expert's mask, so entries
+  // are ordered by row.
+  __shared__ uint32_t l_mask[64];
+  __shared__ int l_off[64];
   const int nent = R * topk;
-  if (threadIdx.x < 64) {
-    const int e = threadIdx.x;
-    int c = 0;
-#pragma unroll 8
-    for (int x = 0; x < nent; ++x) c += sel[x] == e;
-    l_cnt[e] = e < E ? c : 0;
-  }
+  if (threadIdx.x < 64) l_mask[threadIdx.x] = 0u;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int e = threadIdx.x;
-    int o = 0;
-    for (int x = 0; x < e; ++x) o += l_cnt[x];
-    if (e < E) {
-      cnt[e] = l_cnt[e];
-      off[e] = o;
+  if (threadIdx.x < nent) atomicOr(&l_mask[sel[threadIdx.x]], 1u << (threadIdx.x / topk));
+  __syncthreads();
+  if (w == 0) {
+    const int c = lane < E ? __popc(l_mask[lane]) : 0;
+    int pre = c;  // inclusive scan over the 64 experts
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(pre, d, MTP_WAVE);
+      if (lane >= d) pre += v;
     }
-    l_off[e] = o;
+    const int o = pre - c;
+    l_off[lane] = o;
+    if (lane < E) {
+      cnt[lane] = c;
+      off[lane] = o;
+    }
+    const uint64_t has = __ballot(c > 0);
+    if (c > 0) touched[__popcll(has & ((1ull << lane) - 1ull))] = lane;
+    if (lane == 0) *n_touched = __popcll(has);
   }
   __syncthreads();
   if (threadIdx.x < nent) {
-    const int x = threadIdx.x, e = sel[x];
-    int before = 0;
-    for (int y = 0; y < x; ++y) before += sel[y] == e;
-    const int t = l_off[e] + before;
-    ent_row[t] = x / topk;
+    const int x = threadIdx.x, e = sel[x], r = x / topk;
+    const int t = l_off[e] + __popc(l_mask[e] & ((1u << r) - 1u));
+    ent_row[t] = r;
     ent_slot[t] = x % topk;
     ent_w[t] = selw[x];
-  }
-  if (threadIdx.x == 0) {  // touched-expert list (ascending id)
-    int n = 0;
-    for (int e = 0; e < E; ++e)
-      if (l_cnt[e] > 0) touched[n++] = e;
-    *n_touched = n;
   }
 }
 
@@ -604,7 +638,7 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
 // instance (so profiles separate decode from prefill launches); the draft
 // roles are the dense-only form (the draft block's FFN, launched with E = 0).
 enum { GU_VERIFY = 0, GU_DRAFT = 1, GU_PREFILL = 2, GU_DRAFT_PREFILL = 3 };
-template <int ROLE>
+template <int ROLE, int MAXT>
 __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI,
                                               const uint16_t* __restrict__ xg,
                                               const float* __restrict__ h,
@@ -639,9 +673,9 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
     G = base + (size_t)it * nkt * 64;
     U = base + (size_t)(I / 16 + it) * nkt * 64;
   }
-  uint4 ag_[16], au_[16];
-  preload<16>(G, w * per, per, ag_);
-  preload<16>(U, w * per, per, au_);
+  uint4 ag_[MAXT], au_[MAXT];
+  preload<MAXT>(G, w * per, per, ag_);
+  preload<MAXT>(U, w * per, per, au_);
   const int t = t0 + (lane & 15);  // entry (routed) or row (dense)
   const uint16_t* xrow = nullptr;
   if (g) {
@@ -653,8 +687,8 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
     xrow = xg + (size_t)(dense ? t : ent_row[o + t]) * H;
   }
   const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  f32x4_t cg = mma_pre<16>(ag_, w * per, per, xrow, z4);
-  f32x4_t cu = mma_pre<16>(au_, w * per, per, xrow, z4);
+  f32x4_t cg = z4, cu = z4;
+  mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
   cg = block_acc_sum<4>(cg, red);
   cu = block_acc_sum<4>(cu, red + 4 * 64);
   if (w != 0 || t >= n) return;
@@ -747,6 +781,99 @@ __global__ void __launch_bounds__(1024) k_s_down(int R, int H, int E, int I, int
   if (rr < R) {
     float sum = 0.f;
     for (int x = 0; x < NW; ++x) sum += acc_l[x][rr][f];
+    h[(size_t)rr * H + nt * 16 + f] += sum;
+  }
+}
+
+// Same product spread over NG blocks per strip (grid (H/16, NG), 4 waves
+// each): virtual expert v goes to wave slot v % (4*NG).  Each block stores
+// its wave-ordered partial [R][16] (write-through); the last block of the
+// strip adds the NG partials to h in block order, so the summation order is
+// fixed.  ctr[H/16] must be zero at launch (it is left at zero).
+template <int NG>
+__global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I, int S,
+                                                      const uint16_t* __restrict__ act,
+                                                      const uint16_t* __restrict__ act_sh,
+                                                      const uint4* __restrict__ edn,
+                                                      size_t e_stride,
+                                                      const uint4* __restrict__ sdn,
+                                                      const int32_t* __restrict__ cnt,
+                                                      const int32_t* __restrict__ off,
+                                                      const int32_t* __restrict__ ent_row,
+                                                      const float* __restrict__ ent_w,
+                                                      float* __restrict__ part,
+                                                      int32_t* __restrict__ ctr,
+                                                      float* __restrict__ h) {
+  __shared__ float acc_l[4][SR_MAX][17];
+  __shared__ int l_cnt[64], l_off[64], l_list[64], l_n, last;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nt = blockIdx.x, gq = blockIdx.y;
+  if (threadIdx.x < 64) {
+    const int e = threadIdx.x;
+    l_cnt[e] = e < E ? cnt[e] : 0;
+    l_off[e] = e < E ? off[e] : 0;
+  }
+  for (int e = threadIdx.x; e < 4 * SR_MAX * 17; e += blockDim.x) (&acc_l[0][0][0])[e] = 0.f;
+  __syncthreads();
+  if (w == 0) {  // compact list of touched experts, ascending id
+    const int has = l_cnt[lane] > 0;
+    int pre = has;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(pre, d, MTP_WAVE);
+      if (lane >= d) pre += v;
+    }
+    if (has) l_list[pre - 1] = lane;
+    if (lane == 63) l_n = pre;
+  }
+  __syncthreads();
+  const int n_routed = l_n, nvirt = n_routed + S;
+  const int nkt = I / 32;
+  const int t = lane & 15;
+  for (int v = gq * 4 + w; v < nvirt; v += NG * 4) {
+    const uint4* A;
+    const uint16_t* xrow = nullptr;
+    int row = -1;
+    float wt = 1.f;
+    if (v < n_routed) {
+      const int e = l_list[v];
+      const int n = l_cnt[e], o = l_off[e];
+      A = edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
+      if (t < n) {
+        xrow = act + (size_t)(o + t) * I;
+        row = ent_row[o + t];
+        wt = ent_w[o + t];
+      }
+    } else {
+      const int sx = v - n_routed;
+      A = sdn + (size_t)nt * S * nkt * 64 + (size_t)sx * nkt * 64;
+      if (t < R) {
+        xrow = act_sh + (size_t)t * S * I + (size_t)sx * I;
+        row = t;
+      }
+    }
+    const f32x4_t a = sk_range<8>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    if (row >= 0) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += wt * a[q];
+    }
+  }
+  __syncthreads();
+  const int rr = threadIdx.x >> 4, f = threadIdx.x & 15;
+  float* pp = part + ((size_t)gq * R + rr) * H + nt * 16 + f;
+  if (rr < R) st_agent(pp, ((acc_l[0][rr][f] + acc_l[1][rr][f]) + acc_l[2][rr][f]) + acc_l[3][rr][f]);
+  vmem_release();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(ctr + nt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+           NG - 1;
+  __syncthreads();
+  if (!last) return;
+  if (threadIdx.x == 0) __hip_atomic_store(ctr + nt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (rr < R) {
+    float sum = 0.f;
+#pragma unroll
+    for (int x = 0; x < NG; ++x) sum += ld_agent(part + ((size_t)x * R + rr) * H + nt * 16 + f);
     h[(size_t)rr * H + nt * 16 + f] += sum;
   }
 }

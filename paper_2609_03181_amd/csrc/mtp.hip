@@ -60,6 +60,7 @@ inline void launch_k(Timing* tm, int kc, void (*k)(KA...), dim3 grid, dim3 block
 namespace {
 
 constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
+constexpr int kDownSplit = 4;  // blocks per output strip of the small-batch MoE down
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -73,7 +74,8 @@ struct Ws {
   void *xin, *attn, *act, *xhead;
   // bf16 fast path
   float *part, *slot, *ent_w;
-  int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr;
+  int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr, *dn_ctr;
+  float* dn_part;  // MoE down split partials [kDownSplit][R][H] (R <= 16)
   uint16_t* act_sh;
   int n_ctr;  // entries of att_ctr (zeroed at the start of each call)
   size_t bytes;
@@ -133,8 +135,11 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.ent_slot = (int32_t*)take(R * k * 4);
     w.touched = (int32_t*)take((size_t)c.n_routed * 4);
     w.n_touched = (int32_t*)take(4);
-    w.att_ctr = (int32_t*)take(R * c.n_heads * 4);
-    w.n_ctr = (int)(R * c.n_heads);
+    // attention split counters then MoE-down strip counters, one region
+    w.att_ctr = (int32_t*)take((R * c.n_heads + (size_t)H / 16) * 4);
+    w.dn_ctr = w.att_ctr + R * c.n_heads;
+    w.n_ctr = (int)(R * c.n_heads + H / 16);
+    w.dn_part = (float*)take((size_t)kDownSplit * (R < 16 ? R : 16) * H * 4);
     const size_t shw = (size_t)(SI > c.draft_inter ? SI : c.draft_inter);
     w.act_sh = (uint16_t*)take(R * shw * 2);
   } else {
@@ -329,9 +334,12 @@ struct Model {
   void attn_mfma(const Ws& ws, int B, int C, const float* g, const uint16_t* xg,
                  const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
-    launch_k(tm, MTP_KC_QKV, k_s_qkv, dim3(D / 8, groups(R)), dim3(256),
-             xg ? 0 : lds_rows(R, H), s, R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv,
-             rope, ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q);
+#define MTP_QKV(M)                                                                          \
+  launch_k(tm, MTP_KC_QKV, k_s_qkv<M>, dim3(D / 8, groups(R)), dim3(256),                   \
+           xg ? 0 : lds_rows(R, H), s, R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv, \
+           rope, ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q)
+    MTP_MAXT_DISPATCH(H / 128, MTP_QKV);
+#undef MTP_QKV
     if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
     else sattn<64>(ws, B, C, cache, seq_stride);
     smm(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
@@ -385,17 +393,20 @@ struct Model {
         const dim3 grid(cdiv(SI > I ? SI : I, 16), E + 1, G);
         const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
         const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
-        launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL> : k_s_gu<GU_VERIFY>, grid,
-                 dim3(256), 0, s, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,
-                 egu, pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act,
-                 ws.act_sh);
+#define MTP_GU(M)                                                                             \
+  launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL, M> : k_s_gu<GU_VERIFY, M>, grid,    \
+           dim3(256), 0, s, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps, egu, \
+           pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act, ws.act_sh)
+        MTP_MAXT_DISPATCH(H / 128, MTP_GU);
+#undef MTP_GU
       }
       const uint4* edn = pk.exp_down + (size_t)l * E * pk.exp_down_s;
       const uint4* sdn = pk.sh_down + l * pk.sh_down_s;
       if (small)
-        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down, dim3(H / 16), dim3(1024), 0, s, R, H, E, I, S,
-                 (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn, ws.cnt, ws.off,
-                 ws.ent_row, ws.ent_w, ws.h);
+        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_split<kDownSplit>, dim3(H / 16, kDownSplit),
+                 dim3(256), 0, s, R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh, edn,
+                 pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.dn_part,
+                 ws.dn_ctr, ws.h);
       else
         launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot, dim3(H / 16, E + 1, G), dim3(256), 0, s, R,
                  E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn,
@@ -427,10 +438,14 @@ struct Model {
                                                          eps, (T*)ws.xin, ws.status);
     smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
     attn_mfma(ws, B, C, w.d_attn_norm, nullptr, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
-    launch_k(tm, MTP_KC_DRAFT_FFN, prefill ? k_s_gu<GU_DRAFT_PREFILL> : k_s_gu<GU_DRAFT>,
-             dim3(F / 16, 1, groups(R)), dim3(256), lds_rows(R, H), s, R, H, 0, F, F, nullptr,
-             ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr, nullptr, nullptr,
-             ws.act_sh);
+#define MTP_DFFN(M)                                                                           \
+  launch_k(tm, MTP_KC_DRAFT_FFN,                                                              \
+           prefill ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT, M>,                       \
+           dim3(F / 16, 1, groups(R)), dim3(256), lds_rows(R, H), s, R, H, 0, F, F, nullptr,  \
+           ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr, nullptr, nullptr,   \
+           ws.act_sh)
+    MTP_MAXT_DISPATCH(H / 128, MTP_DFFN);
+#undef MTP_DFFN
     smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
     if (!head) return;
     k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
