@@ -974,60 +974,92 @@ __global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
 }
 
 // ---------------------------------------------------------------- LM head
-// Block = 4 vocabulary strips (64 rows) x a 16-row group (blockIdx.y) of
-// the nr input rows X (bf16); per row the best logit, its id (lowest on
-// ties) and the second best.
+// Block = 4 vocabulary strips (64 rows) x RG 16-row groups (blockIdx.y)
+// of the nr input rows X (bf16): each weight tile feeds RG MFMAs.  Per row
+// the best logit, its id (lowest on ties) and the second best.
+template <int RG>
 __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16_t* __restrict__ X,
                                               const uint4* __restrict__ Wp,
                                               float* __restrict__ logits, size_t ldl,
                                               float* __restrict__ pv, int32_t* __restrict__ pi,
                                               float* __restrict__ p2) {
-  __shared__ float bv[4][SR_MAX], sv[4][SR_MAX];
-  __shared__ int bi[4][SR_MAX];
+  constexpr int BT = 4;  // A tiles per batch (each used by RG MFMAs)
+  __shared__ float bv[4][16 * RG], sv[4][16 * RG];
+  __shared__ int bi[4][16 * RG];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int nkt = H / 32;
   const int nt = blockIdx.x * 4 + wv;
-  const int r0 = blockIdx.y * 16;
-  const int r = lane & 15;
-  const uint16_t* xrow = r0 + r < nr ? X + (size_t)(r0 + r) * H : nullptr;
+  const int r0 = blockIdx.y * 16 * RG;
+  const int r = lane & 15, koff = 8 * (lane >> 4);
+  const uint16_t* xrow[RG];
+#pragma unroll
+  for (int g = 0; g < RG; ++g)
+    xrow[g] = r0 + 16 * g + r < nr ? X + (size_t)(r0 + 16 * g + r) * H : nullptr;
   const bool live = nt * 16 < V;
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  if (live) acc = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow, acc);
-  const int v0 = nt * 16 + 4 * (lane >> 4);
-  float b1 = -INFINITY, b2 = -INFINITY;
-  int id = 1 << 30;
+  f32x4_t acc[RG];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int v = v0 + t;
-    const float x = (live && v < V) ? acc[t] : -INFINITY;
-    if (logits && r0 + r < nr && live && v < V) logits[(size_t)(r0 + r) * ldl + v] = x;
-    if (x > b1) {
-      b2 = b1;
-      b1 = x;
-      id = v;
-    } else if (x > b2) {
-      b2 = x;
-    }
-  }
-#pragma unroll
-  for (int o = 16; o <= 32; o <<= 1) {
-    const float ob1 = __shfl_xor(b1, o, MTP_WAVE), ob2 = __shfl_xor(b2, o, MTP_WAVE);
-    const int oid = __shfl_xor(id, o, MTP_WAVE);
-    if (ob1 > b1 || (ob1 == b1 && oid < id)) {
-      b2 = fmaxf(b1, ob2);
-      b1 = ob1;
-      id = oid;
+  for (int g = 0; g < RG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    if (RG == 1) {
+      acc[0] = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow[0], acc[0]);
     } else {
-      b2 = fmaxf(b2, ob1);
+      const uint4* A = Wp + (size_t)nt * nkt * 64;
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      for (int t0 = 0; t0 < nkt; t0 += BT) {
+        uint4 a[BT], b[RG][BT];
+#pragma unroll
+        for (int u = 0; u < BT; ++u) a[u] = t0 + u < nkt ? A[(size_t)(t0 + u) * 64 + lane] : z;
+#pragma unroll
+        for (int g = 0; g < RG; ++g)
+#pragma unroll
+          for (int u = 0; u < BT; ++u)
+            b[g][u] = (t0 + u < nkt && xrow[g]) ? ldx(xrow[g] + (t0 + u) * 32 + koff) : z;
+#pragma unroll
+        for (int u = 0; u < BT; ++u)
+#pragma unroll
+          for (int g = 0; g < RG; ++g) acc[g] = mfma16(a[u], b[g][u], acc[g]);
+      }
     }
   }
-  if (lane < 16) {
-    bv[wv][lane] = b1;
-    sv[wv][lane] = b2;
-    bi[wv][lane] = id;
+  const int v0 = nt * 16 + 4 * (lane >> 4);
+#pragma unroll
+  for (int g = 0; g < RG; ++g) {
+    const int row = r0 + 16 * g + r;
+    float b1 = -INFINITY, b2 = -INFINITY;
+    int id = 1 << 30;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int v = v0 + t;
+      const float x = (live && v < V) ? acc[g][t] : -INFINITY;
+      if (logits && row < nr && live && v < V) logits[(size_t)row * ldl + v] = x;
+      if (x > b1) {
+        b2 = b1;
+        b1 = x;
+        id = v;
+      } else if (x > b2) {
+        b2 = x;
+      }
+    }
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float ob1 = __shfl_xor(b1, o, MTP_WAVE), ob2 = __shfl_xor(b2, o, MTP_WAVE);
+      const int oid = __shfl_xor(id, o, MTP_WAVE);
+      if (ob1 > b1 || (ob1 == b1 && oid < id)) {
+        b2 = fmaxf(b1, ob2);
+        b1 = ob1;
+        id = oid;
+      } else {
+        b2 = fmaxf(b2, ob1);
+      }
+    }
+    if (lane < 16) {
+      bv[wv][16 * g + lane] = b1;
+      sv[wv][16 * g + lane] = b2;
+      bi[wv][16 * g + lane] = id;
+    }
   }
   __syncthreads();
-  if (threadIdx.x < 16 && r0 + (int)threadIdx.x < nr) {
+  if (threadIdx.x < 16 * RG && r0 + (int)threadIdx.x < nr) {
     const int rr = threadIdx.x;
     float c1 = bv[0][rr], c2 = sv[0][rr];
     int cid = bi[0][rr];

@@ -350,8 +350,16 @@ struct Model {
                int32_t* tok, float* margin) {
     const int V = c.vocab, H = c.hidden;
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
-    launch_k(tm, MTP_KC_LM_HEAD, k_s_lm, dim3(nblk, groups(nr)), dim3(256), 0, s, nr, V, H,
-             (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
+    const unsigned G = groups(nr);
+    if (G >= 4)
+      launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<4>, dim3(nblk, cdiv(G, 4)), dim3(256), 0, s, nr, V, H,
+               (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
+    else if (G >= 2)
+      launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<2>, dim3(nblk, cdiv(G, 2)), dim3(256), 0, s, nr, V, H,
+               (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
+    else
+      launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<1>, dim3(nblk, G), dim3(256), 0, s, nr, V, H,
+               (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
     k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
   }
