@@ -351,16 +351,25 @@ struct Model {
     const int V = c.vocab, H = c.hidden;
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
     const unsigned G = groups(nr);
-    if (G >= 4)
-      launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<4>, dim3(nblk, cdiv(G, 4)), dim3(256), 0, s, nr, V, H,
-               (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
-    else if (G >= 2)
+    unsigned nb = nblk;
+    if (G >= 4) {  // many rows: tiled GEMM, 128 vocabulary rows per block
+      nb = cdiv(V, 128);
+      const int NG = G >= 16 ? 16 : (G >= 8 ? 8 : 4);
+#define MTP_LMG(N)                                                                              \
+  launch_k(tm, MTP_KC_LM_HEAD, k_lm_gemm<N>, dim3(nb, cdiv(G, N)), dim3(512), 0, s, nr, V, H,   \
+           (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2)
+      if (NG == 16) MTP_LMG(16);
+      else if (NG == 8) MTP_LMG(8);
+      else MTP_LMG(4);
+#undef MTP_LMG
+    } else if (G >= 2) {
       launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<2>, dim3(nblk, cdiv(G, 2)), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
-    else
+    } else {
       launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<1>, dim3(nblk, G), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
-    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
+    }
+    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nb, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
   }
 
