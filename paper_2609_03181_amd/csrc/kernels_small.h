@@ -629,17 +629,18 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
 }
 
 // ---------------------------------------------------------------- MoE gate/up
-// Block = (16-wide intermediate tile, expert y, 16-entry chunk z): routed
-// expert y < E over its entries z*16.. (blocks past cnt[y] exit after one
-// load), or y == E: the dense SwiGLU over rows z*16.. (the shared experts as one
-// width-SI SwiGLU, or the draft FFN).  K split over 4 waves; weight tiles
+// Block = (16-wide intermediate tile, expert y, cpb 16-entry chunks from
+// z*16*cpb): routed expert y < E over its entries (blocks past cnt[y] exit
+// after one load), or y == E: the dense SwiGLU over rows (the shared
+// experts as one width-SI SwiGLU, or the draft FFN).  The weight tiles are
+// loaded once and applied to the block's chunks in turn.  K split over 4 waves; weight tiles
 // are loaded first.  With g != NULL the B rows are RMSNorm(h; g) computed
 // into LDS (dense mode), else the bf16 rows xg.  ROLE only names the
 // instance (so profiles separate decode from prefill launches); the draft
 // roles are the dense-only form (the draft block's FFN, launched with E = 0).
 enum { GU_VERIFY = 0, GU_DRAFT = 1, GU_PREFILL = 2, GU_DRAFT_PREFILL = 3 };
 template <int ROLE, int MAXT>
-__global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI,
+__global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int I, int SI,
                                               const uint16_t* __restrict__ xg,
                                               const float* __restrict__ h,
                                               const float* __restrict__ g, float eps,
@@ -653,7 +654,7 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
   extern __shared__ __align__(16) uint16_t xs[];
   __shared__ f32x4_t red[2 * 4 * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int it = blockIdx.x, e = blockIdx.y, t0 = blockIdx.z * 16;
+  const int it = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
   const bool dense = (ROLE & 1) || e == E;
   const int width = dense ? SI : I;
   if (it * 16 >= width) return;
@@ -662,7 +663,7 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
     n = cnt[e];
     o = off[e];
   }
-  if (t0 >= n) return;
+  if (tb >= n) return;
   const int nkt = H / 32, per = nkt / 4, ldl = H + XPAD;
   const uint4 *G, *U;
   if (dense) {
@@ -676,30 +677,56 @@ __global__ void __launch_bounds__(256) k_s_gu(int R, int H, int E, int I, int SI
   uint4 ag_[MAXT], au_[MAXT];
   preload<MAXT>(G, w * per, per, ag_);
   preload<MAXT>(U, w * per, per, au_);
-  const int t = t0 + (lane & 15);  // entry (routed) or row (dense)
-  const uint16_t* xrow = nullptr;
-  if (g) {
-    norm_rows_lds(min(16, n - t0), H, h + (size_t)t0 * H, nullptr, g, eps, xs, ldl, nullptr, 0,
-                  false);
-    __syncthreads();
-    if (t < n) xrow = xs + (lane & 15) * ldl;
-  } else if (t < n) {
-    xrow = xg + (size_t)(dense ? t : ent_row[o + t]) * H;
+  if (cpb == 1) {  // one chunk (with the RMSNorm prologue when g != NULL)
+    const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
+    const uint16_t* xrow = nullptr;
+    if (g) {
+      norm_rows_lds(min(16, n - t0), H, h + (size_t)t0 * H, nullptr, g, eps, xs, ldl, nullptr, 0,
+                    false);
+      __syncthreads();
+      if (t < n) xrow = xs + (lane & 15) * ldl;
+    } else if (t < n) {
+      xrow = xg + (size_t)(dense ? t : ent_row[o + t]) * H;
+    }
+    const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t cg = z4, cu = z4;
+    mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
+    cg = block_acc_sum<4>(cg, red);
+    cu = block_acc_sum<4>(cu, red + 4 * 64);
+    if (w != 0 || t >= n) return;
+    const int i = it * 16 + 4 * (lane >> 4);
+    uint2 pk;
+    pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
+    pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
+    if (dense)
+      *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
+    else
+      *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
+    return;
   }
-  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  f32x4_t cg = z4, cu = z4;
-  mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
-  cg = block_acc_sum<4>(cg, red);
-  cu = block_acc_sum<4>(cu, red + 4 * 64);
-  if (w != 0 || t >= n) return;
-  const int i = it * 16 + 4 * (lane >> 4);
-  uint2 pk;
-  pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
-  pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
-  if (dense)
-    *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
-  else
-    *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
+  // several chunks (bf16 rows xg): weight tiles kept in registers
+  for (int c = 0; c < cpb; ++c) {
+    const int t0 = tb + 16 * c;
+    if (t0 >= n) break;  // block-uniform
+    if (c > 0) __syncthreads();  // red of the previous chunk is consumed
+    const int t = t0 + (lane & 15);
+    const uint16_t* xrow = t < n ? xg + (size_t)(dense ? t : ent_row[o + t]) * H : nullptr;
+    const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t cg = z4, cu = z4;
+    mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
+    cg = block_acc_sum<4>(cg, red);
+    cu = block_acc_sum<4>(cu, red + 4 * 64);
+    if (w == 0 && t < n) {
+      const int i = it * 16 + 4 * (lane >> 4);
+      uint2 pk;
+      pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
+      pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
+      if (dense)
+        *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
+      else
+        *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- MoE down
@@ -879,12 +906,14 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
 }
 
 // ---------------------------------------------------------------- MoE down (slots)
-// Any batch: block = (16 output features, expert y, 16-entry chunk z), K
-// split over 4 waves.  Routed y < E: slot[(row*(k+1) + slot)][n] =
+// Any batch: block = (16 output features, expert y, cpb 16-entry chunks
+// from z*16*cpb), K split over 4 waves (with cpb > 1 the tiles are loaded
+// once and applied to the chunks in turn).  Routed y < E: slot[(row*(k+1) + slot)][n] =
 // w * (Wd_y[n] . act_t); y == E: slot[(r*(k+1) + k)][n] = Wsd[n] . act_sh[r]
 // (the shared experts as one width-SI SwiGLU).  k_combine_norm then adds
 // the k+1 slots of each row to h in a fixed order.
-__global__ void __launch_bounds__(256) k_s_down_slot(int R, int E, int topk, int H, int I, int SI,
+__global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int topk, int H,
+                                                     int I, int SI,
                                                      const uint16_t* __restrict__ act,
                                                      const uint16_t* __restrict__ act_sh,
                                                      const uint4* __restrict__ edn,
@@ -898,37 +927,71 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int R, int E, int topk, int
                                                      float* __restrict__ slot) {
   __shared__ f32x4_t red[4 * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int nt = blockIdx.x, e = blockIdx.y, t0 = blockIdx.z * 16;
+  const int nt = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
   const bool dense = e == E;
   int n = R, o = 0;
   if (!dense) {
     n = cnt[e];
     o = off[e];
   }
-  if (t0 >= n) return;
+  if (tb >= n) return;
   const int K = dense ? SI : I, nkt = K / 32, per = nkt / 4;
   const uint4* A = dense ? sdn + (size_t)nt * nkt * 64
                          : edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
-  const int t = t0 + (lane & 15);
-  const uint16_t* xrow = nullptr;
-  int row = 0, sl = topk;
-  float wt = 1.f;
-  if (t < n) {
-    if (dense) {
-      xrow = act_sh + (size_t)t * SI;
-      row = t;
-    } else {
-      xrow = act + (size_t)(o + t) * I;
-      row = ent_row[o + t];
-      sl = ent_slot[o + t];
-      wt = ent_w[o + t];
+  if (cpb == 1) {  // one chunk: stream the tiles (double-buffered)
+    const int t = tb + (lane & 15);
+    const uint16_t* xrow = nullptr;
+    int row = 0, sl = topk;
+    float wt = 1.f;
+    if (t < n) {
+      if (dense) {
+        xrow = act_sh + (size_t)t * SI;
+        row = t;
+      } else {
+        xrow = act + (size_t)(o + t) * I;
+        row = ent_row[o + t];
+        sl = ent_slot[o + t];
+        wt = ent_w[o + t];
+      }
+    }
+    f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    acc = block_acc_sum<4>(acc, red);
+    if (w != 0 || t >= n) return;
+    float4* dst =
+        (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
+    *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
+    return;
+  }
+  // several chunks: the wave's tiles (per <= 16) stay in registers
+  uint4 a[16];
+  preload<16>(A, w * per, per, a);
+  for (int c = 0; c < cpb; ++c) {
+    const int t0 = tb + 16 * c;
+    if (t0 >= n) break;  // block-uniform
+    if (c > 0) __syncthreads();
+    const int t = t0 + (lane & 15);
+    const uint16_t* xrow = nullptr;
+    int row = 0, sl = topk;
+    float wt = 1.f;
+    if (t < n) {
+      if (dense) {
+        xrow = act_sh + (size_t)t * SI;
+        row = t;
+      } else {
+        xrow = act + (size_t)(o + t) * I;
+        row = ent_row[o + t];
+        sl = ent_slot[o + t];
+        wt = ent_w[o + t];
+      }
+    }
+    f32x4_t acc = mma_pre<16, 4>(a, w * per, per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    acc = block_acc_sum<4>(acc, red);
+    if (w == 0 && t < n) {
+      float4* dst =
+          (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
+      *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
     }
   }
-  f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
-  acc = block_acc_sum<4>(acc, red);
-  if (w != 0 || t >= n) return;
-  float4* dst = (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
-  *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
 }
 
 // Grouping of (row, slot) pairs by expert for any number of rows: counts,

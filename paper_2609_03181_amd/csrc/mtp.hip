@@ -407,12 +407,14 @@ struct Model {
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
                                    ws.ent_slot, ws.ent_w);
       {
-        const dim3 grid(cdiv(SI > I ? SI : I, 16), E + 1, G);
+        const int cpb = G >= 8 ? 4 : 1;  // 16-entry chunks per block
+        const dim3 grid(cdiv(SI > I ? SI : I, 16), E + 1, cdiv(G, cpb));
         const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
         const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
 #define MTP_GU(M)                                                                             \
   launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL, M> : k_s_gu<GU_VERIFY, M>, grid,    \
-           dim3(256), 0, s, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps, egu, \
+           dim3(256), 0, s, cpb, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,  \
+           egu,                                                                                \
            pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act, ws.act_sh)
         MTP_MAXT_DISPATCH(H / 128, MTP_GU);
 #undef MTP_GU
@@ -424,10 +426,13 @@ struct Model {
                  dim3(256), 0, s, R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh, edn,
                  pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.dn_part,
                  ws.dn_ctr, ws.h);
-      else
-        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot, dim3(H / 16, E + 1, G), dim3(256), 0, s, R,
-                 E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn,
-                 ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot);
+      else {
+        const int cpb_d = G >= 8 ? 4 : 1;
+        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot, dim3(H / 16, E + 1, cdiv(G, cpb_d)),
+                 dim3(256), 0, s, cpb_d, R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh,
+                 edn, pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w,
+                 ws.slot);
+      }
     }
     k_combine_norm<<<R, 256, 0, s>>>(H, small ? 0 : k, small ? nullptr : ws.slot, ws.h,
                                      w.final_norm, eps, hid,
@@ -458,7 +463,7 @@ struct Model {
 #define MTP_DFFN(M)                                                                           \
   launch_k(tm, MTP_KC_DRAFT_FFN,                                                              \
            prefill ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT, M>,                       \
-           dim3(F / 16, 1, groups(R)), dim3(256), lds_rows(R, H), s, R, H, 0, F, F, nullptr,  \
+           dim3(F / 16, 1, groups(R)), dim3(256), lds_rows(R, H), s, 1, R, H, 0, F, F, nullptr, \
            ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr, nullptr, nullptr,   \
            ws.act_sh)
     MTP_MAXT_DISPATCH(H / 128, MTP_DFFN);
