@@ -44,44 +44,38 @@ __global__ void k_pack(const uint16_t* __restrict__ W, int N, int K, uint4* __re
 
 // ---------------------------------------------------------------- top-k helper
 // Router decision for one row, one lane per expert (E <= 64): lv = the
-// float32 logit (lanes >= E ignored).  Every lane reads all E logits from
-// LDS (broadcast reads, no cross-lane chains) and derives its rank --
+// float32 logit (lanes >= E ignored).  Every lane reads all 64 slots from
+// LDS (broadcast reads, issued together) and derives its rank --
 // #{j : l_j > l_e or (l_j == l_e and j < e)}, i.e. larger logit first, equal
-// logits to the lower id -- and its float32 softmax probability.  Lanes of
-// rank < topk write ridx/rw[rank]; gap = l_(k) - l_(k+1) (0 when k == E).
+// logits to the lower id; slots >= E hold -inf and never outrank a finite
+// logit, so the loop has no per-expert branch.  The float32 softmax
+// probability uses the wave max and a wave sum of the exponentials.  Lanes
+// of rank < topk write ridx/rw[rank]; gap = l_(k) - l_(k+1) (0 when k == E).
 // sc is 68 floats of wave-private, 16-byte aligned LDS.
 __device__ __forceinline__ void lane_topk(float lv, int E, int topk, float* sc, int32_t* ridx,
                                           float* rw, float* gap, int32_t* ridx_out, int* sel,
                                           float* selw) {
   const int lane = threadIdx.x & 63;
-  sc[lane] = lane < E ? lv : -INFINITY;
+  const float v = lane < E ? lv : -INFINITY;
+  sc[lane] = v;
   __builtin_amdgcn_wave_barrier();
   lds_wait();
-  float mx = -INFINITY;
+  float4 c[16];
+#pragma unroll
+  for (int j4 = 0; j4 < 16; ++j4) c[j4] = *(const float4*)(sc + 4 * j4);
   int rank = 0;
 #pragma unroll
   for (int j4 = 0; j4 < 16; ++j4) {
-    const float4 v = *(const float4*)(sc + 4 * j4);
-    const float vv[4] = {v.x, v.y, v.z, v.w};
+    const float vv[4] = {c[j4].x, c[j4].y, c[j4].z, c[j4].w};
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int j = 4 * j4 + q;
-      if (j < E) {
-        mx = fmaxf(mx, vv[q]);
-        rank += (vv[q] > lv) || (vv[q] == lv && j < lane);
-      }
+      rank += (int)(vv[q] > v) | (int)((vv[q] == v) & (j < lane));
     }
   }
-  float se = 0.f;
-#pragma unroll
-  for (int j4 = 0; j4 < 16; ++j4) {
-    const float4 v = *(const float4*)(sc + 4 * j4);
-    const float vv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (4 * j4 + q < E) se += __expf(vv[q] - mx);
-  }
-  const float p = __expf(lv - mx) / se;
+  const float mx = wave_max(v);
+  const float ex = lane < E ? __expf(v - mx) : 0.f;
+  const float p = ex / wave_sum(ex);
   __builtin_amdgcn_wave_barrier();
   if (lane < E && rank < topk) {
     ridx[rank] = lane;
@@ -92,8 +86,8 @@ __device__ __forceinline__ void lane_topk(float lv, int E, int topk, float* sc, 
       selw[rank] = p;
     }
   }
-  if (lane < E && rank == topk - 1) sc[64] = lv;
-  if (lane < E && rank == topk) sc[65] = lv;
+  if (lane < E && rank == topk - 1) sc[64] = v;
+  if (lane < E && rank == topk) sc[65] = v;
   __builtin_amdgcn_wave_barrier();
   lds_wait();
   if (lane == 0 && gap) *gap = topk < E ? sc[64] - sc[65] : 0.f;

@@ -142,52 +142,56 @@ __device__ __forceinline__ f32x4_t block_acc_sum(f32x4_t acc, f32x4_t* red) {
   return s;
 }
 
-// RMSNorm of rows r < R of src (row idx[r] when idx, row stride H,
-// H % 256 == 0, H <= 2048) with gain g into LDS xs[r][ldl] (bf16);
-// optionally float32 copies to yf (row stride ldf) when write_f.  One wave
-// per row; each lane loads its (up to 8) float4 of the row before using
-// any of them (the gain is re-read per row from cache).
+// RMSNorm of rows r < R of src (row stride H, H % 256 == 0, H <= 256*NV)
+// with gain g into LDS xs[r][ldl] (bf16).  Wave w takes rows w, w+nw, ...;
+// each row and the gain are loaded together, before the row's reduction,
+// so no load waits on a reduction.
+template <int NV>
 __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restrict__ src,
-                                              const int32_t* __restrict__ idx,
                                               const float* __restrict__ g, float eps,
-                                              uint16_t* xs, int ldl, float* __restrict__ yf,
-                                              int ldf, bool write_f) {
+                                              uint16_t* xs, int ldl) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int n4 = H / 256;  // float4 per lane
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int r = w; r < R; r += nw) {
-    const float4* x = (const float4*)(src + (size_t)(idx ? idx[r] : r) * H);
-    float4 xv[8];
+    float4 xv[NV], gv[NV];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (u < n4) xv[u] = x[u * 64 + lane];
+    for (int u = 0; u < NV; ++u) {
+      xv[u] = u < n4 ? ((const float4*)(src + (size_t)r * H))[u * 64 + lane] : z;
+      gv[u] = u < n4 ? ((const float4*)g)[u * 64 + lane] : z;
+    }
     float ss = 0.f;
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (u < n4) ss += xv[u].x * xv[u].x + xv[u].y * xv[u].y + xv[u].z * xv[u].z + xv[u].w * xv[u].w;
+    for (int u = 0; u < NV; ++u)
+      ss += xv[u].x * xv[u].x + xv[u].y * xv[u].y + xv[u].z * xv[u].z + xv[u].w * xv[u].w;
     ss = wave_sum(ss);
     const float rinv = rsqrtf(ss / (float)H + eps);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < NV; ++u) {
       if (u < n4) {
-        const int j = (u * 64 + lane) * 4;
-        const float4 gv = ((const float4*)g)[u * 64 + lane];
-        const float y0 = xv[u].x * rinv * gv.x, y1 = xv[u].y * rinv * gv.y;
-        const float y2 = xv[u].z * rinv * gv.z, y3 = xv[u].w * rinv * gv.w;
         uint2 pk;
-        pk.x = (uint32_t)f2bf(y0) | ((uint32_t)f2bf(y1) << 16);
-        pk.y = (uint32_t)f2bf(y2) | ((uint32_t)f2bf(y3) << 16);
-        *(uint2*)(xs + r * ldl + j) = pk;
-        if (write_f) *(float4*)(yf + (size_t)r * ldf + j) = make_float4(y0, y1, y2, y3);
+        pk.x = (uint32_t)f2bf(xv[u].x * rinv * gv[u].x) |
+               ((uint32_t)f2bf(xv[u].y * rinv * gv[u].y) << 16);
+        pk.y = (uint32_t)f2bf(xv[u].z * rinv * gv[u].z) |
+               ((uint32_t)f2bf(xv[u].w * rinv * gv[u].w) << 16);
+        *(uint2*)(xs + r * ldl + (u * 64 + lane) * 4) = pk;
       }
     }
   }
 }
 
+// float4 per lane of a row for the register tile count MAXT (= H/128
+// rounded up): H/256 <= (MAXT+1)/2
+#define MTP_NV(MAXT) (((MAXT) + 1) / 2)
+
 // ---------------------------------------------------------------- dense split-K
 // Y[r][n] (=|+=) X[r] . W[n], one 16-feature strip (blockIdx.x) x one
 // 16-row group (blockIdx.y) per block, K split over NW waves.  X bf16 rows
-// in global memory.
-template <int NW, bool ADD>
+// in global memory.  MAXT > 0: each wave's per = nkt/NW <= MAXT tiles are
+// all loaded first (and the residual being added to, by wave 0), so the
+// block waits on one round of loads; MAXT == 0 streams the tiles in
+// double-buffered batches (long K).
+template <int NW, bool ADD, int MAXT>
 __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
                                                   const uint16_t* __restrict__ X, int ldx_,
                                                   const uint4* __restrict__ Wp,
@@ -198,19 +202,25 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
   const int r = blockIdx.y * 16 + (lane & 15);  // 16-row group blockIdx.y
   const uint16_t* xrow = r < R ? X + (size_t)r * ldx_ : nullptr;
   const int per = nkt / NW;
-  f32x4_t acc = sk_range<(NW >= 16 ? 4 : 8)>(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per,
-                                            xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
-  acc = block_acc_sum<NW>(acc, red);
-  if (w != 0 || r >= R) return;
   const int n = nt * 16 + 4 * (lane >> 4);
-  if (n >= N) return;
-  float4* y = (float4*)(Y + (size_t)r * ldy + n);
-  float4 v = make_float4(acc[0], acc[1], acc[2], acc[3]);
-  if (ADD) {
-    const float4 o = *y;
-    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+  const bool out = w == 0 && r < R && n < N;
+  f32x4_t acc;
+  float4 y0 = make_float4(0.f, 0.f, 0.f, 0.f);
+  if constexpr (MAXT > 0) {
+    uint4 a[MAXT];
+    preload<MAXT>(Wp + (size_t)nt * nkt * 64, w * per, per, a);
+    if (ADD && out) y0 = *(const float4*)(Y + (size_t)r * ldy + n);
+    acc = mma_pre<MAXT, (NW >= 16 && MAXT > 8) ? MAXT / 2 : MAXT>(a, w * per, per, xrow,
+                                                                  f32x4_t{0.f, 0.f, 0.f, 0.f});
+  } else {
+    if (ADD && out) y0 = *(const float4*)(Y + (size_t)r * ldy + n);
+    acc = sk_range<(NW >= 16 ? 4 : 8)>(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per, xrow,
+                                        f32x4_t{0.f, 0.f, 0.f, 0.f});
   }
-  *y = v;
+  acc = block_acc_sum<NW>(acc, red);
+  if (!out) return;
+  *(float4*)(Y + (size_t)r * ldy + n) =
+      make_float4(acc[0] + y0.x, acc[1] + y0.y, acc[2] + y0.z, acc[3] + y0.w);
 }
 
 // ---------------------------------------------------------------- QKV
@@ -253,17 +263,24 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
   uint4 a0[MAXT], a1[MAXT];
   preload<MAXT>(Wp + (size_t)ta * nkt * 64, w * per, per, a0);
   preload<MAXT>(Wp + (size_t)tb * nkt * 64, w * per, pair ? per : 0, a1);
-  // row bookkeeping loads, independent of everything above
+  // row bookkeeping and the RoPE factors of this lane's features, loaded
+  // before the prologue so none of them waits on a reduction
   const int r0 = blockIdx.y * 16;
   const int nloc = min(16, R - r0);
   const int r = r0 + (lane & 15);
   const int valid = r < R ? row_valid[r] : 0;
   const int pos = r < R ? row_pos[r] : 0;
+  float2 cs[4] = {};
+  if (pair && w == 0 && r < R) {
+    const int p = valid ? pos : 0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) cs[t] = rope[(size_t)p * half + pt * 16 + 4 * (lane >> 4) + t];
+  }
   const uint16_t* xrow = nullptr;
   if (xg) {
     if (r < R) xrow = xg + (size_t)r * H;
   } else {
-    norm_rows_lds(nloc, H, h + (size_t)r0 * H, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+    norm_rows_lds<MTP_NV(MAXT)>(nloc, H, h + (size_t)r0 * H, g, eps, xs, ldl);
     __syncthreads();
     if (r < R) xrow = xs + (lane & 15) * ldl;
   }
@@ -280,9 +297,8 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int i = pt * 16 + 4 * (lane >> 4) + t;
-      const float2 cs = rope[(size_t)p * half + i];
       const float x0 = c0[t], x1 = c1[t];
-      const float y0 = x0 * cs.x - x1 * cs.y, y1 = x1 * cs.x + x0 * cs.y;
+      const float y0 = x0 * cs[t].x - x1 * cs[t].y, y1 = x1 * cs[t].x + x0 * cs[t].y;
       if (sec == 0) {
         q_out[(size_t)r * D + hh * dh + i] = y0;
         q_out[(size_t)r * D + hh * dh + i + half] = y1;
@@ -522,6 +538,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
 // first, equal -> lower id), k-th vs (k+1)-th gap; then the grouping of
 // (row, slot) pairs by expert (rows ascending) and the list of touched
 // experts (ascending id).
+template <int MAXT>
 __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk,
                                                    const float* __restrict__ h,
                                                    const float* __restrict__ g, float eps,
@@ -556,10 +573,13 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   // 16 waves = 4 strips x 4 K-quarters; weight tiles first
   const int strip = w >> 2, qk = w & 3, per = nkt / 4;
   const bool live = strip * 16 < E;
-  uint4 a[16];
-  preload<16>(Wp + (size_t)(live ? strip : 0) * nkt * 64, qk * per, live ? per : 0, a);
+  uint4 a[MAXT];
+  // (above 10 tiles per wave the prologue runs first: 1024-thread blocks
+  // have 128 registers per lane)
+  if constexpr (MAXT > 10) norm_rows_lds<MTP_NV(MAXT)>(nloc, H, h, g, eps, xs, ldl);
+  preload<MAXT>(Wp + (size_t)(live ? strip : 0) * nkt * 64, qk * per, live ? per : 0, a);
   const float bl = (bias && lane < E) ? bias[lane] : 0.f;
-  norm_rows_lds(nloc, H, h, nullptr, g, eps, xs, ldl, nullptr, 0, false);
+  if constexpr (MAXT <= 10) norm_rows_lds<MTP_NV(MAXT)>(nloc, H, h, g, eps, xs, ldl);
   __syncthreads();
   for (int e = threadIdx.x; e < nloc * H / 8; e += blockDim.x) {
     const int rr = e / (H / 8), c8 = e % (H / 8);
@@ -568,7 +588,7 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   const int r = lane & 15;
   const uint16_t* xrow = r < nloc ? xs + r * ldl : nullptr;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  if (live) acc = mma_pre<16, 4>(a, qk * per, per, xrow, acc);
+  if (live) acc = mma_pre<MAXT, (MAXT % 4 == 0 ? 4 : (MAXT % 5 == 0 ? 5 : MAXT))>(a, qk * per, per, xrow, acc);
   red[w * 64 + lane] = acc;
   __syncthreads();
   if (qk == 0 && live) {
@@ -680,9 +700,8 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
   if (cpb == 1) {  // one chunk (with the RMSNorm prologue when g != NULL)
     const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
     const uint16_t* xrow = nullptr;
-    if (g) {
-      norm_rows_lds(min(16, n - t0), H, h + (size_t)t0 * H, nullptr, g, eps, xs, ldl, nullptr, 0,
-                    false);
+    if ((ROLE & 1) != 0 && g) {  // draft roles, few rows: RMSNorm(h; g) prologue
+      norm_rows_lds<MTP_NV(MAXT)>(min(16, n - t0), H, h + (size_t)t0 * H, g, eps, xs, ldl);
       __syncthreads();
       if (t < n) xrow = xs + (lane & 15) * ldl;
     } else if (t < n) {

@@ -60,7 +60,7 @@ inline void launch_k(Timing* tm, int kc, void (*k)(KA...), dim3 grid, dim3 block
 namespace {
 
 constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
-constexpr int kDownSplit = 4;  // blocks per output strip of the small-batch MoE down
+constexpr int kDownSplit = 8;  // blocks per output strip of the small-batch MoE down
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -292,13 +292,19 @@ struct Model {
   // Y (=|+=) X . W^T over R rows (16-row groups)
   void smm(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
            bool add) {
-    const int nkt = K / 32, nw = nw_for(nkt);
+    const int nkt = K / 32, nw = nw_for(nkt), per = nkt / nw;
     const dim3 g(cdiv(N, 16), groups(R));
-#define MTP_SMM(NW)                                                                       \
-  if (add) k_s_mm<NW, true><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);        \
-  else k_s_mm<NW, false><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);
+#define MTP_SMM_T(NW, M)                                                                   \
+  if (add) k_s_mm<NW, true, M><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);      \
+  else k_s_mm<NW, false, M><<<g, NW * 64, 0, s>>>(R, N, nkt, X, ldx_, Wp, Y, ldy);
+#define MTP_SMM(NW)                                   \
+  if (per <= 4) { MTP_SMM_T(NW, 4) }                  \
+  else if (per <= 10) { MTP_SMM_T(NW, 10) }           \
+  else if (per <= 16) { MTP_SMM_T(NW, 16) }           \
+  else { MTP_SMM_T(NW, 0) }
     if (nw == 16) { MTP_SMM(16) } else if (nw == 8) { MTP_SMM(8) } else { MTP_SMM(4) }
 #undef MTP_SMM
+#undef MTP_SMM_T
   }
 
   // Key splits for one call: enough blocks to fill the chip (about 2048),
@@ -389,20 +395,23 @@ struct Model {
                                                   ws.status);
     for (int l = 0; l < L; ++l) {
       const uint16_t* xg = nullptr;
-      if (!small && l > 0) {  // add the previous layer's expert slots, normalise
-        k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.attn_norm + (size_t)l * H, eps,
-                                         nullptr, (uint16_t*)ws.xin);
+      if (!small) {  // add the previous layer's expert slots (if any), normalise once
+        k_combine_norm<<<R, 256, 0, s>>>(H, k, l > 0 ? ws.slot : nullptr, ws.h,
+                                         w.attn_norm + (size_t)l * H, eps, nullptr,
+                                         (uint16_t*)ws.xin);
         xg = (const uint16_t*)ws.xin;
       }
       attn_mfma(ws, B, C, w.attn_norm + (size_t)l * H, xg, pk.wqkv + l * pk.wqkv_s,
                 pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
-      launch_k(tm, MTP_KC_ROUTER, k_s_router, dim3(G), dim3(1024), lds_rows(R, H), s, R, H, E,
-               k, ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin,
-               pk.router + l * pk.router_s,
-               w.router_bias ? w.router_bias + (size_t)l * E : nullptr, ws.ridx, ws.rw,
-               route_gap ? route_gap + (size_t)l * R : ws.rgap,
-               route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.cnt, ws.off, ws.ent_row,
-               ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched);
+#define MTP_ROUTER(M)                                                                           \
+  launch_k(tm, MTP_KC_ROUTER, k_s_router<M>, dim3(G), dim3(1024), lds_rows(R, H), s, R, H, E, k, \
+           ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin, pk.router + l * pk.router_s, \
+           w.router_bias ? w.router_bias + (size_t)l * E : nullptr, ws.ridx, ws.rw,               \
+           route_gap ? route_gap + (size_t)l * R : ws.rgap,                                       \
+           route_idx ? route_idx + (size_t)l * R * k : nullptr, ws.cnt, ws.off, ws.ent_row,       \
+           ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched)
+      MTP_MAXT_DISPATCH(H / 128, MTP_ROUTER);
+#undef MTP_ROUTER
       if (G > 1)
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
                                    ws.ent_slot, ws.ent_w);
@@ -459,13 +468,26 @@ struct Model {
                                                          vis_off, a, a_ld, w.d_enorm, w.d_hnorm,
                                                          eps, (T*)ws.xin, ws.status);
     smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
-    attn_mfma(ws, B, C, w.d_attn_norm, nullptr, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
+    // Up to 16 rows the products normalise their rows in a prologue; with
+    // several row groups the rows are normalised once (bf16, into xin) and
+    // the products read them, each weight tile applied to cpb groups.
+    const unsigned G = groups(R);
+    const bool pre = G > 1;
+    const uint16_t* xn = pre ? (const uint16_t*)ws.xin : nullptr;
+    if (pre)
+      k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.d_attn_norm, eps, nullptr, 0,
+                                      (T*)ws.xin, H, 0);
+    attn_mfma(ws, B, C, w.d_attn_norm, xn, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
+    if (pre)
+      k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.d_ffn_norm, eps, nullptr, 0,
+                                      (T*)ws.xin, H, 0);
+    const int cpb = G >= 8 ? 4 : 1;
 #define MTP_DFFN(M)                                                                           \
   launch_k(tm, MTP_KC_DRAFT_FFN,                                                              \
            prefill ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT, M>,                       \
-           dim3(F / 16, 1, groups(R)), dim3(256), lds_rows(R, H), s, 1, R, H, 0, F, F, nullptr, \
-           ws.h, w.d_ffn_norm, eps, nullptr, 0, pk.d_gu, nullptr, nullptr, nullptr, nullptr,   \
-           ws.act_sh)
+           dim3(F / 16, 1, cdiv(G, cpb)), dim3(256), pre ? 0 : lds_rows(R, H), s, cpb, R, H, 0, \
+           F, F, xn, pre ? nullptr : ws.h, pre ? nullptr : w.d_ffn_norm, eps, nullptr, 0,       \
+           pk.d_gu, nullptr, nullptr, nullptr, nullptr, ws.act_sh)
     MTP_MAXT_DISPATCH(H / 128, MTP_DFFN);
 #undef MTP_DFFN
     smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);

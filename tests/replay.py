@@ -121,11 +121,14 @@ def new_stats():
     return dict(steps=0, followed_tokens=0, followed_routes=0)
 
 
-def teacher_forced_check(orc, tok_prefix, vis_prefix, gen, stats):
+def teacher_forced_check(orc, tok_prefix, vis_prefix, gen, stats, routes=None):
     """One causal oracle pass over the prefix and the generated tokens (the
     tokens the GPU produced are fed back in); the greedy token of the row
     before each generated token must be that token, or a near-tie of it
-    (reading of several correct results).  Returns the number checked."""
+    (reading of several correct results).  routes [L][P+n-1][k]: the GPU's
+    routing of every position of that pass, followed by the oracle where it
+    is a near-tie of its own (elsewhere the two must agree).  Returns the
+    number of tokens checked."""
     c = orc.cfg
     P, n = len(tok_prefix), len(gen)
     toks = np.concatenate([np.asarray(tok_prefix, np.int32), np.asarray(gen[:-1], np.int32)])
@@ -134,7 +137,12 @@ def teacher_forced_check(orc, tok_prefix, vis_prefix, gen, stats):
     hm = np.zeros(P + n - 1, np.uint8)
     hm[P - 1:] = 1
     kv = orc.new_kv(P + n)
-    r = orc.verify_rows(kv, toks, np.arange(P + n - 1), emb=emb, head_mask=hm, want_logits=True)
+    fr = None if routes is None else np.ascontiguousarray(routes[:, :P + n - 1])
+    r = orc.verify_rows(kv, toks, np.arange(P + n - 1), emb=emb, head_mask=hm, want_logits=True,
+                        want_routes=fr is not None, follow_route=fr)
+    if r["route_rejected"]:
+        raise Mismatch(f"{r['route_rejected']} routing decisions differ beyond the tolerance")
+    stats["followed_routes"] += r["route_followed"]
     for i in range(n):
         check_token(r["logits"][P - 1 + i], int(r["amax"][P - 1 + i]), int(gen[i]),
                     f"generated token {i}", stats)
