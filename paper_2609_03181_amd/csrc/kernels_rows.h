@@ -55,6 +55,66 @@ __global__ void k_row_tokens_verify(int B, int K, const int32_t* __restrict__ pe
   row_tok[r] = i == 0 ? pending[b] : draft[(size_t)b * K + i - 1];
 }
 
+// Depth-1 draft rows (catch-up): row r = b*C + i at row_pos_in[b] + i,
+// valid when i < n_rows[b] and inside the cache, token next_tok[b*C + i];
+// head_row[b] = the last valid row.  Row (b, 0) also checks that the
+// catch-up starts inside the valid base-form region and moves its end to
+// row_pos_in[b] + n_rows[b].  zero[0..n_zero) is cleared as in
+// k_rows_setup.
+__global__ void k_draft_rows(int B, int C, const int32_t* __restrict__ row_pos_in,
+                             const int32_t* __restrict__ n_rows,
+                             const int32_t* __restrict__ next_tok, int cap,
+                             int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
+                             int32_t* __restrict__ head_row, int32_t* __restrict__ row_tok,
+                             int32_t* __restrict__ draft_len, int32_t* __restrict__ status,
+                             int32_t* __restrict__ zero, int n_zero) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  for (int z = r; z < n_zero; z += gridDim.x * blockDim.x) zero[z] = 0;
+  if (r >= B * C) return;
+  const int b = r / C, i = r - b * C;
+  const int p0 = row_pos_in[b], p = p0 + i;
+  int nv = n_rows[b];
+  if (nv < 0 || nv > C) {
+    set_status(status, MTP_ECAPACITY);
+    nv = nv < 0 ? 0 : C;
+  }
+  int valid = i < nv;
+  if (valid && (p < 0 || p >= cap)) {
+    set_status(status, MTP_ECAPACITY);
+    valid = 0;
+  }
+  row_pos[r] = p;
+  row_valid[r] = valid;
+  row_tok[r] = next_tok[(size_t)b * C + i];
+  if (i == (nv > 0 ? nv - 1 : 0)) head_row[b] = r;
+  if (i == 0) {
+    if (p0 > draft_len[b]) set_status(status, MTP_ECAPACITY);
+    draft_len[b] = p0 + n_rows[b];
+  }
+}
+
+// Draft chain row of depth d >= 2 (one row per sequence): position
+// row_pos_in[b] + n_rows[b] - 1 + (d - 1), token draft_tok[b*K + d - 2].
+__global__ void k_chain_rows(int B, int d, int K, const int32_t* __restrict__ row_pos_in,
+                             const int32_t* __restrict__ n_rows,
+                             const int32_t* __restrict__ draft_tok, int cap,
+                             int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
+                             int32_t* __restrict__ head_row, int32_t* __restrict__ row_tok,
+                             int32_t* __restrict__ status) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int p = row_pos_in[b] + n_rows[b] - 1 + (d - 1);
+  int valid = 1;
+  if (p < 0 || p >= cap) {
+    set_status(status, MTP_ECAPACITY);
+    valid = 0;
+  }
+  row_pos[b] = p;
+  row_valid[b] = valid;
+  head_row[b] = b;
+  row_tok[b] = draft_tok[(size_t)b * K + d - 2];
+}
+
 // Loads input row r (token embedding, or a vision row when the token is
 // negative) as float32 into smem[0..H).  Vision row of (b, i):
 // vision[((size_t)b*vis_ld + vis_off + i)*H].  Invalid rows and bad tokens
@@ -93,6 +153,37 @@ __global__ void k_embed(int R, int C, int H, int V, const int32_t* __restrict__ 
   load_input_row<BF>(r, C, H, V, row_valid[r], row_tok, embed, vision, vis_ld, vis_off, sm,
                      status);
   for (int j = threadIdx.x; j < H; j += blockDim.x) h[(size_t)r * H + j] = sm[j];
+}
+
+// Verify rows fused with their embedding: row r = b*(K+1) + i at
+// kv_len[b] + i (valid inside the cache), token pending[b] (i = 0) or
+// draft[b*K + i - 1]; h[r] = its embedding row (zero for invalid rows; a
+// token outside the vocabulary sets MTP_ETOKEN).  One block per row;
+// zero[0..n_zero) is cleared as in k_rows_setup.
+template <bool BF>
+__global__ void k_verify_rows(int B, int K, const int32_t* __restrict__ kv_len,
+                              const int32_t* __restrict__ pending,
+                              const int32_t* __restrict__ draft, int cap, int H, int V,
+                              const typename St<BF>::T* __restrict__ embed,
+                              int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
+                              float* __restrict__ h, int32_t* __restrict__ status,
+                              int32_t* __restrict__ zero, int n_zero) {
+  using S = St<BF>;
+  for (int z = blockIdx.x * blockDim.x + threadIdx.x; z < n_zero; z += gridDim.x * blockDim.x)
+    zero[z] = 0;
+  const int C = K + 1, r = blockIdx.x;
+  const int b = r / C, i = r - b * C;
+  const int p = kv_len[b] + i;
+  const int valid = p >= 0 && p < cap;
+  const int t = i == 0 ? pending[b] : draft[(size_t)b * K + i - 1];
+  if (threadIdx.x == 0) {
+    if (!valid) set_status(status, MTP_ECAPACITY);
+    else if (t < 0 || t >= V) set_status(status, MTP_ETOKEN);
+    row_pos[r] = p;
+    row_valid[r] = valid;
+  }
+  const typename S::T* src = (valid && t >= 0 && t < V) ? embed + (size_t)t * H : nullptr;
+  for (int j = threadIdx.x; j < H; j += blockDim.x) h[(size_t)r * H + j] = src ? S::ld(src, j) : 0.f;
 }
 
 // RMSNorm of x[src_row] (float32, row stride ldx) with gain g:

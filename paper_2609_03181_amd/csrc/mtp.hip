@@ -193,19 +193,21 @@ struct Model {
     const unsigned nblk = cdiv(V, kLmBlk);
     k_lm_partial<BF><<<nblk, 256, 0, s>>>(nr, V, H, (const T*)ws.xhead, W, logits, ldl, ws.pv,
                                           ws.pi, ws.p2);
-    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
+    k_argmax_final<<<nr, 256, 0, s>>>(nr, nblk, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
   }
 
   // Verifier over B x C rows (row tokens and row setup already in ws).
   // b states go to hid (row stride H); LM head on every row (head_all)
   // or on ws.head_row only.
+  // embedded: ws.h already holds the input rows (the caller fused the
+  // embedding into its row setup)
   void verifier(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
                 float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
-                float* margin, int32_t* route_idx, float* route_gap) {
+                float* margin, int32_t* route_idx, float* route_gap, bool embedded = false) {
     if constexpr (BF) {
       verifier_mfma(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
-                    logits, margin, route_idx, route_gap);
+                    logits, margin, route_idx, route_gap, embedded);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -213,7 +215,8 @@ struct Model {
     const int SI = c.n_shared * I;
     const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
     const size_t layer_stride = (size_t)B * seq_stride;
-    k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed,
+    if (!embedded)
+      k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed,
                                                   vision, vis_ld, vis_off, ws.h, ws.status);
     for (int l = 0; l < L; ++l) {
       attn_sublayer(ws, B, C, w.attn_norm + (size_t)l * H, wp(w.wqkv, (size_t)l * 3 * D * H),
@@ -375,13 +378,14 @@ struct Model {
       launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<1>, dim3(nblk, G), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
     }
-    k_argmax_final<<<cdiv(nr, 4), 256, 0, s>>>(nr, nb, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
+    k_argmax_final<<<nr, 256, 0, s>>>(nr, nb, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
                                                tok, margin);
   }
 
   void verifier_mfma(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
                      float* hid, bool head_all, int32_t* tok, int per, int ostride,
-                     float* logits, float* margin, int32_t* route_idx, float* route_gap) {
+                     float* logits, float* margin, int32_t* route_idx, float* route_gap,
+                     bool embedded) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter, S = c.n_shared;
     const int SI = S * I;
@@ -390,7 +394,8 @@ struct Model {
     const size_t layer_stride = (size_t)B * seq_stride;
     const bool small = R <= SR_MAX;  // MoE down adds straight into h
     const unsigned G = groups(R);
-    k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok,
+    if (!embedded)
+      k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok,
                                                   (const T*)w.embed, vision, vis_ld, vis_off, ws.h,
                                                   ws.status);
     for (int l = 0; l < L; ++l) {
@@ -754,24 +759,20 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
     Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
-    k_draft_len<<<cdiv(batch, 256), 256, 0, s>>>(batch, n_rows, row_pos, draft_len, w.status);
     // depth 1 over the catch-up rows; the last valid row starts the chain
-    k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, 0, n_rows, c.max_ctx, w.row_pos,
-                                               w.row_valid, w.head_row, w.status, w.att_ctr,
-                                               w.n_ctr);
-    k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, C, next_tok, C, 0, w.row_tok);
+    k_draft_rows<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, n_rows, next_tok, c.max_ctx,
+                                               w.row_pos, w.row_valid, w.head_row, w.row_tok,
+                                               draft_len, w.status, w.att_ctr, w.n_ctr);
     m.draft(w, batch, C, hid, (size_t)C * H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k, 0,
             draft_logits, (size_t)k * V);
     // depth d = 2..k: one row at (row_pos + n_rows - 1) + (d - 1), state u
-    // of depth d-1, input the depth d-1 draft token
-    k_chain_pos<<<cdiv(batch, 256), 256, 0, s>>>(batch, row_pos, n_rows, w.chain_pos);
+    // of depth d-1 (read by the draft input before the head rewrites it),
+    // input the depth d-1 draft token
     for (int d = 2; d <= k; ++d) {
-      k_rows_setup<<<cdiv(batch, 256), 256, 0, s>>>(batch, 1, w.chain_pos, d - 1, nullptr,
+      k_chain_rows<<<cdiv(batch, 256), 256, 0, s>>>(batch, d, k, row_pos, n_rows, draft_tok,
                                                      c.max_ctx, w.row_pos, w.row_valid,
-                                                     w.head_row, w.status);
-      k_row_tokens<<<cdiv(batch, 256), 256, 0, s>>>(batch, 1, draft_tok, k, d - 2, w.row_tok);
-      k_copy_rows<<<batch, 256, 0, s>>>(batch, H, nullptr, w.ustate, w.bbuf, (size_t)H);
-      m.draft(w, batch, 1, w.bbuf, (size_t)H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k,
+                                                     w.head_row, w.row_tok, w.status);
+      m.draft(w, batch, 1, w.ustate, (size_t)H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k,
               d - 1, draft_logits ? draft_logits + (size_t)(d - 1) * V : nullptr, (size_t)k * V);
     }
     return launch_status();
@@ -798,12 +799,11 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
     Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
-    k_rows_setup<<<cdiv(R, 256), 256, 0, s>>>(batch, C, kv_len, 0, nullptr, c.max_ctx, w.row_pos,
-                                               w.row_valid, nullptr, w.status, w.att_ctr,
-                                               w.n_ctr);
-    k_row_tokens_verify<<<cdiv(R, 256), 256, 0, s>>>(batch, k, pending, draft_tok, w.row_tok);
+    k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
+                                        c.hidden, c.vocab, (const T*)ctx->w.embed, w.row_pos,
+                                        w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
     m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
-               margin, route_idx, route_gap);
+               margin, route_idx, route_gap, /*embedded=*/true);
     return launch_status();
   };
   if (c.dtype == MTP_BF16) return run(std::true_type{});
