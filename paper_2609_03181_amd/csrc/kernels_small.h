@@ -832,10 +832,16 @@ __global__ void __launch_bounds__(1024) k_s_down(int R, int H, int E, int I, int
 }
 
 // Same product spread over NG blocks per strip (grid (H/16, NG), 4 waves
-// each): virtual expert v goes to wave slot v % (4*NG).  Each block stores
-// its wave-ordered partial [R][16] (write-through); the last block of the
-// strip adds the NG partials to h in block order, so the summation order is
-// fixed.  ctr[H/16] must be zero at launch (it is left at zero).
+// each): virtual expert v goes to wave slot v % (4*NG).  The contributions
+// w * (Wd[n] . act) are summed in 64-bit fixed point (2^-32 units): integer
+// addition is exact and associative, so a row's sum does not depend on
+// which wave or block handled which expert -- and hence not on the other
+// rows of the pass -- and is rounded to float32 once.  Each block stores its
+// wave-summed partial (write-through); the last block of the strip adds the
+// NG partials and the rounded total to h.  ctr[H/16] must be zero at launch
+// (it is left at zero).
+__device__ __forceinline__ long long fx32(float x) { return __float2ll_rn(x * 4294967296.0f); }
+
 template <int NG>
 __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I, int S,
                                                       const uint16_t* __restrict__ act,
@@ -847,10 +853,10 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
                                                       const int32_t* __restrict__ off,
                                                       const int32_t* __restrict__ ent_row,
                                                       const float* __restrict__ ent_w,
-                                                      float* __restrict__ part,
+                                                      unsigned long long* __restrict__ part,
                                                       int32_t* __restrict__ ctr,
                                                       float* __restrict__ h) {
-  __shared__ float acc_l[4][SR_MAX][17];
+  __shared__ long long acc_l[4][SR_MAX][17];
   __shared__ int l_cnt[64], l_off[64], l_list[64], l_n, last;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nt = blockIdx.x, gq = blockIdx.y;
@@ -859,7 +865,7 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
     l_cnt[e] = e < E ? cnt[e] : 0;
     l_off[e] = e < E ? off[e] : 0;
   }
-  for (int e = threadIdx.x; e < 4 * SR_MAX * 17; e += blockDim.x) (&acc_l[0][0][0])[e] = 0.f;
+  for (int e = threadIdx.x; e < 4 * SR_MAX * 17; e += blockDim.x) (&acc_l[0][0][0])[e] = 0;
   __syncthreads();
   if (w == 0) {  // compact list of touched experts, ascending id
     const int has = l_cnt[lane] > 0;
@@ -901,13 +907,17 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
     const f32x4_t a = sk_range<8>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
     if (row >= 0) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += wt * a[q];
+      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += fx32(wt * a[q]);
     }
   }
   __syncthreads();
   const int rr = threadIdx.x >> 4, f = threadIdx.x & 15;
-  float* pp = part + ((size_t)gq * R + rr) * H + nt * 16 + f;
-  if (rr < R) st_agent(pp, ((acc_l[0][rr][f] + acc_l[1][rr][f]) + acc_l[2][rr][f]) + acc_l[3][rr][f]);
+  unsigned long long* pp = part + ((size_t)gq * R + rr) * H + nt * 16 + f;
+  if (rr < R)
+    __hip_atomic_store(pp,
+                       (unsigned long long)(acc_l[0][rr][f] + acc_l[1][rr][f] + acc_l[2][rr][f] +
+                                            acc_l[3][rr][f]),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   vmem_release();
   __syncthreads();
   if (threadIdx.x == 0)
@@ -917,10 +927,12 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
   if (!last) return;
   if (threadIdx.x == 0) __hip_atomic_store(ctr + nt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (rr < R) {
-    float sum = 0.f;
+    long long sum = 0;
 #pragma unroll
-    for (int x = 0; x < NG; ++x) sum += ld_agent(part + ((size_t)x * R + rr) * H + nt * 16 + f);
-    h[(size_t)rr * H + nt * 16 + f] += sum;
+    for (int x = 0; x < NG; ++x)
+      sum += (long long)__hip_atomic_load(part + ((size_t)x * R + rr) * H + nt * 16 + f,
+                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    h[(size_t)rr * H + nt * 16 + f] += (float)sum * 2.3283064365386963e-10f;  // 2^-32
   }
 }
 

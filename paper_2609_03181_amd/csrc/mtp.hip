@@ -75,7 +75,7 @@ struct Ws {
   // bf16 fast path
   float *part, *slot, *ent_w;
   int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr, *dn_ctr;
-  float* dn_part;  // MoE down split partials [kDownSplit][R][H] (R <= 16)
+  unsigned long long* dn_part;  // MoE down split partials [kDownSplit][R][H], fixed point (R <= 16)
   uint16_t* act_sh;
   int n_ctr;  // entries of att_ctr (zeroed at the start of each call)
   size_t bytes;
@@ -139,7 +139,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.att_ctr = (int32_t*)take((R * c.n_heads + (size_t)H / 16) * 4);
     w.dn_ctr = w.att_ctr + R * c.n_heads;
     w.n_ctr = (int)(R * c.n_heads + H / 16);
-    w.dn_part = (float*)take((size_t)kDownSplit * (R < 16 ? R : 16) * H * 4);
+    w.dn_part = (unsigned long long*)take((size_t)kDownSplit * (R < 16 ? R : 16) * H * 8);
     const size_t shw = (size_t)(SI > c.draft_inter ? SI : c.draft_inter);
     w.act_sh = (uint16_t*)take(R * shw * 2);
   } else {

@@ -20,7 +20,7 @@ import oracle
 import synth
 from paper_2609_03181_amd.session import Model, Session
 from tests import replay
-from tests.gpu_util import (gpu_prefill, load_synthetic, log, oracle_prefill,
+from tests.gpu_util import (finished, gpu_prefill, load_synthetic, log, oracle_prefill,
                             oracle_synthetic_state, prefix_inputs, step_records,
                             synthetic_context)
 
@@ -99,6 +99,33 @@ def test_full_shape_batch1_prefill_and_steps(plain):
     np.testing.assert_allclose(s.hid.cpu().numpy()[0, 0], st.hid[0], rtol=TOL, atol=STATE_TOL)
     stats = _replay_steps(orc, s, {0: st}, K, n_steps)
     log(f"[full B=1] {n_steps} steps ok, followed near-ties: {stats}")
+
+
+def test_full_shape_batch1_spec_equals_greedy_bitwise(plain):
+    """Losslessness on the GPU at full shape, bit for bit: with up to 16 rows
+    a row's result does not depend on the other rows of its verify pass (the
+    MoE down sums in exact fixed point), so speculative decoding with K = 1
+    and 3 emits exactly the tokens of plain greedy decoding (K = 0) and
+    writes the same verifier K/V."""
+    w, model, orc = plain
+    n_vis, n_txt, n_new = 256, 512, 48
+    tok, vis = prefix_inputs(CFG, 1, n_vis, n_txt)
+    outs, kvs = {}, {}
+    for K in (0, 1, 3):
+        s = gpu_prefill(model, 1, K, tok, vis, n_new, record=False, prefill_rows=64)
+        s.capture()
+        while not finished(s):
+            s.replay()
+        assert s.status() == 0
+        outs[K] = s.outputs()[0]
+        kvs[K] = (int(s.kv_len[0]), s.kv[:, 0].clone())
+        log(f"[full B=1 bitwise] K={K}: {len(outs[K])} tokens, kv_len {kvs[K][0]}")
+        del s
+    n = min(v[0] for v in kvs.values())  # committed rows (later ones may be rejected drafts)
+    assert n >= n_vis + n_txt + n_new - 4
+    for K in (1, 3):
+        assert outs[K] == outs[0]
+        assert torch.equal(kvs[K][1][..., :n, :], kvs[0][1][..., :n, :])
 
 
 def test_full_shape_batch16_sampled_sequences(plain):
