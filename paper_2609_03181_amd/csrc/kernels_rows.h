@@ -44,17 +44,6 @@ __global__ void k_row_tokens(int B, int C, const int32_t* __restrict__ src, int 
   row_tok[r] = off + i < ld ? src[(size_t)b * ld + off + i] : -1;
 }
 
-// verify rows: row (b, 0) = pending[b], row (b, i>0) = draft[b][i-1]
-__global__ void k_row_tokens_verify(int B, int K, const int32_t* __restrict__ pending,
-                                    const int32_t* __restrict__ draft,
-                                    int32_t* __restrict__ row_tok) {
-  int r = blockIdx.x * blockDim.x + threadIdx.x;
-  int C = K + 1;
-  if (r >= B * C) return;
-  int b = r / C, i = r - b * C;
-  row_tok[r] = i == 0 ? pending[b] : draft[(size_t)b * K + i - 1];
-}
-
 // Depth-1 draft rows (catch-up): row r = b*C + i at row_pos_in[b] + i,
 // valid when i < n_rows[b] and inside the cache, token next_tok[b*C + i];
 // head_row[b] = the last valid row.  Row (b, 0) also checks that the

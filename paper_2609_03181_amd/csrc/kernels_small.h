@@ -6,9 +6,10 @@
 //     accumulators are summed in LDS in wave order (deterministic);
 //   - RMSNorm is a prologue that recomputes the (few) normalised rows into
 //     LDS, which then feeds the MFMA B operand;
-//   - the MoE down projection is n-tile-major: one block owns 16 output
-//     features, its waves take the touched experts round-robin, and the
-//     block adds the sum straight into the residual stream.
+//   - the MoE down projection is n-tile-major: the blocks of a 16-feature
+//     strip share the touched experts round-robin, and the strip's last
+//     block adds the (exact fixed-point) sum straight into the residual
+//     stream.
 #pragma once
 #include "common.h"
 #include "kernels_mfma.h"
@@ -749,90 +750,12 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
 }
 
 // ---------------------------------------------------------------- MoE down
-// Block = 16 output features (one strip of every down matrix); its 16 waves
-// take the virtual experts round-robin -- the touched routed experts in
-// ascending id, then the S shared experts (width I each) -- and accumulate
-// w_t * (Wd[n] . act_t) into per-wave LDS rows; the block then adds the
-// wave-ordered sum into h (only this block writes these 16 columns).  The
-// expert lists are staged in LDS first so no wave chains index loads.
-__global__ void __launch_bounds__(1024) k_s_down(int R, int H, int E, int I, int S,
-                                                 const uint16_t* __restrict__ act,
-                                                 const uint16_t* __restrict__ act_sh,
-                                                 const uint4* __restrict__ edn, size_t e_stride,
-                                                 const uint4* __restrict__ sdn,
-                                                 const int32_t* __restrict__ cnt,
-                                                 const int32_t* __restrict__ off,
-                                                 const int32_t* __restrict__ ent_row,
-                                                 const float* __restrict__ ent_w,
-                                                 float* __restrict__ h) {
-  constexpr int NW = 16;
-  __shared__ float acc_l[NW][SR_MAX][17];
-  __shared__ int l_cnt[64], l_off[64], l_list[64], l_n;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int nt = blockIdx.x;
-  if (threadIdx.x < 64) {
-    const int e = threadIdx.x;
-    l_cnt[e] = e < E ? cnt[e] : 0;
-    l_off[e] = e < E ? off[e] : 0;
-  }
-  for (int e = threadIdx.x; e < NW * SR_MAX * 17; e += blockDim.x) (&acc_l[0][0][0])[e] = 0.f;
-  __syncthreads();
-  if (w == 0) {  // compact list of touched experts, ascending id
-    const int has = l_cnt[lane] > 0;
-    int pre = has;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int v = __shfl_up(pre, d, MTP_WAVE);
-      if (lane >= d) pre += v;
-    }
-    if (has) l_list[pre - 1] = lane;
-    if (lane == 63) l_n = pre;
-  }
-  __syncthreads();
-  const int n_routed = l_n, nvirt = n_routed + S;
-  const int nkt = I / 32;
-  const int t = lane & 15;
-  for (int v = w; v < nvirt; v += NW) {
-    const uint4* A;
-    const uint16_t* xrow = nullptr;
-    int row = -1;
-    float wt = 1.f;
-    if (v < n_routed) {
-      const int e = l_list[v];
-      const int n = l_cnt[e], o = l_off[e];
-      A = edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
-      if (t < n) {
-        xrow = act + (size_t)(o + t) * I;
-        row = ent_row[o + t];
-        wt = ent_w[o + t];
-      }
-    } else {
-      const int sx = v - n_routed;
-      // shared expert sx: columns sx*I.. of the [H][S*I] down matrix, whose
-      // packed strip nt has S*nkt tiles
-      A = sdn + (size_t)nt * S * nkt * 64 + (size_t)sx * nkt * 64;
-      if (t < R) {
-        xrow = act_sh + (size_t)t * S * I + (size_t)sx * I;
-        row = t;
-      }
-    }
-    const f32x4_t a = sk_range<4>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
-    if (row >= 0) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += wt * a[q];
-    }
-  }
-  __syncthreads();
-  const int rr = threadIdx.x >> 4, f = threadIdx.x & 15;
-  if (rr < R) {
-    float sum = 0.f;
-    for (int x = 0; x < NW; ++x) sum += acc_l[x][rr][f];
-    h[(size_t)rr * H + nt * 16 + f] += sum;
-  }
-}
-
-// Same product spread over NG blocks per strip (grid (H/16, NG), 4 waves
-// each): virtual expert v goes to wave slot v % (4*NG).  The contributions
+// MoE down for up to 16 rows: grid (H/16 output strips, NG groups), 4
+// waves per block.  The virtual experts -- the touched routed experts in
+// ascending id, then the S shared experts (width I each) -- go to wave slot
+// v % (4*NG); a wave streams each of its experts' strip tiles in
+// double-buffered batches and accumulates w * (Wd[n] . act) per row in LDS
+// (the expert lists are staged in LDS first).  The contributions
 // w * (Wd[n] . act) are summed in 64-bit fixed point (2^-32 units): integer
 // addition is exact and associative, so a row's sum does not depend on
 // which wave or block handled which expert -- and hence not on the other

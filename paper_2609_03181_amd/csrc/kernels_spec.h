@@ -49,24 +49,6 @@ __global__ void k_commit(int B, int K, const int32_t* __restrict__ accept_len,
   n_out[b] = no + take;
 }
 
-// Draft bookkeeping: the catch-up must start inside the valid base-form
-// region; afterwards the region ends at row_pos + n_rows.
-__global__ void k_draft_len(int B, const int32_t* __restrict__ n_rows,
-                            const int32_t* __restrict__ row_pos, int32_t* __restrict__ draft_len,
-                            int32_t* __restrict__ status) {
-  int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  if (row_pos[b] > draft_len[b]) set_status(status, MTP_ECAPACITY);
-  draft_len[b] = row_pos[b] + n_rows[b];
-}
-
-// chain base position: the last catch-up row, row_pos + n_rows - 1
-__global__ void k_chain_pos(int B, const int32_t* __restrict__ row_pos,
-                            const int32_t* __restrict__ n_rows, int32_t* __restrict__ out) {
-  int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < B) out[b] = row_pos[b] + n_rows[b] - 1;
-}
-
 // End of prefill: step state for the first step.
 __global__ void k_prefill_state(int B, int K, int P, const int32_t* __restrict__ tok_last,
                                 int32_t* __restrict__ kv_len, int32_t* __restrict__ draft_len,
