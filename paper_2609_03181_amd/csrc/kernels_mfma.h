@@ -25,6 +25,18 @@ __device__ __forceinline__ f32x4_t mfma16(uint4 a, uint4 b, f32x4_t c) {
 
 __device__ __forceinline__ uint4 ldx(const uint16_t* p) { return *(const uint4*)p; }
 
+// One lane's 16 bytes of a weight tile.  Tiles a launch reads once are
+// loaded non-temporally (measured: a 330 MB stream reaches 6.9 TB/s this
+// way against 6.5 TB/s with ordinary loads).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_tile(const uint4* p, bool nt) {
+  if (nt) {
+    const u32x4_t x = __builtin_nontemporal_load((const u32x4_t*)p);
+    return make_uint4(x[0], x[1], x[2], x[3]);
+  }
+  return *p;
+}
+
 inline size_t packed_elems(int N, int K) {  // in uint4 units
   return (size_t)((N + 15) / 16) * (K / 32) * 64;
 }

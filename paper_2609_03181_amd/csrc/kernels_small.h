@@ -27,13 +27,13 @@ constexpr int XPAD = 8;     // LDS row padding (bf16 elements)
 template <int BT>
 __device__ __forceinline__ void sk_load(const uint4* __restrict__ A, int t, int t1,
                                         const uint16_t* xrow, int koff, uint4 (&a)[BT],
-                                        uint4 (&b)[BT]) {
+                                        uint4 (&b)[BT], bool nt) {
   const int lane = threadIdx.x & 63;
   const uint4 z = make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int u = 0; u < BT; ++u) {
     if (t + u < t1) {
-      a[u] = A[(size_t)(t + u) * 64 + lane];
+      a[u] = ld_tile(A + (size_t)(t + u) * 64 + lane, nt);
       b[u] = xrow ? ldx(xrow + (t + u) * 32 + koff) : z;
     }
   }
@@ -41,18 +41,18 @@ __device__ __forceinline__ void sk_load(const uint4* __restrict__ A, int t, int 
 
 template <int BT = 8>
 __device__ __forceinline__ f32x4_t sk_range(const uint4* __restrict__ A, int t0, int t1,
-                                            const uint16_t* xrow, f32x4_t acc) {
+                                            const uint16_t* xrow, f32x4_t acc, bool nt = false) {
   const int koff = 8 * ((threadIdx.x & 63) >> 4);
   const uint4 z = make_uint4(0, 0, 0, 0);
   uint4 a[BT], b[BT];
 #pragma unroll
   for (int u = 0; u < BT; ++u) a[u] = b[u] = z;  // every staged register defined
-  if (t0 < t1) sk_load<BT>(A, t0, t1, xrow, koff, a, b);
+  if (t0 < t1) sk_load<BT>(A, t0, t1, xrow, koff, a, b, nt);
   for (int t = t0; t < t1; t += BT) {
     uint4 an[BT], bn[BT];
 #pragma unroll
     for (int u = 0; u < BT; ++u) an[u] = bn[u] = z;
-    if (t + BT < t1) sk_load<BT>(A, t + BT, t1, xrow, koff, an, bn);
+    if (t + BT < t1) sk_load<BT>(A, t + BT, t1, xrow, koff, an, bn, nt);
 #pragma unroll
     for (int u = 0; u < BT; ++u)
       if (t + u < t1) acc = mfma16(a[u], b[u], acc);
@@ -68,11 +68,11 @@ __device__ __forceinline__ f32x4_t sk_range(const uint4* __restrict__ A, int t0,
 // up to MAXT tiles of a strip, loaded into registers ahead of their use
 template <int MAXT>
 __device__ __forceinline__ void preload(const uint4* __restrict__ A, int t0, int n,
-                                        uint4 (&a)[MAXT]) {
+                                        uint4 (&a)[MAXT], bool nt = false) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int u = 0; u < MAXT; ++u)
-    a[u] = u < n ? A[(size_t)(t0 + u) * 64 + lane] : make_uint4(0, 0, 0, 0);
+    a[u] = u < n ? ld_tile(A + (size_t)(t0 + u) * 64 + lane, nt) : make_uint4(0, 0, 0, 0);
 }
 
 // acc += preloaded tiles a[0..n) against this lane's B row; the B operands
@@ -209,14 +209,14 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
   float4 y0 = make_float4(0.f, 0.f, 0.f, 0.f);
   if constexpr (MAXT > 0) {
     uint4 a[MAXT];
-    preload<MAXT>(Wp + (size_t)nt * nkt * 64, w * per, per, a);
+    preload<MAXT>(Wp + (size_t)nt * nkt * 64, w * per, per, a, gridDim.y == 1);
     if (ADD && out) y0 = *(const float4*)(Y + (size_t)r * ldy + n);
     acc = mma_pre<MAXT, (NW >= 16 && MAXT > 8) ? MAXT / 2 : MAXT>(a, w * per, per, xrow,
                                                                   f32x4_t{0.f, 0.f, 0.f, 0.f});
   } else {
     if (ADD && out) y0 = *(const float4*)(Y + (size_t)r * ldy + n);
     acc = sk_range<(NW >= 16 ? 4 : 8)>(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per, xrow,
-                                        f32x4_t{0.f, 0.f, 0.f, 0.f});
+                                        f32x4_t{0.f, 0.f, 0.f, 0.f}, gridDim.y == 1);
   }
   acc = block_acc_sum<NW>(acc, red);
   if (!out) return;
@@ -262,8 +262,9 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
     tb = ta;
   }
   uint4 a0[MAXT], a1[MAXT];
-  preload<MAXT>(Wp + (size_t)ta * nkt * 64, w * per, per, a0);
-  preload<MAXT>(Wp + (size_t)tb * nkt * 64, w * per, pair ? per : 0, a1);
+  const bool once = gridDim.y == 1;  // one row group: every tile is read once
+  preload<MAXT>(Wp + (size_t)ta * nkt * 64, w * per, per, a0, once);
+  preload<MAXT>(Wp + (size_t)tb * nkt * 64, w * per, pair ? per : 0, a1, once);
   // row bookkeeping and the RoPE factors of this lane's features, loaded
   // before the prologue so none of them waits on a reduction
   const int r0 = blockIdx.y * 16;
@@ -578,7 +579,8 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   // (above 10 tiles per wave the prologue runs first: 1024-thread blocks
   // have 128 registers per lane)
   if constexpr (MAXT > 10) norm_rows_lds<MTP_NV(MAXT)>(nloc, H, h, g, eps, xs, ldl);
-  preload<MAXT>(Wp + (size_t)(live ? strip : 0) * nkt * 64, qk * per, live ? per : 0, a);
+  preload<MAXT>(Wp + (size_t)(live ? strip : 0) * nkt * 64, qk * per, live ? per : 0, a,
+                gridDim.x == 1);
   const float bl = (bias && lane < E) ? bias[lane] : 0.f;
   if constexpr (MAXT <= 10) norm_rows_lds<MTP_NV(MAXT)>(nloc, H, h, g, eps, xs, ldl);
   __syncthreads();
@@ -696,8 +698,8 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
     U = base + (size_t)(I / 16 + it) * nkt * 64;
   }
   uint4 ag_[MAXT], au_[MAXT];
-  preload<MAXT>(G, w * per, per, ag_);
-  preload<MAXT>(U, w * per, per, au_);
+  preload<MAXT>(G, w * per, per, ag_, gridDim.z == 1);
+  preload<MAXT>(U, w * per, per, au_, gridDim.z == 1);
   if (cpb == 1) {  // one chunk (with the RMSNorm prologue when g != NULL)
     const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
     const uint16_t* xrow = nullptr;
@@ -827,7 +829,7 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
         row = t;
       }
     }
-    const f32x4_t a = sk_range<8>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    const f32x4_t a = sk_range<8>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f}, true);
     if (row >= 0) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += fx32(wt * a[q]);
@@ -908,7 +910,8 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
         wt = ent_w[o + t];
       }
     }
-    f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f},
+                           gridDim.z == 1);
     acc = block_acc_sum<4>(acc, red);
     if (w != 0 || t >= n) return;
     float4* dst =
@@ -918,7 +921,7 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
   }
   // several chunks: the wave's tiles (per <= 16) stay in registers
   uint4 a[16];
-  preload<16>(A, w * per, per, a);
+  preload<16>(A, w * per, per, a, gridDim.z == 1);
   for (int c = 0; c < cpb; ++c) {
     const int t0 = tb + 16 * c;
     if (t0 >= n) break;  // block-uniform
@@ -1023,7 +1026,7 @@ __global__ void __launch_bounds__(512) k_lm_gemm(int nr, int V, int H,
   for (int g = 0; g < NG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   uint4 a[KC];
 #pragma unroll
-  for (int u = 0; u < KC; ++u) a[u] = (live && u < nkt) ? A[(size_t)u * 64 + lane] : z;
+  for (int u = 0; u < KC; ++u) a[u] = (live && u < nkt) ? ld_tile(A + (size_t)u * 64 + lane, true) : z;
   for (int k0 = 0; k0 < nkt; k0 += KC) {
     __syncthreads();  // the previous chunk of xs is consumed
     for (int idx = threadIdx.x; idx < KC * NG * 64; idx += 512) {
@@ -1037,7 +1040,7 @@ __global__ void __launch_bounds__(512) k_lm_gemm(int nr, int V, int H,
     uint4 an[KC];
 #pragma unroll
     for (int u = 0; u < KC; ++u)
-      an[u] = (live && k0 + KC + u < nkt) ? A[(size_t)(k0 + KC + u) * 64 + lane] : z;
+      an[u] = (live && k0 + KC + u < nkt) ? ld_tile(A + (size_t)(k0 + KC + u) * 64 + lane, true) : z;
 #pragma unroll
     for (int kk = 0; kk < KC; ++kk) {
       if (k0 + kk < nkt) {
@@ -1143,7 +1146,7 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
       for (int t0 = 0; t0 < nkt; t0 += BT) {
         uint4 a[BT], b[RG][BT];
 #pragma unroll
-        for (int u = 0; u < BT; ++u) a[u] = t0 + u < nkt ? A[(size_t)(t0 + u) * 64 + lane] : z;
+        for (int u = 0; u < BT; ++u) a[u] = t0 + u < nkt ? ld_tile(A + (size_t)(t0 + u) * 64 + lane, true) : z;
 #pragma unroll
         for (int g = 0; g < RG; ++g)
 #pragma unroll
