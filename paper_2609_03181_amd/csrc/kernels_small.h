@@ -326,7 +326,8 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
 // ---------------------------------------------------------------- attention
 // One 64-key tile of K and V into registers: 16-byte chunk c = threadIdx.x
 // + 256u is key c / (DH/8), part c % (DH/8); keys past the capacity clamp
-// to the last row (their scores are masked).
+// to the last row (their scores are masked).  A launch reads each cached
+// row once, so the loads are non-temporal.
 template <int DH, int VPT>
 __device__ __forceinline__ void attn_load_tile(const uint16_t* __restrict__ Kc,
                                                const uint16_t* __restrict__ Vc, int t0, int cap,
@@ -335,8 +336,8 @@ __device__ __forceinline__ void attn_load_tile(const uint16_t* __restrict__ Kc,
   for (int u = 0; u < VPT; ++u) {
     const int c = threadIdx.x + 256 * u;
     const int j = min(t0 + c / (DH / 8), cap - 1);
-    kr[u] = *(const uint4*)(Kc + (size_t)j * DH + (c % (DH / 8)) * 8);
-    vr[u] = *(const uint4*)(Vc + (size_t)j * DH + (c % (DH / 8)) * 8);
+    kr[u] = ld_tile((const uint4*)(Kc + (size_t)j * DH + (c % (DH / 8)) * 8), true);
+    vr[u] = ld_tile((const uint4*)(Vc + (size_t)j * DH + (c % (DH / 8)) * 8), true);
   }
 }
 
