@@ -699,8 +699,9 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
     U = base + (size_t)(I / 16 + it) * nkt * 64;
   }
   uint4 ag_[MAXT], au_[MAXT];
-  preload<MAXT>(G, w * per, per, ag_, gridDim.z == 1);
-  preload<MAXT>(U, w * per, per, au_, gridDim.z == 1);
+  const bool once = n <= 16 * cpb;  // the expert's tiles are read by this block only
+  preload<MAXT>(G, w * per, per, ag_, once);
+  preload<MAXT>(U, w * per, per, au_, once);
   if (cpb == 1) {  // one chunk (with the RMSNorm prologue when g != NULL)
     const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
     const uint16_t* xrow = nullptr;
@@ -912,7 +913,7 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
       }
     }
     f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f},
-                           gridDim.z == 1);
+                           n <= 16);  // read by this block only
     acc = block_acc_sum<4>(acc, red);
     if (w != 0 || t >= n) return;
     float4* dst =
@@ -922,7 +923,7 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
   }
   // several chunks: the wave's tiles (per <= 16) stay in registers
   uint4 a[16];
-  preload<16>(A, w * per, per, a, gridDim.z == 1);
+  preload<16>(A, w * per, per, a, n <= 16 * cpb);  // read by this block only
   for (int c = 0; c < cpb; ++c) {
     const int t0 = tb + 16 * c;
     if (t0 >= n) break;  // block-uniform
