@@ -79,6 +79,15 @@ KERNEL_CLASSES = {  # timing-hook class -> kernel name as the profiler lists it
 }
 
 
+def class_kernel(kc, rows):
+    """Profiler name prefix of class kc's kernel for a verify pass of `rows`
+    rows (up to 16 rows the MoE gate/up runs in its persistent streaming
+    form)."""
+    if kc == 2 and rows <= 16:
+        return "mtp::k_s_gu_stream"
+    return KERNEL_CLASSES[kc][1]
+
+
 def class_cost(cfg, B, K, kv_len, draft_len, routes, kc):
     """Algorithmic HBM bytes and FLOPs of one step's launches of kernel
     class kc (every weight each launch touches read once, activations read
@@ -417,7 +426,8 @@ def main():
     # library around each launch of the class, eager steps on the same
     # stream), with the class's algorithmic bytes and FLOPs
     kernels = {}
-    for kc, (what, kname) in KERNEL_CLASSES.items():
+    for kc, (what, _) in KERNEL_CLASSES.items():
+        kname = class_kernel(kc, B * (K + 1))
         tot_ms = tot_b = tot_f = 0.0
         n_l = 0
         for _ in range(4):

@@ -753,6 +753,123 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
   }
 }
 
+// MoE gate/up for up to 16 rows, persistent streaming form.  Work items:
+// (touched routed expert, 16-wide intermediate tile) in touched-list order,
+// then the SI/16 tiles of the shared SwiGLU; block b takes items b,
+// b + gridDim.x, ...  The R rows are staged in LDS once.  K is split over
+// the 4 waves as in k_s_gu; as a wave's product consumes a weight tile, the
+// tile's registers are refilled with the block's next item, so the next
+// item's loads are in flight during this item's reduction and store (with
+// one block per item, blocks that do not fit on the machine at once start
+// only when a resident block has finished, after its loads have drained).
+// Sums are taken in the same order as k_s_gu's one-chunk path.
+template <int MAXT>
+__global__ void __launch_bounds__(256) k_s_gu_stream(int R, int H, int I, int SI,
+                                                     const uint16_t* __restrict__ xg,
+                                                     const uint4* __restrict__ egu,
+                                                     size_t e_stride,
+                                                     const uint4* __restrict__ sgu,
+                                                     const int32_t* __restrict__ cnt,
+                                                     const int32_t* __restrict__ off,
+                                                     const int32_t* __restrict__ ent_row,
+                                                     const int32_t* __restrict__ touched,
+                                                     const int32_t* __restrict__ n_touched,
+                                                     uint16_t* __restrict__ act,
+                                                     uint16_t* __restrict__ act_sh) {
+  extern __shared__ __align__(16) uint16_t xs[];  // [R][H + XPAD]
+  __shared__ f32x4_t red[2 * 4 * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nkt = H / 32, per = nkt / 4, ldl = H + XPAD, nI = I / 16;
+  const int nr = *n_touched * nI, nitems = nr + SI / 16;
+  int j = blockIdx.x;
+  if (j >= nitems) return;  // block-uniform
+  // item -> gate and up strips, expert (-1: shared) and tile
+  auto item = [&](int jj, const uint4*& G, const uint4*& U, int& e, int& it) {
+    if (jj < nr) {
+      e = touched[jj / nI];
+      it = jj % nI;
+      const uint4* base = egu + (size_t)e * e_stride;
+      G = base + (size_t)it * nkt * 64;
+      U = base + (size_t)(nI + it) * nkt * 64;
+    } else {
+      e = -1;
+      it = jj - nr;
+      G = sgu + (size_t)it * nkt * 64;
+      U = sgu + (size_t)(SI / 16 + it) * nkt * 64;
+    }
+  };
+  const uint4 *G, *U;
+  int e, it;
+  item(j, G, U, e, it);
+  // the rows' first 4 KB per wave are loaded before the tiles, so writing
+  // them to LDS does not wait on the tiles
+  const int nx = R * H / 8;  // 16-byte chunks of the rows
+  uint4 xv[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = threadIdx.x + q * 256;
+    xv[q] = c < nx ? ((const uint4*)xg)[c] : make_uint4(0, 0, 0, 0);
+  }
+  uint4 ag_[MAXT], au_[MAXT];
+  preload<MAXT>(G, w * per, per, ag_, true);
+  preload<MAXT>(U, w * per, per, au_, true);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = threadIdx.x + q * 256;
+    if (c < nx) *(uint4*)(xs + (c / (H / 8)) * ldl + (c % (H / 8)) * 8) = xv[q];
+  }
+  for (int c = threadIdx.x + 1024; c < nx; c += 256)
+    *(uint4*)(xs + (c / (H / 8)) * ldl + (c % (H / 8)) * 8) = ((const uint4*)xg)[c];
+  __syncthreads();
+  const int koff = 8 * (lane >> 4), t = lane & 15;
+  for (bool first = true;; first = false) {
+    const int jn = j + gridDim.x;
+    const bool more = jn < nitems;  // block-uniform
+    const uint4 *Gn = G, *Un = U;
+    int en = 0, itn = 0;
+    if (more) item(jn, Gn, Un, en, itn);
+    int n = R, o = 0;
+    if (e >= 0) {
+      n = cnt[e];
+      o = off[e];
+    }
+    const int row = t < n ? (e >= 0 ? ent_row[o + t] : t) : 0;
+    const uint16_t* xrow = xs + row * ldl;
+    if (!first) __syncthreads();  // red of the previous item is consumed
+    f32x4_t cg = {0.f, 0.f, 0.f, 0.f}, cu = cg;
+#pragma unroll
+    for (int u = 0; u < MAXT; ++u) {
+      if (u < per) {
+        const uint4 b = ldx(xrow + (w * per + u) * 32 + koff);
+        cg = mfma16(ag_[u], b, cg);
+        cu = mfma16(au_[u], b, cu);
+        if (more) {
+          ag_[u] = ld_tile(Gn + (size_t)(w * per + u) * 64 + lane, true);
+          au_[u] = ld_tile(Un + (size_t)(w * per + u) * 64 + lane, true);
+        }
+      }
+    }
+    cg = block_acc_sum<4>(cg, red);
+    cu = block_acc_sum<4>(cu, red + 4 * 64);
+    if (w == 0 && t < n) {
+      const int i = it * 16 + 4 * (lane >> 4);
+      uint2 pk;
+      pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
+      pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
+      if (e < 0)
+        *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
+      else
+        *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
+    }
+    if (!more) break;
+    j = jn;
+    G = Gn;
+    U = Un;
+    e = en;
+    it = itn;
+  }
+}
+
 // ---------------------------------------------------------------- MoE down
 // MoE down for up to 16 rows: grid (H/16 output strips, NG groups), 4
 // waves per block.  The virtual experts -- the touched routed experts in

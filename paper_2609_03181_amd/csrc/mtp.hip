@@ -41,6 +41,7 @@ struct mtp_ctx {
   Packed pk;     // bf16 models only
   int n_split;   // attention key splits ...
   int spl;       // ... of spl positions each (multiple of 64)
+  int n_cu;      // compute units of the device the context was created on
   Timing tm;
 };
 
@@ -164,6 +165,7 @@ struct Model {
   int n_split;
   int spl;
   Timing* tm;
+  int n_cu;              // compute units of the device (persistent grids)
   bool prefill = false;  // prefill calls launch the prefill-tagged kernel instances
 
   const T* wp(const void* p, size_t off_elems) const { return (const T*)p + off_elems; }
@@ -420,7 +422,16 @@ struct Model {
       if (G > 1)
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
                                    ws.ent_slot, ws.ent_w);
-      {
+      if (G == 1) {  // persistent streaming form: two blocks per compute unit
+        const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
+        const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
+#define MTP_GU(M)                                                                              \
+  launch_k(tm, MTP_KC_MOE_GU, k_s_gu_stream<M>, dim3(2 * n_cu), dim3(256), lds_rows(R, H), s, R, \
+           H, I, SI, (const uint16_t*)ws.xin, egu, pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, \
+           ws.touched, ws.n_touched, (uint16_t*)ws.act, ws.act_sh)
+        MTP_MAXT_DISPATCH(H / 128, MTP_GU);
+#undef MTP_GU
+      } else {
         const int cpb = G >= 8 ? 4 : 1;  // 16-entry chunks per block
         const dim3 grid(cdiv(SI > I ? SI : I, 16), E + 1, cdiv(G, cpb));
         const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
@@ -603,6 +614,16 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   ctx->w = *w;
   ctx->rope = nullptr;
   ctx->pk = Packed{};
+  {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ctx->n_cu, hipDeviceAttributeMultiprocessorCount, dev) !=
+            hipSuccess ||
+        ctx->n_cu < 1) {
+      delete ctx;
+      return MTP_EHIP;
+    }
+  }
   // key splits for decode attention: about 128 positions each, at most 64
   ctx->n_split = (c.max_ctx + 127) / 128;
   if (ctx->n_split > 64) ctx->n_split = 64;
@@ -699,7 +720,7 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
     m.prefill = true;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     for (int c0 = 0; c0 < n_rows; c0 += C) {
@@ -756,7 +777,7 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     // depth 1 over the catch-up rows; the last valid row starts the chain
@@ -796,7 +817,7 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
