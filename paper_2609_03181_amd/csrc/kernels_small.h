@@ -873,10 +873,10 @@ __global__ void __launch_bounds__(256) k_s_gu_stream(int R, int H, int I, int SI
 // ---------------------------------------------------------------- MoE down
 // MoE down for up to 16 rows: grid (H/16 output strips, NG groups), 4
 // waves per block.  The virtual experts -- the touched routed experts in
-// ascending id, then the S shared experts (width I each) -- go to wave slot
-// v % (4*NG); a wave streams each of its experts' strip tiles in
-// double-buffered batches and accumulates w * (Wd[n] . act) per row in LDS
-// (the expert lists are staged in LDS first).  The contributions
+// ascending id (the router's touched list), then the S shared experts
+// (width I each) -- go to wave slot v % (4*NG); a wave streams each of its
+// experts' strip tiles in double-buffered batches and accumulates
+// w * (Wd[n] . act) per row in LDS.  The contributions
 // w * (Wd[n] . act) are summed in 64-bit fixed point (2^-32 units): integer
 // addition is exact and associative, so a row's sum does not depend on
 // which wave or block handled which expert -- and hence not on the other
@@ -897,33 +897,22 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
                                                       const int32_t* __restrict__ off,
                                                       const int32_t* __restrict__ ent_row,
                                                       const float* __restrict__ ent_w,
+                                                      const int32_t* __restrict__ touched,
+                                                      const int32_t* __restrict__ n_touched,
                                                       unsigned long long* __restrict__ part,
                                                       int32_t* __restrict__ ctr,
                                                       float* __restrict__ h) {
   __shared__ long long acc_l[4][SR_MAX][17];
-  __shared__ int l_cnt[64], l_off[64], l_list[64], l_n, last;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __shared__ int last;
+  const int lane = threadIdx.x & 63;
+  // wave-uniform indices: the expert list, counts and offsets are read with
+  // scalar loads, so the first weight tiles are issued without waiting on a
+  // vector round trip
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nt = blockIdx.x, gq = blockIdx.y;
-  if (threadIdx.x < 64) {
-    const int e = threadIdx.x;
-    l_cnt[e] = e < E ? cnt[e] : 0;
-    l_off[e] = e < E ? off[e] : 0;
-  }
+  const int n_routed = *n_touched, nvirt = n_routed + S;
   for (int e = threadIdx.x; e < 4 * SR_MAX * 17; e += blockDim.x) (&acc_l[0][0][0])[e] = 0;
   __syncthreads();
-  if (w == 0) {  // compact list of touched experts, ascending id
-    const int has = l_cnt[lane] > 0;
-    int pre = has;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int v = __shfl_up(pre, d, MTP_WAVE);
-      if (lane >= d) pre += v;
-    }
-    if (has) l_list[pre - 1] = lane;
-    if (lane == 63) l_n = pre;
-  }
-  __syncthreads();
-  const int n_routed = l_n, nvirt = n_routed + S;
   const int nkt = I / 32;
   const int t = lane & 15;
   for (int v = gq * 4 + w; v < nvirt; v += NG * 4) {
@@ -932,8 +921,8 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
     int row = -1;
     float wt = 1.f;
     if (v < n_routed) {
-      const int e = l_list[v];
-      const int n = l_cnt[e], o = l_off[e];
+      const int e = touched[v];
+      const int n = cnt[e], o = off[e];
       A = edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
       if (t < n) {
         xrow = act + (size_t)(o + t) * I;

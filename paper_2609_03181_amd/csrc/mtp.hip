@@ -449,8 +449,8 @@ struct Model {
       if (small)
         launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_split<kDownSplit>, dim3(H / 16, kDownSplit),
                  dim3(256), 0, s, R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh, edn,
-                 pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.dn_part,
-                 ws.dn_ctr, ws.h);
+                 pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.touched,
+                 ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h);
       else {
         const int cpb_d = G >= 8 ? 4 : 1;
         launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot, dim3(H / 16, E + 1, cdiv(G, cpb_d)),
