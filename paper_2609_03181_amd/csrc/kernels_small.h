@@ -1247,7 +1247,7 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
   for (int g = 0; g < RG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (live) {
     if (RG == 1) {
-      acc[0] = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow[0], acc[0]);
+      acc[0] = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow[0], acc[0], true);
     } else {
       const uint4* A = Wp + (size_t)nt * nkt * 64;
       const uint4 z = make_uint4(0, 0, 0, 0);
