@@ -104,6 +104,139 @@ __global__ void k_chain_rows(int B, int d, int K, const int32_t* __restrict__ ro
   row_tok[b] = draft_tok[(size_t)b * K + d - 2];
 }
 
+// NV (float4 per lane of an H-row read by one wave) for n4 = H/256
+#define MTP_NV_DISPATCH(n4, F)     \
+  do {                             \
+    if ((n4) <= 2) { F(2); }       \
+    else if ((n4) <= 4) { F(4); }  \
+    else if ((n4) <= 5) { F(5); }  \
+    else { F(8); }                 \
+  } while (0)
+
+// FastMTP draft input of one row by one wave (bf16 model, H % 256 == 0,
+// H <= 256*NV): x[0..H) = N_e(e), x[H..2H) = N_h(a) rounded to bf16, with
+// e the embedding row (bf16; NULL: zero) and a the state row (float32;
+// NULL: zero).  Every load of the row is issued before the two sums.
+template <int NV>
+__device__ __forceinline__ void draft_in_wave(int H, const uint16_t* __restrict__ e,
+                                              const float* __restrict__ a,
+                                              const float* __restrict__ ge,
+                                              const float* __restrict__ gh, float eps,
+                                              uint16_t* __restrict__ x) {
+  const int lane = threadIdx.x & 63, n4 = H / 256;
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 ev[NV], av[NV], gev[NV], ghv[NV];
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    ev[u] = av[u] = gev[u] = ghv[u] = z;
+    if (u < n4) {
+      const int j4 = u * 64 + lane;  // float4 index within the row
+      if (e) {
+        const uint2 q = ((const uint2*)e)[j4];
+        ev[u] = make_float4(bf2f((uint16_t)q.x), bf2f((uint16_t)(q.x >> 16)),
+                            bf2f((uint16_t)q.y), bf2f((uint16_t)(q.y >> 16)));
+      }
+      if (a) av[u] = ((const float4*)a)[j4];
+      gev[u] = ((const float4*)ge)[j4];
+      ghv[u] = ((const float4*)gh)[j4];
+    }
+  }
+  float se = 0.f, sa = 0.f;
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    se += ev[u].x * ev[u].x + ev[u].y * ev[u].y + ev[u].z * ev[u].z + ev[u].w * ev[u].w;
+    sa += av[u].x * av[u].x + av[u].y * av[u].y + av[u].z * av[u].z + av[u].w * av[u].w;
+  }
+  se = wave_sum(se);
+  sa = wave_sum(sa);
+  const float re = rsqrtf(se / (float)H + eps), ra = rsqrtf(sa / (float)H + eps);
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    if (u < n4) {
+      const int j4 = u * 64 + lane;
+      uint2 pe, pa;
+      pe.x = (uint32_t)f2bf(ev[u].x * re * gev[u].x) | ((uint32_t)f2bf(ev[u].y * re * gev[u].y) << 16);
+      pe.y = (uint32_t)f2bf(ev[u].z * re * gev[u].z) | ((uint32_t)f2bf(ev[u].w * re * gev[u].w) << 16);
+      pa.x = (uint32_t)f2bf(av[u].x * ra * ghv[u].x) | ((uint32_t)f2bf(av[u].y * ra * ghv[u].y) << 16);
+      pa.y = (uint32_t)f2bf(av[u].z * ra * ghv[u].z) | ((uint32_t)f2bf(av[u].w * ra * ghv[u].w) << 16);
+      ((uint2*)x)[j4] = pe;
+      ((uint2*)(x + H))[j4] = pa;
+    }
+  }
+}
+
+// k_draft_rows and the draft input of its rows in one launch (bf16 model):
+// one 64-thread block per row r = b*C + i; state row a[b*a_ld + i*H].
+// Same bookkeeping, checks and zeroing as k_draft_rows; x[r] (2H bf16) as
+// k_draft_in.  Tokens outside the vocabulary set MTP_ETOKEN (zero row).
+template <int NV>
+__global__ void __launch_bounds__(64) k_draft_rows_in(
+    int B, int C, const int32_t* __restrict__ row_pos_in, const int32_t* __restrict__ n_rows,
+    const int32_t* __restrict__ next_tok, int cap, int H, int V,
+    const uint16_t* __restrict__ embed, const float* __restrict__ a, size_t a_ld,
+    const float* __restrict__ ge, const float* __restrict__ gh, float eps,
+    int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
+    int32_t* __restrict__ head_row, int32_t* __restrict__ row_tok,
+    int32_t* __restrict__ draft_len, int32_t* __restrict__ status, int32_t* __restrict__ zero,
+    int n_zero, uint16_t* __restrict__ x) {
+  const int r = blockIdx.x, lane = threadIdx.x;
+  for (int zi = r * 64 + lane; zi < n_zero; zi += gridDim.x * 64) zero[zi] = 0;
+  if (r >= B * C) return;
+  const int b = r / C, i = r - b * C;
+  const int p0 = row_pos_in[b], p = p0 + i, nr = n_rows[b];
+  const int t = next_tok[(size_t)b * C + i];
+  int nv = nr;
+  if (nv < 0 || nv > C) nv = nv < 0 ? 0 : C;
+  int valid = i < nv;
+  if (valid && (p < 0 || p >= cap)) valid = 0;
+  const bool bad = valid && (t < 0 || t >= V);
+  if (lane == 0) {
+    if (nr != nv || (i < nv && !valid)) set_status(status, MTP_ECAPACITY);
+    if (bad) set_status(status, MTP_ETOKEN);
+    row_pos[r] = p;
+    row_valid[r] = valid;
+    row_tok[r] = t;
+    if (i == (nv > 0 ? nv - 1 : 0)) head_row[b] = r;
+    if (i == 0) {
+      if (p0 > draft_len[b]) set_status(status, MTP_ECAPACITY);
+      draft_len[b] = p0 + nr;
+    }
+  }
+  const uint16_t* e = (valid && !bad) ? embed + (size_t)t * H : nullptr;
+  const float* ar = valid ? a + (size_t)b * a_ld + (size_t)i * H : nullptr;
+  draft_in_wave<NV>(H, e, ar, ge, gh, eps, x + (size_t)r * 2 * H);
+}
+
+// k_chain_rows and the draft input of its rows in one launch (bf16 model):
+// one 64-thread block per sequence; state row a[b*H].
+template <int NV>
+__global__ void __launch_bounds__(64) k_chain_rows_in(
+    int B, int d, int K, const int32_t* __restrict__ row_pos_in,
+    const int32_t* __restrict__ n_rows, const int32_t* __restrict__ draft_tok, int cap, int H,
+    int V, const uint16_t* __restrict__ embed, const float* __restrict__ a,
+    const float* __restrict__ ge, const float* __restrict__ gh, float eps,
+    int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
+    int32_t* __restrict__ head_row, int32_t* __restrict__ row_tok, int32_t* __restrict__ status,
+    uint16_t* __restrict__ x) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  if (b >= B) return;
+  const int p = row_pos_in[b] + n_rows[b] - 1 + (d - 1);
+  const int t = draft_tok[(size_t)b * K + d - 2];
+  const int valid = p >= 0 && p < cap;
+  const bool bad = valid && (t < 0 || t >= V);
+  if (lane == 0) {
+    if (!valid) set_status(status, MTP_ECAPACITY);
+    if (bad) set_status(status, MTP_ETOKEN);
+    row_pos[b] = p;
+    row_valid[b] = valid;
+    head_row[b] = b;
+    row_tok[b] = t;
+  }
+  const uint16_t* e = (valid && !bad) ? embed + (size_t)t * H : nullptr;
+  const float* ar = valid ? a + (size_t)b * H : nullptr;
+  draft_in_wave<NV>(H, e, ar, ge, gh, eps, x + (size_t)b * 2 * H);
+}
+
 // Loads input row r (token embedding, or a vision row when the token is
 // negative) as float32 into smem[0..H).  Vision row of (b, i):
 // vision[((size_t)b*vis_ld + vis_off + i)*H].  Invalid rows and bad tokens

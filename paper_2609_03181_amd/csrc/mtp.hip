@@ -255,12 +255,14 @@ struct Model {
   // a + b*a_ld + i*H) and inputs from ws.row_tok / vision.  With a head,
   // the last valid row of each sequence gives ws.ustate[b] (its u) and its
   // greedy token at tok[b*ostride + ooff].
+  // xin_ready (bf16 model): the caller has written the draft input rows to
+  // ws.xin already (row setup fused with the draft input)
   void draft(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision, int vis_ld,
              int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
-             size_t ldl) {
+             size_t ldl, bool xin_ready = false) {
     if constexpr (BF) {
       draft_mfma(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
-                 logits, ldl);
+                 logits, ldl, xin_ready);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -474,15 +476,15 @@ struct Model {
 
   void draft_mfma(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
                   int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
-                  float* logits, size_t ldl) {
+                  float* logits, size_t ldl, bool xin_ready) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int F = c.draft_inter;
     const float eps = (float)c.rms_eps;
     const size_t seq_stride = (size_t)2 * nh * c.max_ctx * dh;
-    k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(C, H, c.vocab, ws.row_valid, ws.row_tok,
-                                                         (const T*)w.embed, vision, vis_ld,
-                                                         vis_off, a, a_ld, w.d_enorm, w.d_hnorm,
-                                                         eps, (T*)ws.xin, ws.status);
+    if (!xin_ready)
+      k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(
+          C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed, vision, vis_ld, vis_off, a,
+          a_ld, w.d_enorm, w.d_hnorm, eps, (T*)ws.xin, ws.status);
     smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
     // Up to 16 rows the products normalise their rows in a prologue; with
     // several row groups the rows are normalised once (bf16, into xin) and
@@ -780,21 +782,46 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
     Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
+    const float eps = (float)c.rms_eps;
+    const int n4 = H / 256;  // float4 per lane of a row (bf16 model)
     // depth 1 over the catch-up rows; the last valid row starts the chain
-    k_draft_rows<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, n_rows, next_tok, c.max_ctx,
-                                               w.row_pos, w.row_valid, w.head_row, w.row_tok,
-                                               draft_len, w.status, w.att_ctr, w.n_ctr);
+    if constexpr (BF) {
+#define MTP_DRI(NV)                                                                          \
+  k_draft_rows_in<NV><<<R, 64, 0, s>>>(batch, C, row_pos, n_rows, next_tok, c.max_ctx, H, V, \
+                                       (const uint16_t*)ctx->w.embed, hid, (size_t)C * H,     \
+                                       ctx->w.d_enorm, ctx->w.d_hnorm, eps, w.row_pos,        \
+                                       w.row_valid, w.head_row, w.row_tok, draft_len, w.status, \
+                                       w.att_ctr, w.n_ctr, (uint16_t*)w.xin)
+      MTP_NV_DISPATCH(n4, MTP_DRI);
+#undef MTP_DRI
+    } else {
+      k_draft_rows<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, n_rows, next_tok, c.max_ctx,
+                                                 w.row_pos, w.row_valid, w.head_row, w.row_tok,
+                                                 draft_len, w.status, w.att_ctr, w.n_ctr);
+    }
     m.draft(w, batch, C, hid, (size_t)C * H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k, 0,
-            draft_logits, (size_t)k * V);
+            draft_logits, (size_t)k * V, BF);
     // depth d = 2..k: one row at (row_pos + n_rows - 1) + (d - 1), state u
     // of depth d-1 (read by the draft input before the head rewrites it),
     // input the depth d-1 draft token
     for (int d = 2; d <= k; ++d) {
-      k_chain_rows<<<cdiv(batch, 256), 256, 0, s>>>(batch, d, k, row_pos, n_rows, draft_tok,
-                                                     c.max_ctx, w.row_pos, w.row_valid,
-                                                     w.head_row, w.row_tok, w.status);
+      if constexpr (BF) {
+#define MTP_CRI(NV)                                                                           \
+  k_chain_rows_in<NV><<<batch, 64, 0, s>>>(batch, d, k, row_pos, n_rows, draft_tok, c.max_ctx, \
+                                           H, V, (const uint16_t*)ctx->w.embed, w.ustate,       \
+                                           ctx->w.d_enorm, ctx->w.d_hnorm, eps, w.row_pos,      \
+                                           w.row_valid, w.head_row, w.row_tok, w.status,        \
+                                           (uint16_t*)w.xin)
+        MTP_NV_DISPATCH(n4, MTP_CRI);
+#undef MTP_CRI
+      } else {
+        k_chain_rows<<<cdiv(batch, 256), 256, 0, s>>>(batch, d, k, row_pos, n_rows, draft_tok,
+                                                       c.max_ctx, w.row_pos, w.row_valid,
+                                                       w.head_row, w.row_tok, w.status);
+      }
       m.draft(w, batch, 1, w.ustate, (size_t)H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k,
-              d - 1, draft_logits ? draft_logits + (size_t)(d - 1) * V : nullptr, (size_t)k * V);
+              d - 1, draft_logits ? draft_logits + (size_t)(d - 1) * V : nullptr, (size_t)k * V,
+              BF);
     }
     return launch_status();
   };
