@@ -147,14 +147,16 @@ __device__ __forceinline__ f32x4_t block_acc_sum(f32x4_t acc, f32x4_t* red) {
 // with gain g into LDS xs[r][ldl] (bf16).  Wave w takes rows w, w+nw, ...;
 // each row and the gain are loaded together, before the row's reduction,
 // so no load waits on a reduction.
+// With skip_first, each wave starts at its second row (its first was done
+// by norm_row_load / norm_row_store).
 template <int NV>
 __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restrict__ src,
                                               const float* __restrict__ g, float eps,
-                                              uint16_t* xs, int ldl) {
+                                              uint16_t* xs, int ldl, bool skip_first = false) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int n4 = H / 256;  // float4 per lane
   const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int r = w; r < R; r += nw) {
+  for (int r = w + (skip_first ? nw : 0); r < R; r += nw) {
     float4 xv[NV], gv[NV];
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
@@ -177,6 +179,48 @@ __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restr
                ((uint32_t)f2bf(xv[u].w * rinv * gv[u].w) << 16);
         *(uint2*)(xs + r * ldl + (u * 64 + lane) * 4) = pk;
       }
+    }
+  }
+}
+
+// One row of the same RMSNorm held in registers: its loads can be issued
+// before a kernel's weight tiles, so the row's sum is formed while the
+// tiles are in flight (the result is that of norm_rows_lds).
+template <int NV>
+struct NormRow {
+  float4 x[NV], g[NV];
+};
+template <int NV>
+__device__ __forceinline__ void norm_row_load(int H, const float* __restrict__ src,
+                                              const float* __restrict__ g, NormRow<NV>& nr) {
+  const int lane = threadIdx.x & 63, n4 = H / 256;
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    nr.x[u] = u < n4 ? ((const float4*)src)[u * 64 + lane] : z;
+    nr.g[u] = u < n4 ? ((const float4*)g)[u * 64 + lane] : z;
+  }
+}
+template <int NV>
+__device__ __forceinline__ void norm_row_store(int H, float eps, const NormRow<NV>& nr,
+                                               uint16_t* dst) {
+  const int lane = threadIdx.x & 63, n4 = H / 256;
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < NV; ++u)
+    ss += nr.x[u].x * nr.x[u].x + nr.x[u].y * nr.x[u].y + nr.x[u].z * nr.x[u].z +
+          nr.x[u].w * nr.x[u].w;
+  ss = wave_sum(ss);
+  const float rinv = rsqrtf(ss / (float)H + eps);
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    if (u < n4) {
+      uint2 pk;
+      pk.x = (uint32_t)f2bf(nr.x[u].x * rinv * nr.g[u].x) |
+             ((uint32_t)f2bf(nr.x[u].y * rinv * nr.g[u].y) << 16);
+      pk.y = (uint32_t)f2bf(nr.x[u].z * rinv * nr.g[u].z) |
+             ((uint32_t)f2bf(nr.x[u].w * rinv * nr.g[u].w) << 16);
+      *(uint2*)(dst + (u * 64 + lane) * 4) = pk;
     }
   }
 }
@@ -231,7 +275,7 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
 // block computes x = RMSNorm(h; g) of its rows into LDS (the prologue
 // overlaps the weight fetch) -- or, with xg, reads normalised bf16 rows.
 // q -> q_out (float32), k/v -> cache at the row position.
-template <int MAXT>
+template <int MAXT, bool EARLY = false>
 __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int dh,
                                                const float* __restrict__ h,
                                                const float* __restrict__ g, float eps,
@@ -261,14 +305,20 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
     ta = 2 * D / 16 + (task - n_pair);
     tb = ta;
   }
+  constexpr int NV = MTP_NV(MAXT);
+  const int r0 = blockIdx.y * 16;
+  const int nloc = min(16, R - r0);
+  // EARLY (prologue mode): each wave's first row is loaded ahead of the
+  // weight tiles and normalised while they are in flight
+  NormRow<NV> nr0;
+  const bool early = EARLY && !xg && w < nloc;
+  if (early) norm_row_load<NV>(H, h + (size_t)(r0 + w) * H, g, nr0);
   uint4 a0[MAXT], a1[MAXT];
   const bool once = gridDim.y == 1;  // one row group: every tile is read once
   preload<MAXT>(Wp + (size_t)ta * nkt * 64, w * per, per, a0, once);
   preload<MAXT>(Wp + (size_t)tb * nkt * 64, w * per, pair ? per : 0, a1, once);
   // row bookkeeping and the RoPE factors of this lane's features, loaded
   // before the prologue so none of them waits on a reduction
-  const int r0 = blockIdx.y * 16;
-  const int nloc = min(16, R - r0);
   const int r = r0 + (lane & 15);
   const int valid = r < R ? row_valid[r] : 0;
   const int pos = r < R ? row_pos[r] : 0;
@@ -282,7 +332,8 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
   if (xg) {
     if (r < R) xrow = xg + (size_t)r * H;
   } else {
-    norm_rows_lds<MTP_NV(MAXT)>(nloc, H, h + (size_t)r0 * H, g, eps, xs, ldl);
+    if (early) norm_row_store<NV>(H, eps, nr0, xs + w * ldl);
+    norm_rows_lds<NV>(nloc, H, h + (size_t)r0 * H, g, eps, xs, ldl, EARLY);
     __syncthreads();
     if (r < R) xrow = xs + (lane & 15) * ldl;
   }
@@ -663,7 +714,7 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
 // instance (so profiles separate decode from prefill launches); the draft
 // roles are the dense-only form (the draft block's FFN, launched with E = 0).
 enum { GU_VERIFY = 0, GU_DRAFT = 1, GU_PREFILL = 2, GU_DRAFT_PREFILL = 3 };
-template <int ROLE, int MAXT>
+template <int ROLE, int MAXT, bool EARLY = false>
 __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int I, int SI,
                                               const uint16_t* __restrict__ xg,
                                               const float* __restrict__ h,
@@ -698,6 +749,12 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
     G = base + (size_t)it * nkt * 64;
     U = base + (size_t)(I / 16 + it) * nkt * 64;
   }
+  constexpr int NV = MTP_NV(MAXT);
+  // EARLY (draft roles, prologue mode, one chunk): each wave's first row is
+  // loaded ahead of the weight tiles and normalised while they are in flight
+  NormRow<NV> nr0;
+  const bool early = EARLY && (ROLE & 1) != 0 && g && cpb == 1 && w < min(16, n - tb);
+  if (early) norm_row_load<NV>(H, h + (size_t)(tb + w) * H, g, nr0);
   uint4 ag_[MAXT], au_[MAXT];
   const bool once = n <= 16 * cpb;  // the expert's tiles are read by this block only
   preload<MAXT>(G, w * per, per, ag_, once);
@@ -706,7 +763,8 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
     const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
     const uint16_t* xrow = nullptr;
     if ((ROLE & 1) != 0 && g) {  // draft roles, few rows: RMSNorm(h; g) prologue
-      norm_rows_lds<MTP_NV(MAXT)>(min(16, n - t0), H, h + (size_t)t0 * H, g, eps, xs, ldl);
+      if (early) norm_row_store<NV>(H, eps, nr0, xs + w * ldl);
+      norm_rows_lds<NV>(min(16, n - t0), H, h + (size_t)t0 * H, g, eps, xs, ldl, EARLY);
       __syncthreads();
       if (t < n) xrow = xs + (lane & 15) * ldl;
     } else if (t < n) {

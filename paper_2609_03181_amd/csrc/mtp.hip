@@ -348,7 +348,8 @@ struct Model {
                  const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
 #define MTP_QKV(M)                                                                          \
-  launch_k(tm, MTP_KC_QKV, k_s_qkv<M>, dim3(D / 8, groups(R)), dim3(256),                   \
+  launch_k(tm, MTP_KC_QKV, (!xg && groups(R) == 1) ? k_s_qkv<M, true> : k_s_qkv<M, false>,   \
+           dim3(D / 8, groups(R)), dim3(256),                                                 \
            xg ? 0 : lds_rows(R, H), s, R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv, \
            rope, ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q)
     MTP_MAXT_DISPATCH(H / 128, MTP_QKV);
@@ -502,7 +503,8 @@ struct Model {
     const int cpb = G >= 8 ? 4 : 1;
 #define MTP_DFFN(M)                                                                           \
   launch_k(tm, MTP_KC_DRAFT_FFN,                                                              \
-           prefill ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT, M>,                       \
+           prefill ? (pre ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT_PREFILL, M, true>)  \
+                   : (pre ? k_s_gu<GU_DRAFT, M> : k_s_gu<GU_DRAFT, M, true>),                 \
            dim3(F / 16, 1, cdiv(G, cpb)), dim3(256), pre ? 0 : lds_rows(R, H), s, cpb, R, H, 0, \
            F, F, xn, pre ? nullptr : ws.h, pre ? nullptr : w.d_ffn_norm, eps, nullptr, 0,       \
            pk.d_gu, nullptr, nullptr, nullptr, nullptr, ws.act_sh)
