@@ -144,10 +144,10 @@ def _traffic(workload, kernel):
     or None when none were taken for this workload or the library sources
     changed since."""
     try:
-        t = json.load(open(TRAFFIC_FILE))[workload]
-    except (OSError, KeyError, ValueError):
+        t = json.load(open(TRAFFIC_FILE))[workload][kernel]
+    except (OSError, KeyError, ValueError, TypeError):
         return None
-    if t.get("src_hash") != src_hash() or t.get("kernel") != kernel:
+    if t.get("src_hash") != src_hash():
         return None
     return t["bytes_per_launch"]
 
@@ -206,10 +206,14 @@ def traffic_from(workload, kernel, fetch_csv, write_csv, copy_fetch_csv, copy_wr
         d = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         d = {}
-    d[workload] = entry
+    # per workload, one entry per kernel; entries of other sources are dropped
+    w = {k: v for k, v in d.get(workload, {}).items()
+         if isinstance(v, dict) and v.get("src_hash") == entry["src_hash"]}
+    w[kernel] = entry
+    d[workload] = w
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(d, fh, indent=1)
-    print(json.dumps({workload: entry}))
+    print(json.dumps({workload: {kernel: entry}}))
 
 
 def copy_calibration():
