@@ -4,6 +4,8 @@ whole step captured in a HIP graph and replayed), on sampled sequences the
 oracle recomputes one by one:
 
 * batch 1: real prefill of 256 vision rows + 512 prompt tokens, then steps;
+* batch 4: cached contexts U{512..1024} (seed 5), synthetic caches (16
+  verify rows: one full row group);
 * batch 16: cached contexts U{1024..2048} (seed 2), synthetic caches;
 * batch 64: cached contexts U{512..4096} (seed 12), Zipf(1.1) router bias,
   synthetic caches.
@@ -126,6 +128,14 @@ def test_full_shape_batch1_spec_equals_greedy_bitwise(plain):
     for K in (1, 3):
         assert outs[K] == outs[0]
         assert torch.equal(kvs[K][1][..., :n, :], kvs[0][1][..., :n, :])
+
+
+def test_full_shape_batch4_sixteen_rows_sampled_sequences(plain):
+    """Batch 4: 16 verify rows, one full row group -- the streaming MoE
+    gate/up stages 16 rows of 1280 (beyond its first 1024 16-byte chunks
+    per block) and the RMSNorm prologues take four rows per wave."""
+    w, model, orc = plain
+    _synthetic_case(w, model, orc, 4, 512, 1024, 5, 3)
 
 
 def test_full_shape_batch16_sampled_sequences(plain):
