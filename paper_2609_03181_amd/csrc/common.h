@@ -101,6 +101,68 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   return t;
 }
 
+// Greedy-argmax reduction step: (best value, lowest id on ties, second
+// best value) of two partial results.
+__device__ __forceinline__ void argmax_combine(float& bv, float& sv, int& bi, float v, float s,
+                                               int i) {
+  if (v > bv || (v == bv && i < bi)) {
+    sv = fmaxf(bv, s);
+    bv = v;
+    bi = i;
+  } else {
+    sv = fmaxf(sv, v);
+  }
+}
+
+// Argmax of row r over its nblk LM-head partials (pv/pi/p2 at
+// r*nblk + j) by a 256-thread block: each thread loads its up to 8
+// partials per round before combining them (all loads in flight), then a
+// wave and a block reduction.  The token is returned (and the best and
+// second best values stored) in thread 0.
+__device__ __forceinline__ int argmax_row(int r, int nblk, const float* __restrict__ pv,
+                                          const int32_t* __restrict__ pi,
+                                          const float* __restrict__ p2, float* best = nullptr,
+                                          float* second = nullptr) {
+  __shared__ float wb[4], ws2[4];
+  __shared__ int wi[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float bv = -INFINITY, sv = -INFINITY;
+  int bi = 1 << 30;
+  for (int j0 = 0; j0 < nblk; j0 += 256 * 8) {
+    float v[8], s[8];
+    int id[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u * 256 + threadIdx.x;
+      const size_t o = (size_t)r * nblk + j;
+      const bool ok = j < nblk;
+      v[u] = ok ? pv[o] : -INFINITY;
+      s[u] = ok ? p2[o] : -INFINITY;
+      id[u] = ok ? pi[o] : (1 << 30);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) argmax_combine(bv, sv, bi, v[u], s[u], id[u]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, MTP_WAVE), os = __shfl_xor(sv, o, MTP_WAVE);
+    const int oi = __shfl_xor(bi, o, MTP_WAVE);
+    argmax_combine(bv, sv, bi, ov, os, oi);
+  }
+  if (lane == 0) {
+    wb[w] = bv;
+    ws2[w] = sv;
+    wi[w] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int x = 1; x < 4; ++x) argmax_combine(bv, sv, bi, wb[x], ws2[x], wi[x]);
+    if (best) *best = bv;
+    if (second) *second = sv;
+  }
+  return bi;
+}
+
 // Wait for this wave's outstanding LDS operations only (lgkmcnt(0); vmcnt
 // and expcnt at their maxima, so global loads in flight keep flying).
 // Used with a wave barrier when a wave reads back LDS it has just written.

@@ -208,20 +208,33 @@ __global__ void __launch_bounds__(64) k_draft_rows_in(
 }
 
 // k_chain_rows and the draft input of its rows in one launch (bf16 model):
-// one 64-thread block per sequence; state row a[b*H].
+// one 256-thread block per sequence; state row a[b*H].  The depth d-1
+// token is first reduced from the LM head's nblk partials of row b
+// (pv/pi/p2 as k_argmax_final reads them) and stored to
+// draft_tok[b*K + d-2]; then wave 0 sets up the row and its draft input.
 template <int NV>
-__global__ void __launch_bounds__(64) k_chain_rows_in(
+__global__ void __launch_bounds__(256) k_chain_rows_in(
     int B, int d, int K, const int32_t* __restrict__ row_pos_in,
-    const int32_t* __restrict__ n_rows, const int32_t* __restrict__ draft_tok, int cap, int H,
-    int V, const uint16_t* __restrict__ embed, const float* __restrict__ a,
+    const int32_t* __restrict__ n_rows, int nblk, const float* __restrict__ pv,
+    const int32_t* __restrict__ pi, const float* __restrict__ p2,
+    int32_t* __restrict__ draft_tok, int cap, int H, int V,
+    const uint16_t* __restrict__ embed, const float* __restrict__ a,
     const float* __restrict__ ge, const float* __restrict__ gh, float eps,
     int32_t* __restrict__ row_pos, int32_t* __restrict__ row_valid,
     int32_t* __restrict__ head_row, int32_t* __restrict__ row_tok, int32_t* __restrict__ status,
     uint16_t* __restrict__ x) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+  __shared__ int tok_s;
+  const int b = blockIdx.x, lane = threadIdx.x & 63;
   if (b >= B) return;
+  const int tr = argmax_row(b, nblk, pv, pi, p2);  // valid in thread 0
+  if (threadIdx.x == 0) {
+    draft_tok[(size_t)b * K + d - 2] = tr;
+    tok_s = tr;
+  }
+  __syncthreads();
+  if (threadIdx.x >= 64) return;
   const int p = row_pos_in[b] + n_rows[b] - 1 + (d - 1);
-  const int t = draft_tok[(size_t)b * K + d - 2];
+  const int t = tok_s;
   const int valid = p >= 0 && p < cap;
   const bool bad = valid && (t < 0 || t >= V);
   if (lane == 0) {

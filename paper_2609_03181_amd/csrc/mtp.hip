@@ -257,12 +257,14 @@ struct Model {
   // greedy token at tok[b*ostride + ooff].
   // xin_ready (bf16 model): the caller has written the draft input rows to
   // ws.xin already (row setup fused with the draft input)
+  // defer_argmax (bf16 model): the head's token reduction is left to the
+  // next depth's row setup
   void draft(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision, int vis_ld,
              int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
-             size_t ldl, bool xin_ready = false) {
+             size_t ldl, bool xin_ready = false, bool defer_argmax = false) {
     if constexpr (BF) {
       draft_mfma(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
-                 logits, ldl, xin_ready);
+                 logits, ldl, xin_ready, defer_argmax);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -360,8 +362,13 @@ struct Model {
   }
 
   // LM head over nr rows of ws.xhead (bf16, normalised), greedy argmax
+  // LM-head partials per row (blocks of the launch lm_mfma makes for nr rows)
+  unsigned lm_partials(int nr) const {
+    return groups(nr) >= 4 ? cdiv(c.vocab, 128) : cdiv(cdiv(c.vocab, 16), 4);
+  }
+  // defer_argmax: the partials are left in ws.pv/pi/p2 for the next kernel
   void lm_mfma(const Ws& ws, int nr, float* logits, size_t ldl, int per, int ostride, int ooff,
-               int32_t* tok, float* margin) {
+               int32_t* tok, float* margin, bool defer_argmax = false) {
     const int V = c.vocab, H = c.hidden;
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
     const unsigned G = groups(nr);
@@ -383,8 +390,9 @@ struct Model {
       launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<1>, dim3(nblk, G), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
     }
-    k_argmax_final<<<nr, 256, 0, s>>>(nr, nb, ws.pv, ws.pi, ws.p2, per, ostride, ooff,
-                                               tok, margin);
+    if (!defer_argmax)
+      k_argmax_final<<<nr, 256, 0, s>>>(nr, nb, ws.pv, ws.pi, ws.p2, per, ostride, ooff, tok,
+                                        margin);
   }
 
   void verifier_mfma(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
@@ -477,7 +485,7 @@ struct Model {
 
   void draft_mfma(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
                   int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
-                  float* logits, size_t ldl, bool xin_ready) {
+                  float* logits, size_t ldl, bool xin_ready, bool defer_argmax) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int F = c.draft_inter;
     const float eps = (float)c.rms_eps;
@@ -514,7 +522,7 @@ struct Model {
     if (!head) return;
     k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
                                     (T*)ws.xhead, H, 0);
-    lm_mfma(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr);
+    lm_mfma(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr, defer_argmax);
   }
 };
 
@@ -802,18 +810,20 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
                                                  draft_len, w.status, w.att_ctr, w.n_ctr);
     }
     m.draft(w, batch, C, hid, (size_t)C * H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k, 0,
-            draft_logits, (size_t)k * V, BF);
+            draft_logits, (size_t)k * V, BF, BF && k > 1);
+    const unsigned nbp = m.lm_partials(batch);
     // depth d = 2..k: one row at (row_pos + n_rows - 1) + (d - 1), state u
     // of depth d-1 (read by the draft input before the head rewrites it),
     // input the depth d-1 draft token
     for (int d = 2; d <= k; ++d) {
       if constexpr (BF) {
 #define MTP_CRI(NV)                                                                           \
-  k_chain_rows_in<NV><<<batch, 64, 0, s>>>(batch, d, k, row_pos, n_rows, draft_tok, c.max_ctx, \
-                                           H, V, (const uint16_t*)ctx->w.embed, w.ustate,       \
-                                           ctx->w.d_enorm, ctx->w.d_hnorm, eps, w.row_pos,      \
-                                           w.row_valid, w.head_row, w.row_tok, w.status,        \
-                                           (uint16_t*)w.xin)
+  k_chain_rows_in<NV><<<batch, 256, 0, s>>>(batch, d, k, row_pos, n_rows, (int)nbp, w.pv, w.pi, \
+                                            w.p2, draft_tok, c.max_ctx, H, V,                  \
+                                            (const uint16_t*)ctx->w.embed, w.ustate,           \
+                                            ctx->w.d_enorm, ctx->w.d_hnorm, eps, w.row_pos,    \
+                                            w.row_valid, w.head_row, w.row_tok, w.status,      \
+                                            (uint16_t*)w.xin)
         MTP_NV_DISPATCH(n4, MTP_CRI);
 #undef MTP_CRI
       } else {
@@ -823,7 +833,7 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
       }
       m.draft(w, batch, 1, w.ustate, (size_t)H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k,
               d - 1, draft_logits ? draft_logits + (size_t)(d - 1) * V : nullptr, (size_t)k * V,
-              BF);
+              BF, BF && d < k);
     }
     return launch_status();
   };
