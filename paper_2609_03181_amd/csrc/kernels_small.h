@@ -225,6 +225,43 @@ __device__ __forceinline__ void norm_row_store(int H, float eps, const NormRow<N
   }
 }
 
+// RMSNorm of rows x[idx ? idx[o] : o] (float32, row stride H) with gain
+// g, one wave per output row o, every load issued before the sum: float32
+// to yf[o*H] and/or bf16 to yb[o*H] (each optional).
+template <int NV>
+__global__ void __launch_bounds__(64) k_norm_rows(int H, const float* __restrict__ x,
+                                                  const int32_t* __restrict__ idx,
+                                                  const float* __restrict__ g, float eps,
+                                                  float* __restrict__ yf,
+                                                  uint16_t* __restrict__ yb) {
+  const int o = blockIdx.x, lane = threadIdx.x, n4 = H / 256;
+  const int r = idx ? idx[o] : o;
+  NormRow<NV> nr;
+  norm_row_load<NV>(H, x + (size_t)r * H, g, nr);
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < NV; ++u)
+    ss += nr.x[u].x * nr.x[u].x + nr.x[u].y * nr.x[u].y + nr.x[u].z * nr.x[u].z +
+          nr.x[u].w * nr.x[u].w;
+  ss = wave_sum(ss);
+  const float rinv = rsqrtf(ss / (float)H + eps);
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    if (u < n4) {
+      const float4 y = make_float4(nr.x[u].x * rinv * nr.g[u].x, nr.x[u].y * rinv * nr.g[u].y,
+                                   nr.x[u].z * rinv * nr.g[u].z, nr.x[u].w * rinv * nr.g[u].w);
+      const int j4 = u * 64 + lane;
+      if (yf) ((float4*)(yf + (size_t)o * H))[j4] = y;
+      if (yb) {
+        uint2 pk;
+        pk.x = (uint32_t)f2bf(y.x) | ((uint32_t)f2bf(y.y) << 16);
+        pk.y = (uint32_t)f2bf(y.z) | ((uint32_t)f2bf(y.w) << 16);
+        ((uint2*)(yb + (size_t)o * H))[j4] = pk;
+      }
+    }
+  }
+}
+
 // float4 per lane of a row for the register tile count MAXT (= H/128
 // rounded up): H/256 <= (MAXT+1)/2
 #define MTP_NV(MAXT) (((MAXT) + 1) / 2)

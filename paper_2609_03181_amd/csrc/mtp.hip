@@ -362,6 +362,16 @@ struct Model {
   }
 
   // LM head over nr rows of ws.xhead (bf16, normalised), greedy argmax
+  // RMSNorm of n rows of ws.h-like x (rows idx[o], or o) by one wave each
+  // (bf16 model)
+  void norm_rows(int n, const float* x, const int32_t* idx, const float* g, float* yf,
+                 uint16_t* yb) {
+    const int H = c.hidden, n4 = H / 256;
+    const float eps = (float)c.rms_eps;
+#define MTP_NR(NV) k_norm_rows<NV><<<n, 64, 0, s>>>(H, x, idx, g, eps, yf, yb)
+    MTP_NV_DISPATCH(n4, MTP_NR);
+#undef MTP_NR
+  }
   // LM-head partials per row (blocks of the launch lm_mfma makes for nr rows)
   unsigned lm_partials(int nr) const {
     return groups(nr) >= 4 ? cdiv(c.vocab, 128) : cdiv(cdiv(c.vocab, 16), 4);
@@ -470,15 +480,16 @@ struct Model {
                  ws.slot);
       }
     }
-    k_combine_norm<<<R, 256, 0, s>>>(H, small ? 0 : k, small ? nullptr : ws.slot, ws.h,
-                                     w.final_norm, eps, hid,
-                                     (tok && head_all) ? (uint16_t*)ws.xhead : nullptr);
+    uint16_t* xh = (tok && head_all) ? (uint16_t*)ws.xhead : nullptr;
+    if (small)
+      norm_rows(R, ws.h, nullptr, w.final_norm, hid, xh);
+    else
+      k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.final_norm, eps, hid, xh);
     if (!tok) return;
     if (head_all) {
       lm_mfma(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
     } else {
-      k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, nullptr, 0,
-                                      (T*)ws.xhead, H, 0);
+      norm_rows(B, ws.h, ws.head_row, w.final_norm, nullptr, (uint16_t*)ws.xhead);
       lm_mfma(ws, B, logits, c.vocab, 1, 1, 0, tok, margin);
     }
   }
@@ -501,13 +512,9 @@ struct Model {
     const unsigned G = groups(R);
     const bool pre = G > 1;
     const uint16_t* xn = pre ? (const uint16_t*)ws.xin : nullptr;
-    if (pre)
-      k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.d_attn_norm, eps, nullptr, 0,
-                                      (T*)ws.xin, H, 0);
+    if (pre) norm_rows(R, ws.h, nullptr, w.d_attn_norm, nullptr, (uint16_t*)ws.xin);
     attn_mfma(ws, B, C, w.d_attn_norm, xn, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
-    if (pre)
-      k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.d_ffn_norm, eps, nullptr, 0,
-                                      (T*)ws.xin, H, 0);
+    if (pre) norm_rows(R, ws.h, nullptr, w.d_ffn_norm, nullptr, (uint16_t*)ws.xin);
     const int cpb = G >= 8 ? 4 : 1;
 #define MTP_DFFN(M)                                                                           \
   launch_k(tm, MTP_KC_DRAFT_FFN,                                                              \
@@ -520,8 +527,7 @@ struct Model {
 #undef MTP_DFFN
     smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
     if (!head) return;
-    k_rmsnorm<BF><<<B, 256, 0, s>>>(H, ws.h, H, ws.head_row, w.final_norm, eps, ws.ustate, H,
-                                    (T*)ws.xhead, H, 0);
+    norm_rows(B, ws.h, ws.head_row, w.final_norm, ws.ustate, (uint16_t*)ws.xhead);
     lm_mfma(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr, defer_argmax);
   }
 };
