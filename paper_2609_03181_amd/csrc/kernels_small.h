@@ -65,6 +65,29 @@ __device__ __forceinline__ f32x4_t sk_range(const uint4* __restrict__ A, int t0,
   return acc;
 }
 
+// sk_range with the B row in LDS (xl) and the first batch (tiles t0..)
+// already loaded into a: only the weight tiles are global loads, so
+// waiting on a batch never waits on a B read
+template <int BT = 8>
+__device__ __forceinline__ f32x4_t sk_range_lx(const uint4* __restrict__ A, int t0, int t1,
+                                               const uint16_t* xl, f32x4_t acc, bool nt,
+                                               uint4 (&a)[BT]) {
+  const int lane = threadIdx.x & 63, koff = 8 * (lane >> 4);
+  for (int t = t0; t < t1; t += BT) {
+    uint4 an[BT];
+#pragma unroll
+    for (int u = 0; u < BT; ++u)
+      an[u] = t + BT + u < t1 ? ld_tile(A + (size_t)(t + BT + u) * 64 + lane, nt)
+                              : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < BT; ++u)
+      if (t + u < t1) acc = mfma16(a[u], *(const uint4*)(xl + (t + u) * 32 + koff), acc);
+#pragma unroll
+    for (int u = 0; u < BT; ++u) a[u] = an[u];
+  }
+  return acc;
+}
+
 // up to MAXT tiles of a strip, loaded into registers ahead of their use
 template <int MAXT>
 __device__ __forceinline__ void preload(const uint4* __restrict__ A, int t0, int n,
@@ -1318,13 +1341,17 @@ __global__ void __launch_bounds__(512) k_lm_gemm(int nr, int V, int H,
 // Block = 4 vocabulary strips (64 rows) x RG 16-row groups (blockIdx.y)
 // of the nr input rows X (bf16): each weight tile feeds RG MFMAs.  Per row
 // the best logit, its id (lowest on ties) and the second best.
-template <int RG>
+// XL (one row group of more than a few rows): the block's rows are staged
+// in LDS once ([16][H + XPAD], dynamic) instead of every wave reading them
+// from L2 beside its weight tiles.
+template <int RG, bool XL = false>
 __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16_t* __restrict__ X,
                                               const uint4* __restrict__ Wp,
                                               float* __restrict__ logits, size_t ldl,
                                               float* __restrict__ pv, int32_t* __restrict__ pi,
                                               float* __restrict__ p2) {
   constexpr int BT = 4;  // A tiles per batch (each used by RG MFMAs)
+  extern __shared__ __align__(16) uint16_t xs[];
   __shared__ float bv[4][16 * RG], sv[4][16 * RG];
   __shared__ int bi[4][16 * RG];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -1340,7 +1367,31 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
   f32x4_t acc[RG];
 #pragma unroll
   for (int g = 0; g < RG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (live) {
+  if constexpr (XL) {
+    static_assert(RG == 1, "rows staged for one row group");
+    constexpr int XC = 16 * 2048 / 8 / 256;  // 16-byte row chunks per thread (H <= 2048)
+    const int ldx_l = H + XPAD, nrow = min(16, nr - r0), nx = nrow * H / 8;
+    // row loads first, then the first tile batch: writing the rows to LDS
+    // waits on the row loads only
+    uint4 xv[XC];
+#pragma unroll
+    for (int q = 0; q < XC; ++q) {
+      const int c = threadIdx.x + 256 * q;
+      xv[q] = c < nx ? ((const uint4*)(X + (size_t)r0 * H))[c] : make_uint4(0, 0, 0, 0);
+    }
+    const uint4* A = Wp + (size_t)nt * nkt * 64;
+    uint4 a[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      a[u] = (live && u < nkt) ? ld_tile(A + (size_t)u * 64 + lane, true) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int q = 0; q < XC; ++q) {
+      const int c = threadIdx.x + 256 * q;
+      if (c < nx) *(uint4*)(xs + (c / (H / 8)) * ldx_l + (c % (H / 8)) * 8) = xv[q];
+    }
+    __syncthreads();
+    if (live) acc[0] = sk_range_lx<8>(A, 0, nkt, xs + (r < nrow ? r : 0) * ldx_l, acc[0], true, a);
+  } else if (live) {
     if (RG == 1) {
       acc[0] = sk_range(Wp + (size_t)nt * nkt * 64, 0, nkt, xrow[0], acc[0], true);
     } else {

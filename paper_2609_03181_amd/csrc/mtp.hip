@@ -396,9 +396,11 @@ struct Model {
     } else if (G >= 2) {
       launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<2>, dim3(nblk, cdiv(G, 2)), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
-    } else {
-      launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<1>, dim3(nblk, G), dim3(256), 0, s, nr, V, H,
-               (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
+    } else {  // one row group; above 4 rows the rows are staged in LDS once per block
+      const bool xl = nr > 4;
+      launch_k(tm, MTP_KC_LM_HEAD, xl ? k_s_lm<1, true> : k_s_lm<1, false>, dim3(nblk, G),
+               dim3(256), xl ? lds_rows(nr, H) : 0, s, nr, V, H, (const uint16_t*)ws.xhead, pk.lm,
+               logits, ldl, ws.pv, ws.pi, ws.p2);
     }
     if (!defer_argmax)
       k_argmax_final<<<nr, 256, 0, s>>>(nr, nb, ws.pv, ws.pi, ws.p2, per, ostride, ooff, tok,
