@@ -8,7 +8,9 @@ oracle recomputes one by one:
   verify rows: one full row group);
 * batch 16: cached contexts U{1024..2048} (seed 2), synthetic caches;
 * batch 64: cached contexts U{512..4096} (seed 12), Zipf(1.1) router bias,
-  synthetic caches.
+  synthetic caches;
+* batch 1 at a long context: 30,000 cached positions of a 32,768-position
+  cache (RoPE base 1e6; decode attention in 64 key splits of 512).
 
 For the synthetic-cache cases only the sampled sequences (shortest,
 longest and one more) carry cache values; the others hold zero caches of
@@ -149,6 +151,20 @@ def test_full_shape_batch64_zipf_sampled_sequences():
     model = Model(CFG, w, 64, 4096 + 64, 3)
     try:
         _synthetic_case(w, model, oracle.Oracle(CFG, w), 64, 512, 4096, 12, 2)
+    finally:
+        model.close()
+        torch.cuda.empty_cache()
+
+
+def test_full_shape_long_context_split_kv():
+    """One sequence with 30,000 cached positions in a 32,768-position cache:
+    decode attention over 64 key splits of 512 positions (the merge of the
+    maximum split count), RoPE at positions near 30K."""
+    log("[full] weights (seed 0, draft seed 1), long context")
+    w = synth.make_weights(CFG, 0, 1)
+    model = Model(CFG, w, 1, 32768, 3)
+    try:
+        _synthetic_case(w, model, oracle.Oracle(CFG, w), 1, 30000, 30000, 7, 2)
     finally:
         model.close()
         torch.cuda.empty_cache()
