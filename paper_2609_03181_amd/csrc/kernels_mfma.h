@@ -107,34 +107,56 @@ __device__ __forceinline__ void lane_topk(float lv, int E, int topk, float* sc, 
 
 // h[r] += slot[r][k] (dense) + sum_{j<k} slot[r][j]; then RMSNorm of the
 // new h with gain g -> xin (bf16, product input) and/or yf (float32).
-// One block per row.  slot may be NULL (no MoE contribution to add).
-__global__ void __launch_bounds__(256) k_combine_norm(int H, int topk,
+// One block of H/4 threads per row, thread j owning columns 4j..4j+3: the
+// row, its k+1 slots and the gain are all loaded before any sum (k <= 8).
+// slot may be NULL (no MoE contribution to add).
+__global__ void __launch_bounds__(512) k_combine_norm(int H, int topk,
                                                       const float* __restrict__ slot,
                                                       float* __restrict__ h,
                                                       const float* __restrict__ g, float eps,
                                                       float* __restrict__ yf,
                                                       uint16_t* __restrict__ xin) {
   __shared__ float red[16];
-  const int r = blockIdx.x;
-  float* hr = h + (size_t)r * H;
-  float ss = 0.f;
-  for (int j = threadIdx.x; j < H; j += blockDim.x) {
-    float v = hr[j];
-    if (slot) {
-      const float* s = slot + (size_t)r * (topk + 1) * H + j;
-      float add = s[(size_t)topk * H];
-      for (int x = 0; x < topk; ++x) add += s[(size_t)x * H];
-      v += add;
-      hr[j] = v;
+  const int r = blockIdx.x, j4 = threadIdx.x;
+  float4* hr = (float4*)(h + (size_t)r * H);
+  float4 v = hr[j4];
+  const float4 gv = ((const float4*)g)[j4];
+  if (slot) {
+    const float* s0 = slot + (size_t)r * (topk + 1) * H;
+    float4 sv[9];
+#pragma unroll
+    for (int x = 0; x < 9; ++x)
+      sv[x] = x <= topk ? ((const float4*)(s0 + (size_t)x * H))[j4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 add = sv[0];
+#pragma unroll
+    for (int x = 0; x < 9; ++x)
+      if (x == topk) add = sv[x];  // the dense (shared) slot first
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      if (x < topk) {
+        add.x += sv[x].x;
+        add.y += sv[x].y;
+        add.z += sv[x].z;
+        add.w += sv[x].w;
+      }
     }
-    ss += v * v;
+    v.x += add.x;
+    v.y += add.y;
+    v.z += add.z;
+    v.w += add.w;
+    hr[j4] = v;
   }
+  float ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   ss = block_sum(ss, red);
   const float rinv = rsqrtf(ss / (float)H + eps);
-  for (int j = threadIdx.x; j < H; j += blockDim.x) {
-    const float y = hr[j] * rinv * g[j];
-    if (yf) yf[(size_t)r * H + j] = y;
-    if (xin) xin[(size_t)r * H + j] = f2bf(y);
+  const float4 y = make_float4(v.x * rinv * gv.x, v.y * rinv * gv.y, v.z * rinv * gv.z,
+                               v.w * rinv * gv.w);
+  if (yf) ((float4*)(yf + (size_t)r * H))[j4] = y;
+  if (xin) {
+    uint2 pk;
+    pk.x = (uint32_t)f2bf(y.x) | ((uint32_t)f2bf(y.y) << 16);
+    pk.y = (uint32_t)f2bf(y.z) | ((uint32_t)f2bf(y.w) << 16);
+    ((uint2*)(xin + (size_t)r * H))[j4] = pk;
   }
 }
 

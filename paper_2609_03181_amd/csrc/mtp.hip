@@ -426,7 +426,7 @@ struct Model {
     for (int l = 0; l < L; ++l) {
       const uint16_t* xg = nullptr;
       if (!small) {  // add the previous layer's expert slots (if any), normalise once
-        k_combine_norm<<<R, 256, 0, s>>>(H, k, l > 0 ? ws.slot : nullptr, ws.h,
+        k_combine_norm<<<R, H / 4, 0, s>>>(H, k, l > 0 ? ws.slot : nullptr, ws.h,
                                          w.attn_norm + (size_t)l * H, eps, nullptr,
                                          (uint16_t*)ws.xin);
         xg = (const uint16_t*)ws.xin;
@@ -486,7 +486,7 @@ struct Model {
     if (small)
       norm_rows(R, ws.h, nullptr, w.final_norm, hid, xh);
     else
-      k_combine_norm<<<R, 256, 0, s>>>(H, k, ws.slot, ws.h, w.final_norm, eps, hid, xh);
+      k_combine_norm<<<R, H / 4, 0, s>>>(H, k, ws.slot, ws.h, w.final_norm, eps, hid, xh);
     if (!tok) return;
     if (head_all) {
       lm_mfma(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
