@@ -1089,11 +1089,15 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
 
 // ---------------------------------------------------------------- MoE down (slots)
 // Any batch: block = (16 output features, expert y, cpb 16-entry chunks
-// from z*16*cpb), K split over 4 waves (with cpb > 1 the tiles are loaded
-// once and applied to the chunks in turn).  Routed y < E: slot[(row*(k+1) + slot)][n] =
-// w * (Wd_y[n] . act_t); y == E: slot[(r*(k+1) + k)][n] = Wsd[n] . act_sh[r]
-// (the shared experts as one width-SI SwiGLU).  k_combine_norm then adds
-// the k+1 slots of each row to h in a fixed order.
+// from z*16*cpb), K split over 4 waves.  A routed expert's wave tiles
+// (I/128 <= MAXT) are loaded once and applied to the block's chunks in
+// turn; the shared block (K = SI) streams its tiles per chunk (the shared
+// weights stay in L2), so the registers are sized for one expert's K.
+// Routed y < E: slot[(row*(k+1) + slot)][n] = w * (Wd_y[n] . act_t);
+// y == E: slot[(r*(k+1) + k)][n] = Wsd[n] . act_sh[r] (the shared experts
+// as one width-SI SwiGLU).  k_combine_norm then adds the k+1 slots of
+// each row to h in a fixed order.
+template <int MAXT>
 __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int topk, int H,
                                                      int I, int SI,
                                                      const uint16_t* __restrict__ act,
@@ -1120,11 +1124,13 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
   const int K = dense ? SI : I, nkt = K / 32, per = nkt / 4;
   const uint4* A = dense ? sdn + (size_t)nt * nkt * 64
                          : edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
-  if (cpb == 1) {  // one chunk: stream the tiles (double-buffered)
-    const int t = tb + (lane & 15);
-    const uint16_t* xrow = nullptr;
-    int row = 0, sl = topk;
-    float wt = 1.f;
+  // Chunk c's rows: entries tb + 16c + (lane & 15).
+  auto chunk_rows = [&](int c, const uint16_t*& xrow, int& row, int& sl, float& wt) {
+    const int t = tb + 16 * c + (lane & 15);
+    xrow = nullptr;
+    row = 0;
+    sl = topk;
+    wt = 1.f;
     if (t < n) {
       if (dense) {
         xrow = act_sh + (size_t)t * SI;
@@ -1136,44 +1142,44 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
         wt = ent_w[o + t];
       }
     }
-    f32x4_t acc = sk_range(A, w * per, (w + 1) * per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f},
-                           n <= 16);  // read by this block only
-    acc = block_acc_sum<4>(acc, red);
-    if (w != 0 || t >= n) return;
-    float4* dst =
-        (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
-    *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
-    return;
-  }
-  // several chunks: the wave's tiles (per <= 16) stay in registers
-  uint4 a[16];
-  preload<16>(A, w * per, per, a, n <= 16 * cpb);  // read by this block only
-  for (int c = 0; c < cpb; ++c) {
-    const int t0 = tb + 16 * c;
-    if (t0 >= n) break;  // block-uniform
-    if (c > 0) __syncthreads();
-    const int t = t0 + (lane & 15);
-    const uint16_t* xrow = nullptr;
-    int row = 0, sl = topk;
-    float wt = 1.f;
-    if (t < n) {
-      if (dense) {
-        xrow = act_sh + (size_t)t * SI;
-        row = t;
-      } else {
-        xrow = act + (size_t)(o + t) * I;
-        row = ent_row[o + t];
-        sl = ent_slot[o + t];
-        wt = ent_w[o + t];
-      }
-    }
-    f32x4_t acc = mma_pre<16, 4>(a, w * per, per, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f});
-    acc = block_acc_sum<4>(acc, red);
+  };
+  auto store = [&](int c, f32x4_t acc, int row, int sl, float wt) {
+    const int t = tb + 16 * c + (lane & 15);
     if (w == 0 && t < n) {
       float4* dst =
           (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
       *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
     }
+  };
+  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+  if (dense) {  // the shared block streams its tiles per chunk (double-buffered)
+    for (int c = 0; c < cpb; ++c) {
+      if (tb + 16 * c >= n) break;  // block-uniform
+      if (c > 0) __syncthreads();
+      const uint16_t* xrow;
+      int row, sl;
+      float wt;
+      chunk_rows(c, xrow, row, sl, wt);
+      f32x4_t acc = sk_range<4>(A, w * per, (w + 1) * per, xrow, z4, n <= 16 * cpb);
+      acc = block_acc_sum<4>(acc, red);
+      store(c, acc, row, sl, wt);
+    }
+    return;
+  }
+  // a routed expert's wave tiles (I/128 <= MAXT) stay in registers; each
+  // chunk's B operands are all loaded before its products
+  uint4 a[MAXT];
+  preload<MAXT>(A, w * per, per, a, n <= 16 * cpb);  // read by this block only
+  for (int c = 0; c < cpb; ++c) {
+    if (tb + 16 * c >= n) break;  // block-uniform
+    if (c > 0) __syncthreads();
+    const uint16_t* xrow;
+    int row, sl;
+    float wt;
+    chunk_rows(c, xrow, row, sl, wt);
+    f32x4_t acc = mma_pre<MAXT>(a, w * per, per, xrow, z4);
+    acc = block_acc_sum<4>(acc, red);
+    store(c, acc, row, sl, wt);
   }
 }
 

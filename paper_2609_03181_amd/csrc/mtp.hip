@@ -476,10 +476,12 @@ struct Model {
                  ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h);
       else {
         const int cpb_d = G >= 8 ? 4 : 1;
-        launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot, dim3(H / 16, E + 1, cdiv(G, cpb_d)),
-                 dim3(256), 0, s, cpb_d, R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh,
-                 edn, pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w,
-                 ws.slot);
+#define MTP_DSLOT(M)                                                                            \
+  launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot<M>, dim3(H / 16, E + 1, cdiv(G, cpb_d)), dim3(256), \
+           0, s, cpb_d, R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn,              \
+           pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot)
+        MTP_MAXT_DISPATCH(I / 128, MTP_DSLOT);
+#undef MTP_DSLOT
       }
     }
     uint16_t* xh = (tok && head_all) ? (uint16_t*)ws.xhead : nullptr;
