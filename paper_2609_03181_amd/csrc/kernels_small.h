@@ -763,6 +763,22 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   }
 }
 
+// Compact MoE grids (more than 16 rows): cbp[y] (y <= E) is the number of
+// 16*cpb-entry chunk blocks of the experts before y (the shared experts are
+// y = E, with R entries), cbp[E+1] the total (written by k_group).  Chunk
+// block c lies in expert y = the last one with cbp[y] <= c; returns y and
+// z = c - cbp[y].  Every wave of the block computes it (no barrier).
+__device__ __forceinline__ int chunk_block_expert(int c, int E, const int32_t* __restrict__ cbp,
+                                                  int& z) {
+  const int lane = threadIdx.x & 63;
+  const int pv = lane < E ? cbp[lane] : 0x7fffffff;
+  const int pe = cbp[E];
+  int y = __popcll(__ballot(pv <= c)) - 1;
+  if (c >= pe) y = E;
+  z = c - (y == E ? pe : __shfl(pv, y, MTP_WAVE));
+  return y;
+}
+
 // ---------------------------------------------------------------- MoE gate/up
 // Block = (16-wide intermediate tile, expert y, cpb 16-entry chunks from
 // z*16*cpb): routed expert y < E over its entries (blocks past cnt[y] exit
@@ -785,11 +801,26 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
                                               const int32_t* __restrict__ off,
                                               const int32_t* __restrict__ ent_row,
                                               uint16_t* __restrict__ act,
-                                              uint16_t* __restrict__ act_sh) {
+                                              uint16_t* __restrict__ act_sh,
+                                              const int32_t* __restrict__ cbp) {
   extern __shared__ __align__(16) uint16_t xs[];
   __shared__ f32x4_t red[2 * 4 * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int it = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
+  int it = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
+  if (cbp) {  // compact grid (1-D): I/16 tiles per routed chunk block, SI/16 per shared one
+    const int nI = I / 16, nr = cbp[E] * nI, b = blockIdx.x;
+    int z;
+    if (b < nr) {
+      e = chunk_block_expert(b / nI, E, cbp, z);
+      it = b % nI;
+    } else {
+      e = E;
+      it = (b - nr) % (SI / 16);
+      z = (b - nr) / (SI / 16);
+      if (cbp[E] + z >= cbp[E + 1]) return;  // past the shared chunk blocks
+    }
+    tb = z * 16 * cpb;
+  }
   const bool dense = (ROLE & 1) || e == E;
   const int width = dense ? SI : I;
   if (it * 16 >= width) return;
@@ -1088,8 +1119,8 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
 }
 
 // ---------------------------------------------------------------- MoE down (slots)
-// Any batch: block = (16 output features, expert y, cpb 16-entry chunks
-// from z*16*cpb), K split over 4 waves.  A routed expert's wave tiles
+// More than 16 rows: block = (16 output features, expert y, cpb 16-entry
+// chunks from z*16*cpb), K split over 4 waves.  A routed expert's wave tiles
 // (I/128 <= MAXT) are loaded once and applied to the block's chunks in
 // turn; the shared block (K = SI) streams its tiles per chunk (the shared
 // weights stay in L2), so the registers are sized for one expert's K.
@@ -1184,7 +1215,8 @@ __global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int 
 }
 
 // Grouping of (row, slot) pairs by expert for any number of rows: counts,
-// offsets (ascending expert id) and one entry per pair.  Entries of one
+// offsets (ascending expert id), one entry per pair, and the chunk-block
+// prefix cbp of the compact MoE grids (chunks of 16*cpb entries).  Entries of one
 // expert are placed through LDS atomics, so their order inside the expert
 // varies between runs; every value computed from them does not (an entry's
 // row and slot travel with it and the MFMA columns are independent).
@@ -1195,7 +1227,8 @@ __global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
                                                 int32_t* __restrict__ off,
                                                 int32_t* __restrict__ ent_row,
                                                 int32_t* __restrict__ ent_slot,
-                                                float* __restrict__ ent_w) {
+                                                float* __restrict__ ent_w, int cpb,
+                                                int32_t* __restrict__ cbp) {
   __shared__ int l_cnt[64], l_off[64], l_cur[64];
   if (threadIdx.x < 64) {
     l_cnt[threadIdx.x] = 0;
@@ -1213,6 +1246,19 @@ __global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
     if (e < E) {
       cnt[e] = l_cnt[e];
       off[e] = o;
+    }
+    // chunk blocks of 16*cpb entries per expert, prefix over the experts
+    const int ch = 16 * cpb, nb = e < E ? (l_cnt[e] + ch - 1) / ch : 0;
+    int pre = nb;  // inclusive scan over the 64 lanes
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(pre, d, MTP_WAVE);
+      if (e >= d) pre += v;
+    }
+    if (e < E) cbp[e] = pre - nb;
+    if (e == 63) {
+      cbp[E] = pre;
+      cbp[E + 1] = pre + (R + ch - 1) / ch;
     }
   }
   __syncthreads();

@@ -76,6 +76,7 @@ struct Ws {
   // bf16 fast path
   float *part, *slot, *ent_w;
   int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr, *dn_ctr;
+  int32_t* cbp;  // chunk-block prefix of the compact MoE grids [E + 2]
   unsigned long long* dn_part;  // MoE down split partials [kDownSplit][R][H], fixed point (R <= 16)
   uint16_t* act_sh;
   int n_ctr;  // entries of att_ctr (zeroed at the start of each call)
@@ -136,6 +137,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.ent_slot = (int32_t*)take(R * k * 4);
     w.touched = (int32_t*)take((size_t)c.n_routed * 4);
     w.n_touched = (int32_t*)take(4);
+    w.cbp = (int32_t*)take(((size_t)c.n_routed + 2) * 4);
     // attention split counters then MoE-down strip counters, one region
     w.att_ctr = (int32_t*)take((R * c.n_heads + (size_t)H / 16) * 4);
     w.dn_ctr = w.att_ctr + R * c.n_heads;
@@ -146,6 +148,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
   } else {
     w.part = w.slot = w.ent_w = nullptr;
     w.cnt = w.off = w.ent_row = w.ent_slot = w.touched = w.n_touched = w.att_ctr = nullptr;
+    w.cbp = nullptr;
     w.act_sh = nullptr;
   }
   w.bytes = off;
@@ -442,9 +445,10 @@ struct Model {
            ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched)
       MTP_MAXT_DISPATCH(H / 128, MTP_ROUTER);
 #undef MTP_ROUTER
+      const int cpb = G >= 8 ? 4 : 1;  // 16-entry chunks per MoE block (more than 16 rows)
       if (G > 1)
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
-                                   ws.ent_slot, ws.ent_w);
+                                   ws.ent_slot, ws.ent_w, cpb, ws.cbp);
       if (G == 1) {  // persistent streaming form: two blocks per compute unit
         const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
         const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
@@ -454,16 +458,16 @@ struct Model {
            ws.touched, ws.n_touched, (uint16_t*)ws.act, ws.act_sh)
         MTP_MAXT_DISPATCH(H / 128, MTP_GU);
 #undef MTP_GU
-      } else {
-        const int cpb = G >= 8 ? 4 : 1;  // 16-entry chunks per block
-        const dim3 grid(cdiv(SI > I ? SI : I, 16), E + 1, cdiv(G, cpb));
+      } else {  // compact grid: at most E + R*k/(16*cpb) routed chunk blocks
+        const unsigned nblk = (E + cdiv((size_t)R * k, 16 * cpb)) * (I / 16) +
+                              cdiv(R, 16 * cpb) * (SI / 16);
         const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
         const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
 #define MTP_GU(M)                                                                             \
-  launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL, M> : k_s_gu<GU_VERIFY, M>, grid,    \
-           dim3(256), 0, s, cpb, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr, nullptr, eps,  \
-           egu,                                                                                \
-           pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act, ws.act_sh)
+  launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL, M> : k_s_gu<GU_VERIFY, M>,         \
+           dim3(nblk), dim3(256), 0, s, cpb, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr,  \
+           nullptr, eps, egu, pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act, \
+           ws.act_sh, ws.cbp)
         MTP_MAXT_DISPATCH(H / 128, MTP_GU);
 #undef MTP_GU
       }
@@ -475,10 +479,9 @@ struct Model {
                  pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.touched,
                  ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h);
       else {
-        const int cpb_d = G >= 8 ? 4 : 1;
 #define MTP_DSLOT(M)                                                                            \
-  launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot<M>, dim3(H / 16, E + 1, cdiv(G, cpb_d)), dim3(256), \
-           0, s, cpb_d, R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn,              \
+  launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot<M>, dim3(H / 16, E + 1, cdiv(G, cpb)), dim3(256),  \
+           0, s, cpb, R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn,                \
            pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot)
         MTP_MAXT_DISPATCH(I / 128, MTP_DSLOT);
 #undef MTP_DSLOT
@@ -526,7 +529,7 @@ struct Model {
                    : (pre ? k_s_gu<GU_DRAFT, M> : k_s_gu<GU_DRAFT, M, true>),                 \
            dim3(F / 16, 1, cdiv(G, cpb)), dim3(256), pre ? 0 : lds_rows(R, H), s, cpb, R, H, 0, \
            F, F, xn, pre ? nullptr : ws.h, pre ? nullptr : w.d_ffn_norm, eps, nullptr, 0,       \
-           pk.d_gu, nullptr, nullptr, nullptr, nullptr, ws.act_sh)
+           pk.d_gu, nullptr, nullptr, nullptr, nullptr, ws.act_sh, (const int32_t*)nullptr)
     MTP_MAXT_DISPATCH(H / 128, MTP_DFFN);
 #undef MTP_DFFN
     smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
