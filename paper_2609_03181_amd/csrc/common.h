@@ -101,6 +101,15 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   return t;
 }
 
+// 16-byte load of 4 floats through the native vector type: HIP's float4 is
+// a struct, and a struct load under a condition can be split into four
+// 4-byte loads (four load instructions where one suffices).
+__device__ __forceinline__ float4 ld_f4(const float* p) {
+  typedef float v4f __attribute__((ext_vector_type(4)));
+  const v4f v = *(const v4f*)p;
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+
 // Greedy-argmax reduction step: (best value, lowest id on ties, second
 // best value) of two partial results.
 __device__ __forceinline__ void argmax_combine(float& bv, float& sv, int& bi, float v, float s,

@@ -119,14 +119,14 @@ __global__ void __launch_bounds__(512) k_combine_norm(int H, int topk,
   __shared__ float red[16];
   const int r = blockIdx.x, j4 = threadIdx.x;
   float4* hr = (float4*)(h + (size_t)r * H);
-  float4 v = hr[j4];
-  const float4 gv = ((const float4*)g)[j4];
+  float4 v = ld_f4(h + (size_t)r * H + j4 * 4);
+  const float4 gv = ld_f4(g + j4 * 4);
   if (slot) {
     const float* s0 = slot + (size_t)r * (topk + 1) * H;
     float4 sv[9];
 #pragma unroll
     for (int x = 0; x < 9; ++x)
-      sv[x] = x <= topk ? ((const float4*)(s0 + (size_t)x * H))[j4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      sv[x] = x <= topk ? ld_f4(s0 + (size_t)x * H + j4 * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
     float4 add = sv[0];
 #pragma unroll
     for (int x = 0; x < 9; ++x)

@@ -136,9 +136,9 @@ __device__ __forceinline__ void draft_in_wave(int H, const uint16_t* __restrict_
         ev[u] = make_float4(bf2f((uint16_t)q.x), bf2f((uint16_t)(q.x >> 16)),
                             bf2f((uint16_t)q.y), bf2f((uint16_t)(q.y >> 16)));
       }
-      if (a) av[u] = ((const float4*)a)[j4];
-      gev[u] = ((const float4*)ge)[j4];
-      ghv[u] = ((const float4*)gh)[j4];
+      if (a) av[u] = ld_f4(a + j4 * 4);
+      gev[u] = ld_f4(ge + j4 * 4);
+      ghv[u] = ld_f4(gh + j4 * 4);
     }
   }
   float se = 0.f, sa = 0.f;

@@ -183,8 +183,8 @@ __device__ __forceinline__ void norm_rows_lds(int R, int H, const float* __restr
     float4 xv[NV], gv[NV];
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
-      xv[u] = u < n4 ? ((const float4*)(src + (size_t)r * H))[u * 64 + lane] : z;
-      gv[u] = u < n4 ? ((const float4*)g)[u * 64 + lane] : z;
+      xv[u] = u < n4 ? ld_f4(src + (size_t)r * H + (u * 64 + lane) * 4) : z;
+      gv[u] = u < n4 ? ld_f4(g + (u * 64 + lane) * 4) : z;
     }
     float ss = 0.f;
 #pragma unroll
@@ -220,8 +220,8 @@ __device__ __forceinline__ void norm_row_load(int H, const float* __restrict__ s
   const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int u = 0; u < NV; ++u) {
-    nr.x[u] = u < n4 ? ((const float4*)src)[u * 64 + lane] : z;
-    nr.g[u] = u < n4 ? ((const float4*)g)[u * 64 + lane] : z;
+    nr.x[u] = u < n4 ? ld_f4(src + (u * 64 + lane) * 4) : z;
+    nr.g[u] = u < n4 ? ld_f4(g + (u * 64 + lane) * 4) : z;
   }
 }
 template <int NV>
@@ -314,11 +314,11 @@ __global__ void __launch_bounds__(NW * 64) k_s_mm(int R, int N, int nkt,
   if constexpr (MAXT > 0) {
     uint4 a[MAXT];
     preload<MAXT>(Wp + (size_t)nt * nkt * 64, w * per, per, a, gridDim.y == 1);
-    if (ADD && out) y0 = *(const float4*)(Y + (size_t)r * ldy + n);
+    if (ADD && out) y0 = ld_f4(Y + (size_t)r * ldy + n);
     acc = mma_pre<MAXT, (NW >= 16 && MAXT > 8) ? MAXT / 2 : MAXT>(a, w * per, per, xrow,
                                                                   f32x4_t{0.f, 0.f, 0.f, 0.f});
   } else {
-    if (ADD && out) y0 = *(const float4*)(Y + (size_t)r * ldy + n);
+    if (ADD && out) y0 = ld_f4(Y + (size_t)r * ldy + n);
     acc = sk_range<(NW >= 16 ? 4 : 8)>(Wp + (size_t)nt * nkt * 64, w * per, (w + 1) * per, xrow,
                                         f32x4_t{0.f, 0.f, 0.f, 0.f}, gridDim.y == 1);
   }
