@@ -388,19 +388,24 @@ __global__ void __launch_bounds__(256) k_s_qkv(int R, int C, int H, int nh, int 
 #pragma unroll
     for (int t = 0; t < 4; ++t) cs[t] = rope[(size_t)p * half + pt * 16 + 4 * (lane >> 4) + t];
   }
-  const uint16_t* xrow = nullptr;
+  // B rows from global memory (xg) or LDS (prologue): two call sites, so
+  // each reads with its own load instruction rather than a generic one
+  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t c0 = z4, c1 = z4;
   if (xg) {
-    if (r < R) xrow = xg + (size_t)r * H;
+    const uint16_t* xrow = r < R ? xg + (size_t)r * H : nullptr;
+    if (pair) mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(a0, a1, w * per, per, xrow, c0, c1);
+    else c0 = mma_pre<MAXT>(a0, w * per, per, xrow, z4);
   } else {
     if (early) norm_row_store<NV>(H, eps, nr0, xs + w * ldl);
     norm_rows_lds<NV>(nloc, H, h + (size_t)r0 * H, g, eps, xs, ldl, EARLY);
     __syncthreads();
-    if (r < R) xrow = xs + (lane & 15) * ldl;
+    // lanes of rows past R read row (lane & 15) of the tile; their columns
+    // are not stored
+    const uint16_t* xrow = xs + (lane & 15) * ldl;
+    if (pair) mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(a0, a1, w * per, per, xrow, c0, c1);
+    else c0 = mma_pre<MAXT>(a0, w * per, per, xrow, z4);
   }
-  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  f32x4_t c0 = z4, c1 = z4;
-  if (pair) mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(a0, a1, w * per, per, xrow, c0, c1);
-  else c0 = mma_pre<MAXT>(a0, w * per, per, xrow, z4);
   c0 = block_acc_sum<4>(c0, red);
   if (pair) {
     c1 = block_acc_sum<4>(c1, red + 4 * 64);
@@ -852,18 +857,19 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
   preload<MAXT>(U, w * per, per, au_, once);
   if (cpb == 1) {  // one chunk (with the RMSNorm prologue when g != NULL)
     const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
-    const uint16_t* xrow = nullptr;
+    const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t cg = z4, cu = z4;
     if ((ROLE & 1) != 0 && g) {  // draft roles, few rows: RMSNorm(h; g) prologue
       if (early) norm_row_store<NV>(H, eps, nr0, xs + w * ldl);
       norm_rows_lds<NV>(min(16, n - t0), H, h + (size_t)t0 * H, g, eps, xs, ldl, EARLY);
       __syncthreads();
-      if (t < n) xrow = xs + (lane & 15) * ldl;
-    } else if (t < n) {
-      xrow = xg + (size_t)(dense ? t : ent_row[o + t]) * H;
+      // B rows in LDS (lanes past n read a tile row; their columns are not stored)
+      mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per,
+                                                         xs + (lane & 15) * ldl, cg, cu);
+    } else {
+      const uint16_t* xrow = t < n ? xg + (size_t)(dense ? t : ent_row[o + t]) * H : nullptr;
+      mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
     }
-    const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-    f32x4_t cg = z4, cu = z4;
-    mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
     cg = block_acc_sum<4>(cg, red);
     cu = block_acc_sum<4>(cu, red + 4 * 64);
     if (w != 0 || t >= n) return;
