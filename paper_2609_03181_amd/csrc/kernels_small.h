@@ -512,10 +512,20 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
   uint4 kreg[VPT], vreg[VPT];
 #pragma unroll
   for (int u = 0; u < VPT; ++u) kreg[u] = vreg[u] = make_uint4(0, 0, 0, 0);
+  // the query rows are loaded before the first tile, so storing them to
+  // LDS does not wait on the tile
+  constexpr int QPT = (NR * DH + 255) / 256;
+  float qv[QPT];
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int e = threadIdx.x + 256 * u, i = e / DH, d = e % DH;
+    qv[u] = (e < NR * DH && i < nr) ? q[(size_t)(b * C + i0 + i) * D + h * DH + d] : 0.f;
+  }
   if (k0 < k1) attn_load_tile<DH, VPT>(Kc, Vc, k0, cap, kreg, vreg);
-  for (int e = threadIdx.x; e < NR * DH; e += 256) {
-    const int i = e / DH, d = e % DH;
-    qs[i][d] = i < nr ? q[(size_t)(b * C + i0 + i) * D + h * DH + d] : 0.f;
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int e = threadIdx.x + 256 * u;
+    if (e < NR * DH) qs[e / DH][e % DH] = qv[u];
   }
   float m[RPW], l[RPW], o[RPW][DPL];
 #pragma unroll
@@ -618,6 +628,14 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
     if (i >= nr) break;
     const int r = b * C + i0 + i;
     const float* pp = part + ((size_t)r * nh + h) * n_split * (DH + 2);
+    // the first 16 splits' partial vectors are loaded with the (m, l)
+    // pairs, so their sum does not wait on a second round of loads
+    float ov0[16][DPL];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+#pragma unroll
+      for (int d = 0; d < DPL; ++d)
+        ov0[u][d] = u < n_split ? ld_agent(pp + u * (DH + 2) + lane * DPL + d) : 0.f;
     const float my = lane < n_split ? ld_agent(pp + lane * (DH + 2) + DH) : -INFINITY;
     const float ly = lane < n_split ? ld_agent(pp + lane * (DH + 2) + DH + 1) : 0.f;
     const float M = wave_max(my);
@@ -628,7 +646,13 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
     float O[DPL];
 #pragma unroll
     for (int d = 0; d < DPL; ++d) O[d] = 0.f;
-    for (int y0 = 0; y0 < n_split; y0 += 8) {
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const float f = u < n_split ? ps[wv][u] : 0.f;
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) O[d] += ov0[u][d] * f;
+    }
+    for (int y0 = 16; y0 < n_split; y0 += 8) {
       float ov[8][DPL];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
