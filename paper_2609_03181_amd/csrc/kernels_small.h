@@ -457,6 +457,59 @@ __device__ __forceinline__ void attn_load_tile(const uint16_t* __restrict__ Kc,
   }
 }
 
+// Merge of one (row, head)'s n split partials by one wave (n <= 64): lane y
+// holds split y's (m, l); the weights e^{m_y - M} go through the wave's LDS
+// row w, and each lane sums its dims over the splits with all loads in
+// flight.  Writes the bf16 row (zeros for an invalid row or an empty sum).
+// The first PRE splits' vectors are loaded with the (m, l) pairs, so their
+// sum does not wait on a second round of loads.
+template <int DH, int PRE = 16>
+__device__ __forceinline__ void attn_merge_row(const float* __restrict__ pp, int n, bool valid,
+                                               float* w, uint16_t* __restrict__ out) {
+  constexpr int DPL = DH / 64;
+  const int lane = threadIdx.x & 63;
+  float ov0[PRE][DPL];
+#pragma unroll
+  for (int u = 0; u < PRE; ++u)
+#pragma unroll
+    for (int d = 0; d < DPL; ++d)
+      ov0[u][d] = u < n ? ld_agent(pp + u * (DH + 2) + lane * DPL + d) : 0.f;
+  const float my = lane < n ? ld_agent(pp + lane * (DH + 2) + DH) : -INFINITY;
+  const float ly = lane < n ? ld_agent(pp + lane * (DH + 2) + DH + 1) : 0.f;
+  const float M = wave_max(my);
+  const float fy = (my == -INFINITY) ? 0.f : __expf(my - M);
+  const float L = wave_sum(ly * fy);
+  w[lane] = fy;
+  __builtin_amdgcn_wave_barrier();
+  float O[DPL];
+#pragma unroll
+  for (int d = 0; d < DPL; ++d) O[d] = 0.f;
+#pragma unroll
+  for (int u = 0; u < PRE; ++u) {
+    const float f = u < n ? w[u] : 0.f;
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) O[d] += ov0[u][d] * f;
+  }
+  for (int y0 = PRE; y0 < n; y0 += 8) {
+    float ov[8][DPL];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int d = 0; d < DPL; ++d)
+        ov[u][d] = (y0 + u < n) ? ld_agent(pp + (y0 + u) * (DH + 2) + lane * DPL + d) : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float f = (y0 + u < n) ? w[y0 + u] : 0.f;
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) O[d] += ov[u][d] * f;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  const bool ok = valid && L > 0.f;
+#pragma unroll
+  for (int d = 0; d < DPL; ++d) out[lane * DPL + d] = f2bf(ok ? O[d] / L : 0.f);
+}
+
 // Split-K decode attention, merge fused.  Block (split s, head h,
 // z = b*ngroups + g) covers keys [s*spl, (s+1)*spl) of sequence b for the
 // NR query rows of group g.  Per 64-key tile the block loads K and V with
@@ -619,58 +672,261 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
   __syncthreads();
   if (!last) return;
   if (threadIdx.x == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // merge: wave w merges rows w, w+4.  Lane y holds split y's (m, l)
-  // (n_split <= 64); the weights e^{m_y - M} go through LDS and each lane
-  // then sums its dims over the splits with all loads in flight.
+  // merge: wave w merges rows w, w+4
 #pragma unroll
   for (int x = 0; x < RPW; ++x) {
     const int i = wv + 4 * x;
     if (i >= nr) break;
     const int r = b * C + i0 + i;
-    const float* pp = part + ((size_t)r * nh + h) * n_split * (DH + 2);
-    // the first 16 splits' partial vectors are loaded with the (m, l)
-    // pairs, so their sum does not wait on a second round of loads
-    float ov0[16][DPL];
+    attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_split * (DH + 2), n_split,
+                       row_valid[r] != 0, ps[wv], out + (size_t)r * D + h * DH);
+  }
+}
+
+// sum / max over lanes 0..15 (DPP inside the first 16-lane row), uniform
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f<0x111, 0xf>(0.f, v);
+  v += dpp_f<0x112, 0xf>(0.f, v);
+  v += dpp_f<0x114, 0xf>(0.f, v);
+  v += dpp_f<0x118, 0xf>(0.f, v);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 15));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_f<0x111, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x112, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x114, 0xf>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x118, 0xf>(-INFINITY, v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 15));
+}
+
+// key limits of a group's four rows, and this wave's query row (row wv:
+// lanes 0..15 hold dims 8*lane..8*lane+7; zeros past the group's rows)
+__device__ __forceinline__ void attn4_seg_rows(int z, int h, int C, int ngroups, int D,
+                                               const float* __restrict__ q,
+                                               const int32_t* __restrict__ row_pos,
+                                               const int32_t* __restrict__ row_valid,
+                                               float4& q0, float4& q1, int (&lim)[4]) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int b = z / ngroups, i0 = (z % ngroups) * 4, nr = min(4, C - i0);
 #pragma unroll
-    for (int u = 0; u < 16; ++u)
+  for (int i = 0; i < 4; ++i) {
+    const int r = b * C + i0 + i;
+    lim[i] = (i < nr && row_valid[r]) ? row_pos[r] : -1;
+  }
+  q0 = q1 = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (wv < nr && lane < 16) {
+    const float* p = q + (size_t)(b * C + i0 + wv) * D + h * 128 + 8 * lane;
+    q0 = ld_f4(p);
+    q1 = ld_f4(p + 4);
+  }
+}
+
+// this wave's query row as MFMA A-operand pieces: chunk c = lane (8 dims)
+// is k-step c/4, lane group c%4; entry 4*group + row of each step
+__device__ __forceinline__ void attn4_store_q(uint4 (*qa)[2][16], float4 q0, float4 q1) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane >= 16) return;
+  const float x[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+  uint32_t hi[4], lo[4];
 #pragma unroll
-      for (int d = 0; d < DPL; ++d)
-        ov0[u][d] = u < n_split ? ld_agent(pp + u * (DH + 2) + lane * DPL + d) : 0.f;
-    const float my = lane < n_split ? ld_agent(pp + lane * (DH + 2) + DH) : -INFINITY;
-    const float ly = lane < n_split ? ld_agent(pp + lane * (DH + 2) + DH + 1) : 0.f;
-    const float M = wave_max(my);
-    const float fy = (my == -INFINITY) ? 0.f : __expf(my - M);
-    const float L = wave_sum(ly * fy);
-    ps[wv][lane] = fy;
-    __builtin_amdgcn_wave_barrier();
-    float O[DPL];
+  for (int e = 0; e < 4; ++e) {
+    const uint16_t h0 = f2bf(x[2 * e]), h1 = f2bf(x[2 * e + 1]);
+    const uint16_t l0 = f2bf(x[2 * e] - bf2f(h0)), l1 = f2bf(x[2 * e + 1] - bf2f(h1));
+    hi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    lo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  const int s = lane >> 2, e = 4 * (lane & 3) + wv;
+  qa[s][0][e] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  qa[s][1][e] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+}
+
+// Split decode attention over groups of four query rows with 128-dim heads
+// (every attention call of such a model: a row's arithmetic does not depend
+// on how many rows its group or its call has).  Grid, splits, partials and
+// merge as k_s_attn.
+// Inside a 64-key tile, wave w takes keys 16w..16w+15 for all rows of the
+// group, so each K and V element is read from LDS and widened once per
+// block: the scores are one 16x16x32 MFMA chain (query rows as the A
+// operand, zero rows past the group; the float32 query split into bf16 high
+// and low parts, two products per step, so the scores keep ~16 mantissa
+// bits of the query against the 8 of a bf16 query), the softmax runs over
+// 16-lane rows, and P.V runs on the vector units with the rows' weights
+// broadcast from LDS.  Each wave keeps its own (m, l, o) per row for its
+// keys; the four wave states are combined through LDS at the end of the
+// split, in wave order.  Every update is an explicit fused multiply-add, so
+// a row rounds the same way in the one-row and the multi-row code paths.
+template <int DH>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+k_s_attn4(int C, int nh, int n_split, int spl, const float* __restrict__ q,
+          const uint16_t* __restrict__ cache, size_t seq_stride, int cap,
+          const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_valid,
+          float scale, float* __restrict__ part, int32_t* __restrict__ counters,
+          uint16_t* __restrict__ out) {
+  static_assert(DH == 128, "four k-steps of 32 dims, two dims per lane");
+  constexpr int NR = 4;
+  constexpr int KL = DH + 8;
+  constexpr int VPT = 64 * DH / 8 / 256;
+  constexpr int NS = DH / 32;
+  __shared__ __align__(16) uint16_t Ks[64 * KL];
+  __shared__ __align__(16) uint16_t Vs[64 * DH];
+  __shared__ __align__(16) uint4 qa[NS][2][16];
+  __shared__ __align__(16) float ps[4][64];
+  __shared__ int last;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int s = blockIdx.x, h = blockIdx.y, z = blockIdx.z;
+  const int ngroups = (C + NR - 1) / NR;
+  const int b = z / ngroups, i0 = (z % ngroups) * NR, nr = min(NR, C - i0);
+  const int D = nh * DH;
+  float4 q0, q1;
+  int lim[4];
+  attn4_seg_rows(z, h, C, ngroups, D, q, row_pos, row_valid, q0, q1, lim);
+  const int maxpos = max(max(lim[0], lim[1]), max(lim[2], lim[3]));
+  const int k0 = s * spl, k1 = min(k0 + spl, maxpos + 1);
+  const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
+  const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
+  uint4 kreg[VPT], vreg[VPT];
 #pragma unroll
-    for (int d = 0; d < DPL; ++d) O[d] = 0.f;
+  for (int u = 0; u < VPT; ++u) kreg[u] = vreg[u] = make_uint4(0, 0, 0, 0);
+  if (k0 < k1) attn_load_tile<DH, VPT>(Kc, Vc, k0, cap, kreg, vreg);
+  attn4_store_q(qa, q0, q1);
+  float m[4], l[4], o[4][2];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const float f = u < n_split ? ps[wv][u] : 0.f;
+  for (int r = 0; r < 4; ++r) {
+    m[r] = -INFINITY;
+    l[r] = 0.f;
+    o[r][0] = o[r][1] = 0.f;
+  }
+  const int key16 = lane & 15, grp = lane >> 4;
+  for (int t0 = k0; t0 < k1; t0 += 64) {
+    __syncthreads();  // previous tile fully consumed, query pieces stored
 #pragma unroll
-      for (int d = 0; d < DPL; ++d) O[d] += ov0[u][d] * f;
+    for (int u = 0; u < VPT; ++u) {
+      const int c = threadIdx.x + 256 * u;
+      const int key = c / (DH / 8), part8 = c % (DH / 8);
+      *(uint4*)(Ks + key * KL + part8 * 8) = kreg[u];
+      *(uint4*)(Vs + key * DH + part8 * 8) = vreg[u];
     }
-    for (int y0 = 16; y0 < n_split; y0 += 8) {
-      float ov[8][DPL];
+    __syncthreads();
+    if (t0 + 64 < k1) attn_load_tile<DH, VPT>(Kc, Vc, t0 + 64, cap, kreg, vreg);  // in flight
+    // scores of keys 16wv + key16 for rows 0..3 (lanes 0..15; the other
+    // lanes hold the zero rows)
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    const uint16_t* kp = Ks + (16 * wv + key16) * KL + 8 * grp;
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+    for (int st = 0; st < NS; ++st) {
+      const uint4 kb = *(const uint4*)(kp + 32 * st);
+      uint4 ah = make_uint4(0, 0, 0, 0), al = make_uint4(0, 0, 0, 0);
+      if (key16 < 4) {
+        ah = qa[st][0][4 * grp + key16];
+        al = qa[st][1][4 * grp + key16];
+      }
+      acc = mfma16(ah, kb, acc);
+      acc = mfma16(al, kb, acc);
+    }
+    const int j = t0 + 16 * wv + key16;
+    float corr[4] = {1.f, 1.f, 1.f, 1.f};
 #pragma unroll
-        for (int d = 0; d < DPL; ++d)
-          ov[u][d] = (y0 + u < n_split) ? ld_agent(pp + (y0 + u) * (DH + 2) + lane * DPL + d) : 0.f;
+    for (int r = 0; r < 4; ++r) {
+      if (r >= nr) break;
+      const float si = (j <= lim[r]) ? acc[r] * scale : -INFINITY;
+      const float mn = fmaxf(m[r], row16_max(si));
+      const float p = (mn == -INFINITY) ? 0.f : __expf(si - mn);
+      corr[r] = (mn == -INFINITY) ? 1.f : __expf(m[r] - mn);
+      l[r] = __builtin_fmaf(l[r], corr[r], row16_sum(p));
+      m[r] = mn;
+      if (lane < 16) ps[wv][4 * lane + r] = p;
+    }
+    __builtin_amdgcn_wave_barrier();
+    lds_wait();
+    if (nr == 1) {
+      o[0][0] *= corr[0];
+      o[0][1] *= corr[0];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float f = (y0 + u < n_split) ? ps[wv][y0 + u] : 0.f;
+      for (int kk = 0; kk < 16; ++kk) {
+        const float p0 = ps[wv][4 * kk];
+        const uint32_t uu = *(const uint32_t*)(Vs + (16 * wv + kk) * DH + lane * 2);
+        o[0][0] = __builtin_fmaf(p0, __uint_as_float(uu << 16), o[0][0]);
+        o[0][1] = __builtin_fmaf(p0, __uint_as_float(uu & 0xffff0000u), o[0][1]);
+      }
+    } else {
 #pragma unroll
-        for (int d = 0; d < DPL; ++d) O[d] += ov[u][d] * f;
+      for (int r = 0; r < 4; ++r) {
+        o[r][0] *= corr[r];
+        o[r][1] *= corr[r];
+      }
+#pragma unroll 4
+      for (int kk = 0; kk < 16; ++kk) {
+        const float4 p4 = *(const float4*)&ps[wv][4 * kk];
+        const uint32_t uu = *(const uint32_t*)(Vs + (16 * wv + kk) * DH + lane * 2);
+        const float v0 = __uint_as_float(uu << 16), v1 = __uint_as_float(uu & 0xffff0000u);
+        o[0][0] = __builtin_fmaf(p4.x, v0, o[0][0]);
+        o[0][1] = __builtin_fmaf(p4.x, v1, o[0][1]);
+        o[1][0] = __builtin_fmaf(p4.y, v0, o[1][0]);
+        o[1][1] = __builtin_fmaf(p4.y, v1, o[1][1]);
+        o[2][0] = __builtin_fmaf(p4.z, v0, o[2][0]);
+        o[2][1] = __builtin_fmaf(p4.z, v1, o[2][1]);
+        o[3][0] = __builtin_fmaf(p4.w, v0, o[3][0]);
+        o[3][1] = __builtin_fmaf(p4.w, v1, o[3][1]);
       }
     }
     __builtin_amdgcn_wave_barrier();
-    const bool ok = row_valid[r] && L > 0.f;
+  }
+  // the four waves' states through LDS (over the K tile); row wv combined
+  // by wave wv into the split's partial
+  float* cb = (float*)Ks;
+  __syncthreads();
 #pragma unroll
-    for (int d = 0; d < DPL; ++d)
-      out[(size_t)r * D + h * DH + lane * DPL + d] = f2bf(ok ? O[d] / L : 0.f);
+  for (int r = 0; r < 4; ++r) {
+    if (r >= nr) break;
+    float* e = cb + (wv * 4 + r) * (DH + 2);
+    *(float2*)(e + 2 * lane) = make_float2(o[r][0], o[r][1]);
+    if (lane == 0) {
+      e[DH] = m[r];
+      e[DH + 1] = l[r];
+    }
+  }
+  __syncthreads();
+  if (wv < nr) {
+    float mw[4], lw[4];
+    float2 ow[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float* e = cb + (w * 4 + wv) * (DH + 2);
+      mw[w] = e[DH];
+      lw[w] = e[DH + 1];
+      ow[w] = *(const float2*)(e + 2 * lane);
+    }
+    const float M = fmaxf(fmaxf(mw[0], mw[1]), fmaxf(mw[2], mw[3]));
+    float L = 0.f, O0 = 0.f, O1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = (mw[w] == -INFINITY) ? 0.f : __expf(mw[w] - M);
+      L = __builtin_fmaf(lw[w], f, L);
+      O0 = __builtin_fmaf(ow[w].x, f, O0);
+      O1 = __builtin_fmaf(ow[w].y, f, O1);
+    }
+    const int r = b * C + i0 + wv;
+    float* pp = part + (((size_t)r * nh + h) * n_split + s) * (DH + 2);
+    st_agent(pp + 2 * lane, O0);
+    st_agent(pp + 2 * lane + 1, O1);
+    if (lane == 0) {
+      st_agent(pp + DH, M);
+      st_agent(pp + DH + 1, L);
+    }
+  }
+  vmem_release();
+  __syncthreads();
+  int32_t* ctr = counters + (size_t)z * nh + h;
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+           n_split - 1;
+  __syncthreads();
+  if (!last) return;
+  if (threadIdx.x == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (wv < nr) {
+    const int r = b * C + i0 + wv;
+    attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_split * (DH + 2), n_split,
+                       row_valid[r] != 0, ps[wv], out + (size_t)r * D + h * DH);
   }
 }
 

@@ -339,9 +339,21 @@ struct Model {
              c.n_heads, ns, sp, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
              1.0f / sqrtf((float)DH), ws.part, ws.att_ctr, (uint16_t*)ws.attn);
   }
+  // 128-dim heads: one kernel for every row count (groups of four rows),
+  // so a row's result is the same in the verify pass (K+1 rows), the draft
+  // passes, plain greedy decoding (one row) and prefill chunks of any size
+  void sattn4(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
+    const int ng = (C + 3) / 4;
+    int ns, sp;
+    splits_for(B * ng * c.n_heads, ns, sp);
+    launch_k(tm, MTP_KC_ATTN, k_s_attn4<128>, dim3(ns, c.n_heads, B * ng), dim3(256), 0, s, C,
+             c.n_heads, ns, sp, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
+             1.0f / sqrtf(128.f), ws.part, ws.att_ctr, (uint16_t*)ws.attn);
+  }
   template <int DH>
   void sattn(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
-    if (C <= 1) sattn_launch<DH, 1>(ws, B, C, cache, seq_stride);
+    if (DH == 128) sattn4(ws, B, C, cache, seq_stride);
+    else if (C <= 1) sattn_launch<DH, 1>(ws, B, C, cache, seq_stride);
     else if (C <= 2) sattn_launch<DH, 2>(ws, B, C, cache, seq_stride);
     else if (C <= 4) sattn_launch<DH, 4>(ws, B, C, cache, seq_stride);
     else sattn_launch<DH, 8>(ws, B, C, cache, seq_stride);
