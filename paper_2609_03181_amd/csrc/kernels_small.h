@@ -1575,9 +1575,14 @@ __global__ void __launch_bounds__(512) k_lm_gemm(int nr, int V, int H,
                                                  int32_t* __restrict__ pi,
                                                  float* __restrict__ p2) {
   constexpr int KC = 4;
+  // the per-wave argmax candidates reuse the X staging area once the
+  // products are done (with NG = 16 the two would not leave room for a
+  // second block per CU)
+  static_assert(3 * 8 * 16 * NG * 4 <= KC * NG * 64 * 16, "candidates fit in the staging area");
   __shared__ uint4 xs[KC][NG][64];
-  __shared__ float bv[8][16 * NG], sv[8][16 * NG];
-  __shared__ int bi[8][16 * NG];
+  float(*bv)[16 * NG] = (float(*)[16 * NG])&xs[0][0][0];
+  float(*sv)[16 * NG] = bv + 8;
+  int(*bi)[16 * NG] = (int(*)[16 * NG])(bv + 16);
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int nkt = H / 32;
   const int nt = blockIdx.x * 8 + wv;
@@ -1616,6 +1621,7 @@ __global__ void __launch_bounds__(512) k_lm_gemm(int nr, int V, int H,
     for (int u = 0; u < KC; ++u) a[u] = an[u];
   }
   const int v0 = nt * 16 + 4 * (lane >> 4), r = lane & 15;
+  __syncthreads();  // every wave is done with xs
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
     const int row = r0 + 16 * g + r;
