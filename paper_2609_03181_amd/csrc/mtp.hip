@@ -15,6 +15,12 @@
 #include "kernels_small.h"
 #include "kernels_spec.h"
 
+// 16-entry chunks a routed MoE block takes when a pass has 8 or more row
+// groups (each weight tile read once per block is applied to all of them).
+#ifndef MTP_MOE_CPB
+#define MTP_MOE_CPB 4
+#endif
+
 using namespace mtp;
 
 // Matrices of a bf16 model repacked into MFMA operand tiles (see
@@ -457,7 +463,7 @@ struct Model {
            ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched)
       MTP_MAXT_DISPATCH(H / 128, MTP_ROUTER);
 #undef MTP_ROUTER
-      const int cpb = G >= 8 ? 4 : 1;  // 16-entry chunks per MoE block (more than 16 rows)
+      const int cpb = G >= 8 ? MTP_MOE_CPB : 1;  // 16-entry chunks per MoE block
       if (G > 1)
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
                                    ws.ent_slot, ws.ent_w, cpb, ws.cbp);
