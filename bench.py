@@ -7,8 +7,13 @@ The headline workload is the full-shape B=1 case: 256 vision-prefix rows
 + 512 prompt tokens (real prefill), then verify steps; the value is
 accepted tokens/s (tokens committed per second, bonus included).
 
-Prints one JSON line.  Other workloads (--workload b16 / b64 / tiny) print
-the same line for their configuration.
+Prints one JSON line: with no --workload, the batch-1 headline with the
+batch-16 (forced acceptance) and batch-64 (Zipf routing) workloads as
+sub_records, each with its own roofline; with --workload, that workload's
+line alone.  The roofline unit is the whole verify pass (algorithmic bytes
+of one verifier pass over the K+1 rows of every sequence, over its
+duration as a HIP graph of its own, timed with events on its stream); the
+dominant kernel's own figure is roofline_dominant_kernel.
 """
 from __future__ import annotations
 
@@ -276,65 +281,169 @@ def _f32(a, cfg):
     return synth.bf16_bits_to_f32(a) if cfg.dtype == "bf16" else a
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default="b1", choices=sorted(WORKLOADS) + ["ksweep"])
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--eager", action="store_true", help="time eager launches, not a HIP graph")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain 1 GiB device copy (counter calibration)")
-    ap.add_argument("--traffic-from", nargs=5, metavar=("KERNEL", "FETCH_CSV", "WRITE_CSV",
-                                                        "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
-                    help="record FETCH/WRITE_SIZE traffic of KERNEL for --workload")
-    args = ap.parse_args()
-    if args.traffic_from:
-        traffic_from(args.workload, *args.traffic_from)
-        return
-    if args.copy_calibration:
-        copy_calibration()
-        return
-    if args.gpus != 1:
-        print(f"bench.py measures a single GPU (asked for {args.gpus}): sequences shard across "
-              "GPUs with no exchange inside a step, so one GPU's share is the measured unit",
-              file=sys.stderr)
-        sys.exit(2)
+def _verify_pass_traffic(workload):
+    """Counted HBM bytes of one whole verify pass (profiles/traffic.json,
+    written by --traffic-verify), or None when not taken for this workload
+    or the library sources changed since."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))[workload]["verify_pass"]
+    except (OSError, KeyError, ValueError, TypeError):
+        return None
+    if t.get("src_hash") != src_hash():
+        return None
+    return t["bytes_per_pass"]
 
-    if args.workload == "ksweep":
-        ksweep(args)
-        return
 
+MFMA_FILE = os.path.join(ROOT, "profiles", "mfma.json")
+MFMA_PEAK_TFLOPS = 2500.0   # MI355X dense bf16
+
+
+def _mfma_counters(workload):
+    """MFMA counter summary of the workload's grouped GEMM and LM head
+    (profiles/mfma.json, from --mfma-from), or None when not taken or the
+    library sources changed since."""
+    try:
+        t = json.load(open(MFMA_FILE))[workload]
+    except (OSError, KeyError, ValueError, TypeError):
+        return None
+    if t.get("src_hash") != src_hash():
+        return None
+    return t.get("kernels")
+
+
+def _pass_split(path, counter, marker="FillFunctor"):
+    """Mean per pass of `counter`, summed over the dispatches between
+    consecutive marker kernels: a probe run separates its verify passes
+    with a torch fill kernel, so the passes are the final run of marker
+    intervals that all hold the same number of dispatches (fills made
+    during setup delimit other intervals)."""
+    import csv
+    per = {}
+    names = {}
+    for r in csv.DictReader(open(path)):
+        d = int(r["Dispatch_Id"])
+        names[d] = r["Kernel_Name"]
+        if r["Counter_Name"] == counter:
+            per[d] = per.get(d, 0.0) + float(r["Counter_Value"])
+    ids = sorted(names)
+    marks = [k for k, i in enumerate(ids) if marker in names[i]]
+    spans = [(a, b) for a, b in zip(marks, marks[1:])]
+    if not spans:
+        raise SystemExit(f"no marked passes in {path}")
+    n_last = spans[-1][1] - spans[-1][0]
+    tail = []
+    for a, b in reversed(spans):
+        if b - a != n_last or n_last < 2:
+            break
+        tail.append(sum(per.get(ids[j], 0.0) for j in range(a + 1, b)))
+    if not tail:
+        raise SystemExit(f"no marked passes in {path}")
+    return sum(tail) / len(tail), len(tail)
+
+
+def traffic_verify(workload, fetch_csv, write_csv, copy_fetch, copy_write):
+    """Record the counted HBM bytes of one verify pass of `workload`:
+    FETCH_SIZE and WRITE_SIZE (KiB) summed over a pass's dispatches (two
+    --probe verify counter runs), scaled by the copy calibration (KiB per
+    dispatch of the plain 1 GiB copy, as numbers)."""
+    sf, sw = COPY_BYTES / (float(copy_fetch) * 1024), COPY_BYTES / (float(copy_write) * 1024)
+    f, nf = _pass_split(fetch_csv, "FETCH_SIZE")
+    wv, nw = _pass_split(write_csv, "WRITE_SIZE")
+    entry = {"src_hash": src_hash(), "fetch_kib_per_pass": round(f, 1),
+             "write_kib_per_pass": round(wv, 1), "passes": [nf, nw],
+             "copy_scale": [round(sf, 4), round(sw, 4)],
+             "bytes_per_pass": int(f * 1024 * sf + wv * 1024 * sw)}
+    try:
+        d = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        d = {}
+    d.setdefault(workload, {})["verify_pass"] = entry
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(d, fh, indent=1)
+    print(json.dumps({workload: {"verify_pass": entry}}))
+
+
+def counters_summary(paths):
+    """Per kernel, the mean per-dispatch value of every counter in the
+    rocprofv3 counter_collection.csv files (and the dispatch count), as
+    one JSON object: a short summary of a counter run."""
+    import csv
+    out = {}
+    for path in paths:
+        per = {}
+        for r in csv.DictReader(open(path)):
+            k = (r["Kernel_Name"].removeprefix("void ")[:90], r["Counter_Name"])
+            d = per.setdefault(k, {})
+            d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        for (kern, cnt), d in per.items():
+            e = out.setdefault(kern, {})
+            e[cnt] = round(sum(d.values()) / len(d), 1)
+            e["dispatches"] = len(d)
+    print(json.dumps(out))
+
+
+def mfma_from(workload, summary_json, stats_csv):
+    """Record MFMA counters of `workload` (profiles/mfma.json): per kernel,
+    bf16 MFMA FLOPs per dispatch (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) over
+    the kernel's mean duration (rocprofv3 --stats), and MFMA busy cycles
+    over GRBM_GUI_ACTIVE x SIMDs (the MfmaUtil expression of rocprofv3)."""
+    import csv
+    summ = json.load(open(summary_json))
+    dur = {}
+    for r in csv.DictReader(open(stats_csv)):
+        dur[r["Name"].removeprefix("void ")[:90]] = float(r["AverageNs"]) * 1e-9
+    simds, xcds = 256 * 4, 8   # GRBM_GUI_ACTIVE is reported once per XCD
+    kernels = {}
+    for k, e in summ.items():
+        mops = e.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+        if mops <= 0 or k not in dur:
+            continue
+        fl = mops * 512
+        tf = fl / dur[k] / 1e12
+        util = None
+        if e.get("GRBM_GUI_ACTIVE"):
+            util = round(100 * e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) /
+                         (e["GRBM_GUI_ACTIVE"] / xcds * simds), 2)
+        kernels[k] = {"mfma_flop_per_dispatch": int(fl), "us": round(dur[k] * 1e6, 2),
+                      "TFLOP_s": round(tf, 1), "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS, 4),
+                      "mfma_busy_pct": util, "dispatches": e.get("dispatches")}
+    try:
+        d = json.load(open(MFMA_FILE))
+    except (OSError, ValueError):
+        d = {}
+    d[workload] = {"src_hash": src_hash(), "kernels": kernels}
+    with open(MFMA_FILE, "w") as fh:
+        json.dump(d, fh, indent=1)
+    print(json.dumps({workload: kernels}))
+
+
+def _setup(name, args, steps_needed):
+    """Model, session and inputs of workload `name`, ready for its first
+    step.  Returns (wl, cfg, w, model, s, ctx, prefill_inputs)."""
     import torch
     import synth
-    from paper_2609_03181_amd import _lib
     from paper_2609_03181_amd.session import Model, Session
-
-    wl = WORKLOADS[args.workload]
+    wl = WORKLOADS[name]
     cfg = synth.CONFIGS[wl["model"]]
     B, K = wl["B"], wl["K"]
-    total_steps = args.warmup + args.steps + 8
     t0 = time.time()
     w = synth.make_weights(cfg, 0, 1, zipf_s=wl["zipf"])
-    log(f"weights {time.time() - t0:.1f}s")
-
+    log(f"[{name}] weights {time.time() - t0:.1f}s")
     pages = "new" in wl
     if wl["synthetic"]:
         lo, hi, seed = wl["ctx"]
         ctx = synth.context_lengths(B, lo, hi, seed)
-        max_ctx = int(ctx.max()) + total_steps * (K + 1) + 8
+        max_ctx = int(ctx.max()) + steps_needed * (K + 1) + 8
     else:
         P = wl["n_vis"] + wl["n_txt"]
         ctx = np.full(B, P, np.int32)
-        max_ctx = P + (wl["new"] + 4 * (K + 1) if pages else total_steps * (K + 1)) + 8
-    max_out = wl["new"] if pages else total_steps * (K + 1) + 4
+        max_ctx = P + (wl["new"] + 4 * (K + 1) if pages else steps_needed * (K + 1)) + 8
+    max_out = wl["new"] if pages else steps_needed * (K + 1) + 4
     model = Model(cfg, w, B, max_ctx, K)
-    # the prompt is prefilled in one pass (a pass reads every weight once:
-    # 768 rows take 7.4 ms in one pass against 30 ms in 64-row passes)
+    # the prompt is prefilled in one pass (a pass reads every weight once)
     s = Session(model, B, K, max_out, prefill_rows=64 if wl["synthetic"] else int(ctx.max()))
-    log(f"upload {time.time() - t0:.1f}s")
-
+    log(f"[{name}] upload {time.time() - t0:.1f}s")
+    pin = None
     if wl["synthetic"]:
         _load_synthetic(s, cfg, ctx)
     else:
@@ -347,14 +456,45 @@ def main():
                 vis[b, :wl["n_vis"]] = synth.vision_prefix(cfg, wl["n_vis"], seed=10 + b)
                 tok[b, wl["n_vis"]:] = synth.text_tokens(cfg, wl["n_txt"], seed=11 + b)
         vv = torch.from_numpy(vis.view(np.int16) if cfg.dtype == "bf16" else vis)
+        pin = (torch.from_numpy(tok), vv)
         torch.cuda.synchronize()
         tp = time.perf_counter()
-        s.prefill(torch.from_numpy(tok), vv)
+        s.prefill(*pin)
         torch.cuda.synchronize()
-        log(f"prefill {B}x{P} rows: {1e3 * (time.perf_counter() - tp):.1f} ms")
+        log(f"[{name}] prefill {B}x{P} rows in one pass: {1e3 * (time.perf_counter() - tp):.1f} ms")
     if wl["forced"]:
-        s.set_forced_drafts(torch.from_numpy(_forced_table(s, cfg, B, K, total_steps)))
+        s.set_forced_drafts(torch.from_numpy(_forced_table(s, cfg, B, K, steps_needed)))
     assert s.status() == 0
+    return wl, cfg, w, model, s, ctx, pin
+
+
+def probe_verify(name, args):
+    """Counter probe: eager verify passes of workload `name` separated by a
+    marker kernel (a torch fill), for --traffic-verify and MFMA summaries."""
+    import torch
+    wl, cfg, w, model, s, ctx, pin = _setup(name, args, args.warmup + args.steps + 8)
+    for _ in range(args.warmup):
+        s.step()
+    marker = torch.empty(1, device="cuda")
+    marker.fill_(0)
+    for _ in range(args.steps):
+        s.verify()
+        marker.fill_(0)
+    torch.cuda.synchronize()
+    assert s.status() == 0
+    print(json.dumps({"probe": "verify", "workload": name, "passes": args.steps}))
+
+
+def run_workload(name, args, cpu=False):
+    """One workload: the timed graph-replayed steps and their measurements.
+    Returns the JSON record."""
+    import torch
+    from paper_2609_03181_amd import _lib
+    nb, nk = 8, 4                     # breakdown steps, steps per timed kernel class
+    total_steps = args.warmup + args.steps + nb + nk * len(KERNEL_CLASSES) + 8
+    wl, cfg, w, model, s, ctx, pin = _setup(name, args, total_steps)
+    B, K = wl["B"], wl["K"]
+    pages = "new" in wl
 
     # ---- timed region: graph replays of whole steps
     if not args.eager:
@@ -367,7 +507,7 @@ def main():
         # the whole page job: prefill, then steps until every page has its
         # tokens (checked every 64 steps; finished pages stay frozen)
         t_start = time.perf_counter()
-        s.prefill(torch.from_numpy(tok), vv)
+        s.prefill(*pin)
         n_steps = 0
         while True:
             for _ in range(64):
@@ -378,10 +518,7 @@ def main():
         torch.cuda.synchronize()
         dt = time.perf_counter() - t_start
         accepted = int(s.n_out.sum().item())
-        args.steps = n_steps
-        ms_step = 1e3 * dt / n_steps
-        value = accepted / dt
-        n0 = None
+        steps = n_steps
     else:
         n0 = s.n_out.clone()
         torch.cuda.synchronize()
@@ -391,14 +528,36 @@ def main():
         torch.cuda.synchronize()
         dt = time.perf_counter() - t_start
         accepted = int((s.n_out - n0).sum().item())
-        ms_step = 1e3 * dt / args.steps
-        value = accepted / dt
+        steps = args.steps
+    ms_step = 1e3 * dt / steps
+    value = accepted / dt
+
+    # ---- the verify pass alone: its own graph, replayed on the current
+    # state (a verify pass does not advance the state), timed with events
+    # on the replay stream
+    stream = torch.cuda.current_stream()
+    vg = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(stream)
+    with torch.cuda.graph(vg, stream=cs):
+        s.verify()
+    stream.wait_stream(cs)
+    for _ in range(3):
+        vg.replay()
+    n_vp = max(args.steps, 20)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(n_vp):
+        vg.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    verify_graph_ms = e0.elapsed_time(e1) / n_vp
+    del vg
 
     # ---- per-call breakdown (eager, events on the launch stream) and the
     # routing / cache state each measured step ran on
-    stream = torch.cuda.current_stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)
-    nb = 8
     times = {"draft": [], "verify": [], "accept+commit": []}
     s.route_idx = torch.zeros((cfg.n_layers, B * (K + 1), cfg.top_k), dtype=torch.int32,
                               device="cuda")
@@ -424,8 +583,8 @@ def main():
         times["accept+commit"].append(e[2].elapsed_time(e[3]))
         state.append((kvl, dl, s.route_idx.cpu().numpy().copy()))
     vb, U = zip(*[verify_bytes(cfg, B, K, st[0], st[2]) for st in state])
-    verify_ms = float(np.median(times["verify"]))
     vbytes = float(np.mean(vb))
+    vflops = float(np.mean([verify_flops(cfg, B, K, st[0]) for st in state]))
     dbytes = float(np.mean([draft_bytes(cfg, B, K, st[1], None) for st in state]))
 
     # ---- launch durations of each kernel class (HIP events recorded by the
@@ -436,7 +595,7 @@ def main():
         kname = class_kernel(kc, B * (K + 1))
         tot_ms = tot_b = tot_f = 0.0
         n_l = 0
-        for _ in range(4):
+        for _ in range(nk):
             kvl, dl = snap()
             _lib.mtp_timing_start(model.ctx, kc, 4096)
             s.step()
@@ -445,30 +604,21 @@ def main():
             tot_ms, tot_b, tot_f, n_l = tot_ms + ms, tot_b + b, tot_f + f, n_l + n
         if n_l == 0:
             continue
-        kernels[kname] = {"what": what, "launches_per_step": n_l // 4,
+        kernels[kname] = {"what": what, "launches_per_step": n_l // nk,
                           "us_per_launch": round(1e3 * tot_ms / n_l, 2),
-                          "us_per_step": round(1e3 * tot_ms / 4, 1),
+                          "us_per_step": round(1e3 * tot_ms / nk, 1),
                           "bytes_per_launch": int(tot_b / n_l),
                           "GB_s": round(tot_b / (tot_ms * 1e-3) / 1e9, 1),
                           "TFLOP_s": round(tot_f / (tot_ms * 1e-3) / 1e12, 2)}
     s.route_idx = None
-    if kernels:
-        dom = max(kernels, key=lambda n: kernels[n]["us_per_step"])
-        kd = kernels[dom]
-    else:   # float32 path: no per-kernel hook; the verify pass is the unit
-        dom = "moe_verify_step (whole verify pass)"
-        kd = {"what": "verify pass", "bytes_per_launch": int(vbytes),
-              "us_per_launch": round(1e3 * verify_ms, 2),
-              "GB_s": round(vbytes / (verify_ms * 1e-3) / 1e9, 1)}
-    achieved = kd["GB_s"]
     assert s.status() == 0
-
-    out = {
+    vp_gbs = vbytes / (verify_graph_ms * 1e-3) / 1e9
+    rec = {
         "metric": "accepted tokens/s per GPU",
         "value": round(value, 2),
         "unit": "accepted tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
@@ -476,32 +626,145 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
         "data": "synthetic (seeded random-init weights, N(0,1) vision prefix, uniform tokens)",
-        "config": {"workload": _wl_name(args.workload, wl), "batch": B, "k": K,
+        "config": {"workload": _wl_name(name, wl), "batch": B, "k": K,
                    "mode": "eager" if args.eager else "hipgraph",
-                   "tau": round(accepted / (args.steps * B), 4),
-                   "verify_steps_per_s": round(args.steps / dt, 2)},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": _traffic(args.workload, dom),
-                     "kernel": dom, "what": kd["what"],
-                     "bytes_per_launch": kd["bytes_per_launch"],
-                     "us_per_launch": kd["us_per_launch"]},
-        "verify_pass": {"ms": round(verify_ms, 4), "bytes": int(vbytes),
-                        "GB_s": round(vbytes / (verify_ms * 1e-3) / 1e9, 1),
+                   "tau": None if pages else round(accepted / (steps * B), 4),
+                   "verify_steps_per_s": round(steps / dt, 2)},
+        # the unit of the roofline is the whole verify pass (one verifier
+        # pass over the K+1 rows of every sequence): its algorithmic bytes
+        # over its duration as a graph of its own
+        "roofline": {"bound": "hbm", "achieved": round(vp_gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(vp_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": _verify_pass_traffic(name),
+                     "kernel": "moe_verify_step (whole verify pass)",
+                     "bytes_per_launch": int(vbytes), "us_per_launch": round(1e3 * verify_graph_ms, 2)},
+        "verify_pass": {"ms_graph": round(verify_graph_ms, 4),
+                        "ms_eager": round(float(np.median(times["verify"])), 4),
+                        "bytes": int(vbytes), "flops": int(vflops),
+                        "GB_s": round(vp_gbs, 1),
                         "experts_touched_per_layer": round(float(np.mean(U)), 2)},
         "kernels": kernels,
         "breakdown_ms": {k: round(float(np.median(v)), 4) for k, v in times.items()},
         "draft_bytes_per_step": int(dbytes),
         "src_hash": src_hash(),
     }
+    if kernels:
+        dom = max(kernels, key=lambda n: kernels[n]["us_per_step"])
+        kd = kernels[dom]
+        rec["roofline_dominant_kernel"] = {
+            "bound": "hbm", "achieved": kd["GB_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(kd["GB_s"] / HBM_PEAK_GBS, 4), "traffic": _traffic(name, dom),
+            "kernel": dom, "what": kd["what"], "bytes_per_launch": kd["bytes_per_launch"],
+            "us_per_launch": kd["us_per_launch"]}
+    gu, dn = class_kernel(2, B * (K + 1)), class_kernel(3, B * (K + 1))
+    if gu in kernels and dn in kernels and B * (K + 1) > 16:
+        # the grouped MoE GEMM (gate/up + down): algorithmic FLOPs over its
+        # measured time, against the bf16 MFMA peak and against its own
+        # roofline min(peak, AI x HBM peak)
+        t = (kernels[gu]["us_per_step"] + kernels[dn]["us_per_step"]) * 1e-6
+        fl = (kernels[gu]["TFLOP_s"] * kernels[gu]["us_per_step"] +
+              kernels[dn]["TFLOP_s"] * kernels[dn]["us_per_step"]) * 1e-6 * 1e12
+        by = (kernels[gu]["bytes_per_launch"] * kernels[gu]["launches_per_step"] +
+              kernels[dn]["bytes_per_launch"] * kernels[dn]["launches_per_step"])
+        tf = fl / t / 1e12
+        ai = fl / by
+        ceil = min(MFMA_PEAK_TFLOPS, ai * HBM_PEAK_GBS / 1e3)
+        rec["grouped_gemm"] = {"TFLOP_s": round(tf, 1), "mfma_peak_TFLOP_s": MFMA_PEAK_TFLOPS,
+                               "frac_of_mfma_peak": round(tf / MFMA_PEAK_TFLOPS, 4),
+                               "flop_per_byte": round(ai, 1),
+                               "roofline_TFLOP_s": round(ceil, 1),
+                               "frac_of_own_roofline": round(tf / ceil, 4),
+                               "counters": {k.split("(")[0]: v for k, v in
+                                            (_mfma_counters(name) or {}).items()
+                                            if k.startswith(("mtp::k_s_gu<0,", "mtp::k_s_down",
+                                                             "mtp::k_lm_gemm"))} or None}
     if pages:
-        out["config"]["pages_per_s"] = round(B / dt, 4)
-        out["config"]["new_tokens_per_page"] = wl["new"]
-        out["config"]["job_s"] = round(dt, 3)
-        out["config"]["tau"] = None   # finished pages stay frozen while others finish
-    if not args.no_cpu_baseline and not pages:
+        rec["config"]["pages_per_s"] = round(B / dt, 4)
+        rec["config"]["new_tokens_per_page"] = wl["new"]
+        rec["config"]["job_s"] = round(dt, 3)
+    if cpu and not pages:
         ctx_cpu = int(min(int(ctx[0]), 768))
-        out["cpu_baseline"] = cpu_baseline(cfg, w, K, ctx_cpu)
+        rec["cpu_baseline"] = cpu_baseline(cfg, w, K, ctx_cpu)
+    del s, model
+    torch.cuda.empty_cache()
+    return rec
+
+
+def verify_flops(cfg, B, K, kv_len):
+    """Algorithmic FLOPs of one verify pass: every row through the active
+    parameters (attention projections, router, k routed + S shared experts,
+    LM head) plus the attention scores and values over its context."""
+    H, D, I, S, E, k = (cfg.hidden, cfg.n_heads * cfg.head_dim, cfg.moe_inter, cfg.n_shared,
+                        cfg.n_routed, cfg.top_k)
+    L, V, R = cfg.n_layers, cfg.vocab, B * (K + 1)
+    per_row = L * (3 * D * H + H * D + E * H + (k + S) * 3 * I * H) + V * H
+    attn = L * sum((int(n) + K + 1) * (K + 1) * 2 * D for n in kv_len)
+    return 2 * R * per_row + 2 * attn
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default=None, choices=sorted(WORKLOADS) + ["ksweep"],
+                    help="one workload only (default: batch 1 headline with the batch-16 "
+                         "and batch-64 workloads as sub-records)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="time eager launches, not a HIP graph")
+    ap.add_argument("--probe", choices=["verify"],
+                    help="counter probe: marked verify passes of --workload, no timing")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--traffic-from", nargs=5, metavar=("KERNEL", "FETCH_CSV", "WRITE_CSV",
+                                                        "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="record FETCH/WRITE_SIZE traffic of KERNEL for --workload")
+    ap.add_argument("--traffic-verify", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV",
+                                                          "COPY_FETCH_KIB", "COPY_WRITE_KIB"),
+                    help="record the counted traffic of one verify pass of --workload")
+    ap.add_argument("--counters-summary", nargs="+", metavar="CSV",
+                    help="print per-kernel means of the counters in rocprofv3 CSVs")
+    ap.add_argument("--mfma-from", nargs=2, metavar=("SUMMARY_JSON", "STATS_CSV"),
+                    help="record MFMA counters of --workload from a --counters-summary "
+                         "output and the kernel statistics of a trace run")
+    args = ap.parse_args()
+    if args.counters_summary:
+        counters_summary(args.counters_summary)
+        return
+    if args.mfma_from:
+        mfma_from(args.workload or "b64", *args.mfma_from)
+        return
+    if args.traffic_from:
+        traffic_from(args.workload or "b1", *args.traffic_from)
+        return
+    if args.traffic_verify:
+        traffic_verify(args.workload or "b1", *args.traffic_verify)
+        return
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures a single GPU (asked for {args.gpus}): sequences shard across "
+              "GPUs with no exchange inside a step, so one GPU's share is the measured unit",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.workload == "ksweep":
+        ksweep(args)
+        return
+    if args.probe:
+        probe_verify(args.workload or "b1", args)
+        return
+    if args.workload:
+        print(json.dumps(run_workload(args.workload, args, cpu=not args.no_cpu_baseline)),
+              flush=True)
+        return
+    out = run_workload("b1", args, cpu=not args.no_cpu_baseline)
+    out["sub_records"] = {}
+    for name in ("b16", "b64"):
+        r = run_workload(name, args)
+        keep = ("value", "unit", "ms_per_step", "config", "roofline", "roofline_dominant_kernel",
+                "verify_pass", "grouped_gemm", "breakdown_ms", "kernels")
+        out["sub_records"][name] = {k: r[k] for k in keep if k in r}
     print(json.dumps(out), flush=True)
 
 

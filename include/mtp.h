@@ -55,7 +55,10 @@ typedef enum {
   MTP_ECAPACITY = -2,    /* device: a position would pass max_ctx */
   MTP_EHIP = -3,         /* a HIP call failed */
   MTP_EUNSUPPORTED = -4, /* shape outside what the kernels support */
-  MTP_ETOKEN = -5        /* device: a token id outside [0, vocab) */
+  MTP_ETOKEN = -5,       /* device: a token id outside [0, vocab) */
+  MTP_ERANGE = -6        /* device: a value outside its range (an acceptance length
+                            outside [0, k]; a MoE contribution past the fixed-point
+                            range of the small-batch down projection) */
 } mtp_status;
 
 enum { MTP_F32 = 0, MTP_BF16 = 1 };
@@ -99,22 +102,39 @@ typedef struct mtp_ctx mtp_ctx;
  *   draft KV     [B][2][nh][cap][dh]
  * Position p of sequence b holds the K/V of the row at absolute position p. */
 
-/* Creates a context: validates the shape, uploads a float32 RoPE table
- * [max_ctx][dh/2] (cos, sin from float64 angles) -- the only allocation the
- * library makes.  Returns MTP_EUNSUPPORTED for shapes the kernels do not
- * cover (hidden % 64, head_dim not 64 or 128, n_routed > 64, ...). */
+/* Creates a context: validates the shape and makes the library's only
+ * device allocations, all owned by the context until mtp_destroy:
+ *   - a float32 RoPE table [max_ctx][dh/2] (cos, sin from float64 angles);
+ *   - bf16 models: a second copy of every weight matrix except the
+ *     embedding table, repacked into the MFMA operand-tile layout the
+ *     kernels stream (the embedding table, the norm gains and the router
+ *     bias are read in place, so the caller keeps every weight alive until
+ *     mtp_destroy);
+ *   - a 256-byte device status word of its own (see mtp_status_read).
+ * mtp_context_bytes reports their size (about 6.3 GB for the full-shape
+ * bf16 model).  Synchronises the device once (the repacking).  Returns
+ * MTP_EUNSUPPORTED for shapes the kernels do not cover (hidden % 64,
+ * head_dim not 64 or 128, n_routed > 64, ...), MTP_EHIP when an allocation
+ * or copy fails (nothing is left allocated). */
 mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out /* (host) */);
 void mtp_destroy(mtp_ctx* ctx);
+
+/* Device bytes the context holds (RoPE table, packed weights, status word);
+ * 0 for a NULL context. */
+size_t mtp_context_bytes(const mtp_ctx* ctx);
 
 /* Workspace bytes for steps over `batch` sequences with up to `rows`
  * rows per sequence (a step needs rows = k+1; prefill uses chunks of at
  * most `rows` rows). */
 size_t mtp_workspace_bytes(const mtp_ctx* ctx, int32_t batch, int32_t rows);
 
-/* Blocking read of the sticky device status word (after the caller has
- * synchronised the stream the step ran on). */
+/* Blocking read of the sticky device status (after the caller has
+ * synchronised the stream the step ran on): the workspace's word when it
+ * is set, else the context's own word (set by kv_commit_rollback, which
+ * takes no workspace).  ws may be NULL: the context's word only. */
 mtp_status mtp_status_read(const mtp_ctx* ctx, const void* ws, int32_t* status /* (host) */);
-/* Enqueues a reset of the status word to MTP_OK. */
+/* Enqueues a reset of the context's status word and (ws not NULL) the
+ * workspace's to MTP_OK. */
 mtp_status mtp_status_clear(const mtp_ctx* ctx, void* ws, void* stream);
 
 /* Prefill (the step before the hot path): runs the verifier over n_rows
@@ -145,24 +165,30 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
  * d = 2..k runs one row at position row_pos[b]+n_rows[b]-1+(d-1) with the
  * previous depth's output state and token.  Sets draft_len[b] =
  * row_pos[b]+n_rows[b].  Requires row_pos[b] <= draft_len[b] on entry
- * (device check).  draft_logits [B][k][V] f32 or NULL.  k = 0: no-op. */
+ * (device check).  draft_logits [B][k][V] f32 or NULL; draft_u [B][k][H]
+ * f32 or NULL: the output state u of each depth (the state the next depth
+ * starts from; for checks).  k = 0: no-op. */
 mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
                        const int32_t* next_tok, const int32_t* n_rows, const int32_t* row_pos,
                        void* draft_kv, int32_t* draft_len, int32_t* draft_tok,
-                       float* draft_logits, void* ws, size_t ws_bytes, void* stream);
+                       float* draft_logits, float* draft_u, void* ws, size_t ws_bytes,
+                       void* stream);
 
 /* Verify: rows i = 0..k of sequence b hold pending[b] (i = 0) then
  * draft_tok[b][i-1], at positions kv_len[b]+i.  Writes their K/V in place,
  * runs the verifier, and returns verify_tok [B][k+1] (greedy token of each
  * row), hid [B][k+1][H] (final-norm state b of each row), and optionally
  * logits [B][k+1][V], margin [B][k+1] (top-1 minus top-2 logit),
- * route_idx [L][B*(k+1)][top_k] and route_gap [L][B*(k+1)] (k-th minus
- * (k+1)-th router logit).  kv_len is not changed. */
+ * route_idx [L][B*(k+1)][top_k], route_gap [L][B*(k+1)] (k-th minus
+ * (k+1)-th router logit) and layer_h [L+1][B*(k+1)][H] f32 (the residual
+ * stream entering layer l, and at l = L the last layer's output before the
+ * final norm; for checks).  Row r of the routing and layer outputs is
+ * sequence r / (k+1), row r % (k+1).  kv_len is not changed. */
 mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t* pending,
                            const int32_t* draft_tok, const int32_t* kv_len, void* kv_cache,
                            int32_t* verify_tok, float* hid, float* logits, float* margin,
-                           int32_t* route_idx, float* route_gap, void* ws, size_t ws_bytes,
-                           void* stream);
+                           int32_t* route_idx, float* route_gap, float* layer_h, void* ws,
+                           size_t ws_bytes, void* stream);
 
 /* Acceptance equation: accept_len[b] = m, the longest r <= k with
  * draft_tok[b][s] == verify_tok[b][s] for all s < r; commit_tok[b] =
@@ -172,7 +198,9 @@ mtp_status greedy_accept(int32_t batch, int32_t k, const int32_t* draft_tok,
                          void* stream);
 
 /* Commit / rollback for each unfinished sequence (n_out[b] < limit, limit
- * = min(max_new[b], max_out), max_new NULL = max_out):
+ * = min(max_new[b], max_out), max_new NULL = max_out) whose accept_len[b]
+ * lies in [0, k] (otherwise the context's status word is set to MTP_ERANGE
+ * and the sequence is left unchanged):
  *   n_rows[b] = m+1, row_pos[b] = kv_len[b], kv_len[b] += m+1,
  *   pending[b] = commit_tok[b][m], next_tok[b][0..m] = commit_tok[b][0..m],
  *   out_tok[b][n_out..] += the committed tokens (truncated at the limit).

@@ -33,32 +33,16 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "_oracle.so")
 _lib = None
 
-# Decision tolerances.  Two implementations that round at the same storage
-# points but sum in different orders reach different router logits and
-# token logits; an integer decision (a routing, a greedy token) may then
-# differ only where the oracle's own margin is below the tolerance.
-#   ROUTE_TOL       router k-th vs (k+1)-th logit gap, float32 models;
-#   ROUTE_TOL_BF16  the same for bf16 models: a one-ulp flip of a stored
-#                   bf16 key or value moves every later router logit by
-#                   ~1e-4..1e-3, and a change of summation order alone
-#                   produces such flips.  Measured with float32 instead of
-#                   float64 dot products: router logits move by up to 2.8e-3
-#                   in a 2-layer model over 32 rows; over the full-shape
-#                   768-row prefix by up to 2.9e-3 in layer 0 and a median
-#                   1.3e-2 / 99th percentile 5.4e-2 in layer 11 (sequential
-#                   float32 sums, routing differences left to cascade).  The
-#                   GPU path's routings lie within 2.5e-2 of the oracle's
-#                   top-k there (oracle following them), so 5e-2 is twice
-#                   that;
-#   ARGMAX_TOL      top-1 vs top-2 token logit gap.
+# Decision tolerances of the oracle's own checks (pins of the oracle
+# against brute force): where two correct evaluations that sum in different
+# orders may pick different integers.  The parity tests against the GPU
+# path take their per-layer routing tolerances from a drift measurement
+# (tests/tolerances.py) and pass them to verify_rows.
+#   ROUTE_TOL   router k-th vs (k+1)-th logit gap (the gating margin the
+#               workload statement fixes);
+#   ARGMAX_TOL  top-1 vs top-2 token logit gap.
 ROUTE_TOL = 1e-3
-ROUTE_TOL_BF16 = 5e-2
 ARGMAX_TOL = 0.05
-
-
-def route_tolerances(cfg) -> np.ndarray:
-    """Per-layer routing tolerance of a model configuration."""
-    return np.full(cfg.n_layers, ROUTE_TOL_BF16 if cfg.dtype == "bf16" else ROUTE_TOL)
 
 
 def build(force: bool = True) -> str:
@@ -89,15 +73,22 @@ class _Weights(ctypes.Structure):
 def _L():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
+        # MTP_ORACLE_LIB: another build of oracle.c (the planted-mistake
+        # check loads deliberately broken copies through it)
+        path = os.environ.get("MTP_ORACLE_LIB") or _LIB_PATH
+        if path == _LIB_PATH and not os.path.exists(_LIB_PATH):
             build(force=False)
-        lib = ctypes.CDLL(_LIB_PATH)
+        lib = ctypes.CDLL(path)
         vp, i32, f32, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_double
         lib.orc_verify_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.orc_verify_rows.restype = i32
         lib.orc_draft_rows.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.orc_draft_rows.restype = i32
+        lib.orc_verify_layer.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp, vp, f32, vp, vp,
+                                         vp, vp]
+        lib.orc_verify_layer.restype = i32
+        lib.orc_head.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp]
         lib.orc_rmsnorm.argtypes = [vp, vp, i32, dbl, vp]
         lib.orc_rope.argtypes = [vp, i32, i32, dbl]
         lib.orc_attend.argtypes = [vp, vp, vp, i32, i32, vp]
@@ -143,7 +134,9 @@ class Oracle:
     def verify_rows(self, kv, tok, pos, emb=None, head_mask=None, want_logits=False,
                     want_routes=False, follow_route=None, route_tol=None,
                     want_router_logits=False):
-        """route_tol: per-layer follow tolerance (default route_tolerances)."""
+        """follow_route [L][n][k]: routes chosen elsewhere, adopted where
+        they are a top-k set of the oracle's logits up to route_tol[l]
+        (required with follow_route: per-layer tolerance)."""
         c = self.cfg
         tok = _c(tok, np.int32)
         pos = _c(pos, np.int32)
@@ -162,8 +155,10 @@ class Oracle:
         rl = (np.empty((c.n_layers, n, c.n_routed), np.float32) if want_router_logits
               else None)
         fr = _c(follow_route, np.int32)
+        if follow_route is not None and route_tol is None:
+            raise ValueError("follow_route needs a per-layer route_tol")
         rt = np.ascontiguousarray(np.broadcast_to(
-            route_tolerances(c) if route_tol is None else np.asarray(route_tol, np.float32),
+            np.float32(ROUTE_TOL) if route_tol is None else np.asarray(route_tol, np.float32),
             (c.n_layers,)), np.float32)
         nf = ctypes.c_int(0)
         rc = _L().orc_verify_rows(ctypes.byref(self.dims), ctypes.byref(self.wts), _p(kv),
@@ -174,6 +169,47 @@ class Oracle:
             raise ValueError("oracle: position outside the KV capacity")
         return dict(b=b, amax=amax, margin=margin, logits=logits, route_idx=ri, route_w=rw,
                     route_gap=rg, route_rejected=rc, route_followed=nf.value, router_logits=rl)
+
+    def verify_layer(self, layer, kv_l, h, pos, follow_route=None, route_tol=None):
+        """One verifier layer from the layer input h [n][H] (float32) over
+        the layer's KV slab kv_l [2][nh][cap][dh] (float32; the rows' K/V
+        are written into it).  follow_route [n][k] with route_tol (a
+        float): routes adopted at near-ties, as in verify_rows.  Returns the
+        layer output and the layer's routing (route_idx [n][k], route_gap
+        [n], router_logits [n][E]) and the follow counts."""
+        c = self.cfg
+        h = np.array(h, dtype=np.float32, copy=True, order="C")
+        pos = _c(pos, np.int32)
+        n = len(pos)
+        assert kv_l.dtype == np.float32 and kv_l.flags.c_contiguous
+        if follow_route is not None and route_tol is None:
+            raise ValueError("follow_route needs route_tol")
+        fr = _c(follow_route, np.int32)
+        ri = np.empty((n, c.top_k), np.int32)
+        rg = np.empty(n, np.float32)
+        rl = np.empty((n, c.n_routed), np.float32)
+        nf = ctypes.c_int(0)
+        rc = _L().orc_verify_layer(ctypes.byref(self.dims), ctypes.byref(self.wts), layer,
+                                   _p(kv_l), kv_l.shape[2], n, _p(pos), _p(h), _p(fr),
+                                   float(route_tol or 0.0), ctypes.byref(nf), _p(ri), _p(rg),
+                                   _p(rl))
+        if rc < 0:
+            raise ValueError("oracle: position outside the KV capacity")
+        return dict(h=h, route_idx=ri, route_gap=rg, router_logits=rl, route_rejected=rc,
+                    route_followed=nf.value)
+
+    def head(self, h):
+        """Final norm, LM head and greedy argmax of residual rows h [n][H]."""
+        c = self.cfg
+        h = _c(h, np.float32)
+        n = h.shape[0]
+        b = np.empty((n, c.hidden), np.float32)
+        logits = np.empty((n, c.vocab), np.float32)
+        amax = np.full(n, -1, np.int32)
+        margin = np.full(n, np.nan, np.float32)
+        _L().orc_head(ctypes.byref(self.dims), ctypes.byref(self.wts), n, _p(h), _p(b),
+                      _p(logits), _p(amax), _p(margin))
+        return dict(b=b, logits=logits, amax=amax, margin=margin)
 
     def draft_rows(self, dkv, tok, a, pos, emb=None, head_mask=None, want_logits=False):
         c = self.cfg
@@ -290,6 +326,7 @@ class SeqState:
     last_logits: np.ndarray | None = None   # logits of the last prefill row
     prefill_routes_followed: int = 0        # near-tie routes adopted from follow_route
     prefill_routes_rejected: int = 0        # given routes that were not near-ties
+    prefill_route_gap: np.ndarray | None = None   # [L][P] k-th vs (k+1)-th router gaps
 
     @property
     def finished(self) -> bool:
@@ -297,12 +334,12 @@ class SeqState:
 
 
 def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30,
-            follow_route=None) -> SeqState:
+            follow_route=None, route_tol=None) -> SeqState:
     """Verifier over the prefix (vision rows then text tokens), greedy token
     of the last row, and the draft prefill: rows p = 0..P-2 in base form
     (state b_p, input row p+1 -- a vision row inside the visual prefix).
     follow_route [L][P][k]: routes chosen elsewhere, adopted where they are
-    near-ties of the oracle's own (see Oracle.verify_rows)."""
+    near-ties of the oracle's own up to route_tol[l] (see Oracle.verify_rows)."""
     c = orc.cfg
     nv = 0 if vision is None else len(vision)
     tokens = np.asarray(tokens, dtype=np.int32)
@@ -315,7 +352,8 @@ def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30,
     hm = np.zeros(P, np.uint8)
     hm[P - 1] = 1
     r = orc.verify_rows(kv, tok, np.arange(P), emb=emb, head_mask=hm, want_logits=True,
-                        want_routes=follow_route is not None, follow_route=follow_route)
+                        want_routes=follow_route is not None, follow_route=follow_route,
+                        route_tol=route_tol)
     pending = int(r["amax"][P - 1])
     if P >= 2:
         orc.draft_rows(dkv, tok[1:], r["b"][:P - 1], np.arange(P - 1), emb=emb[1:])
@@ -324,7 +362,8 @@ def prefill(orc: Oracle, cap: int, vision, tokens, max_new: int = 1 << 30,
                     draft_len=P - 1, out=[pending], max_new=max_new,
                     last_logits=r["logits"][P - 1].copy(),
                     prefill_routes_followed=r["route_followed"],
-                    prefill_routes_rejected=r["route_rejected"])
+                    prefill_routes_rejected=r["route_rejected"],
+                    prefill_route_gap=r["route_gap"])
 
 
 def draft_chain(orc: Oracle, st: SeqState, K: int):

@@ -57,6 +57,31 @@ typedef struct {
 /* storage types                                                     */
 /* ---------------------------------------------------------------- */
 
+/* Sensitivity-measurement switch (never set for reference values): when
+ * nonzero, every sum the oracle forms in float64 -- weight dot products,
+ * norm sums of squares, attention scores, softmax sums and the weighted
+ * value sum, the router softmax -- is formed in float32 instead, by
+ * pairwise summation (each product rounded to float32, halves summed
+ * recursively down to blocks of 8 summed in order), and each elementwise
+ * step (SwiGLU, RoPE, the MoE combine) rounds to float32.  That is a
+ * different but equally valid float32 evaluation of the same model at the
+ * same storage points, with about as many roundings in a chain as a
+ * blocked or tree-shaped reduction; the distance between the two shows
+ * how far summation order alone moves each output. */
+static int g_sum32 = 0;
+void orc_set_sum32(int on) { g_sum32 = on; }
+
+/* pairwise float32 sum of v[0..n) */
+static float psum32(const float* v, int n) {
+  if (n <= 8) {
+    float s = 0.f;
+    for (int i = 0; i < n; ++i) s += v[i];
+    return s;
+  }
+  const int h = n / 2;
+  return psum32(v, h) + psum32(v + h, n - h);
+}
+
 /* bfloat16 round-to-nearest-even of a float32 value, returned widened */
 static float bf16_round(float f) {
   uint32_t u;
@@ -93,16 +118,11 @@ static inline const void* woff(const orc_dims* d, const void* base, size_t elems
   return (const char*)base + elems * wsize(d);
 }
 
-/* Sensitivity-measurement switch (never set for reference values): when
- * nonzero, weight dot products accumulate in float32 (sequentially) instead
- * of float64, a different but equally valid summation that shows how far
- * rounding alone moves the outputs. */
-static int g_sum32 = 0;
-void orc_set_sum32(int on) { g_sum32 = on; }
-
 static double wdot32(const orc_dims* d, const void* w, const float* x, int n) {
-  float s = 0.f;
-  for (int k = 0; k < n; ++k) s += wload(d, w, (size_t)k) * x[k];
+  float* t = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+  for (int k = 0; k < n; ++k) t[k] = wload(d, w, (size_t)k) * x[k];
+  const float s = psum32(t, n);
+  free(t);
   return s;
 }
 
@@ -154,6 +174,14 @@ static void linear(const orc_dims* d, const void* W, int no, int ni, const float
 
 /* RMSNorm: out_i = x_i / sqrt(mean(x^2) + eps) * g_i (float32 result). */
 void orc_rmsnorm(const float* x, const float* g, int n, double eps, float* out) {
+  if (g_sum32) {
+    float* t = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+    for (int i = 0; i < n; ++i) t[i] = x[i] * x[i];
+    const float r = 1.0f / sqrtf(psum32(t, n) / (float)n + (float)eps);
+    free(t);
+    for (int i = 0; i < n; ++i) out[i] = x[i] * r * g[i];
+    return;
+  }
   double ss = 0;
   for (int i = 0; i < n; ++i) ss += (double)x[i] * x[i];
   double r = 1.0 / sqrt(ss / n + eps);
@@ -171,6 +199,11 @@ void orc_rope(float* x, int dh, int pos, double theta) {
     double ang = (double)pos * inv;
     float c = (float)cos(ang), s = (float)sin(ang);
     float a = x[i], b = x[i + half];
+    if (g_sum32) {
+      x[i] = a * c - b * s;
+      x[i + half] = b * c + a * s;
+      continue;
+    }
     x[i] = (float)((double)a * c - (double)b * s);
     x[i + half] = (float)((double)b * c + (double)a * s);
   }
@@ -178,7 +211,33 @@ void orc_rope(float* x, int dh, int pos, double theta) {
 
 /* One attention head of one query row: scores s_j = (q . k_j) / sqrt(dh)
  * for j < n_keys (rows of K/V with stride dh), softmax, o = sum_j p_j v_j. */
+static void attend32(const float* q, const float* K, const float* V, int n_keys, int dh,
+                     float* o) {
+  const float scale = 1.0f / sqrtf((float)dh);
+  const size_t nk = (size_t)(n_keys > 0 ? n_keys : 1);
+  float* s = (float*)malloc(sizeof(float) * nk);
+  float* t = (float*)malloc(sizeof(float) * (nk > (size_t)dh ? nk : (size_t)dh));
+  float m = -INFINITY;
+  for (int j = 0; j < n_keys; ++j) {
+    for (int c = 0; c < dh; ++c) t[c] = q[c] * K[(size_t)j * dh + c];
+    s[j] = psum32(t, dh) * scale;
+    if (s[j] > m) m = s[j];
+  }
+  for (int j = 0; j < n_keys; ++j) s[j] = expf(s[j] - m);
+  const float l = psum32(s, n_keys);
+  for (int c = 0; c < dh; ++c) {
+    for (int j = 0; j < n_keys; ++j) t[j] = s[j] * V[(size_t)j * dh + c];
+    o[c] = psum32(t, n_keys) / l;
+  }
+  free(s);
+  free(t);
+}
+
 void orc_attend(const float* q, const float* K, const float* V, int n_keys, int dh, float* o) {
+  if (g_sum32) {
+    attend32(q, K, V, n_keys, dh, o);
+    return;
+  }
   double scale = 1.0 / sqrt((double)dh);
   double* s = (double*)malloc(sizeof(double) * (size_t)(n_keys > 0 ? n_keys : 1));
   double m = -INFINITY;
@@ -272,9 +331,15 @@ void orc_router(const orc_dims* d, const orc_weights* w, int layer, const float*
     logits[e] = r;
     if (r > mx) mx = r;
   }
-  double sum = 0;
-  for (int e = 0; e < E; ++e) sum += exp((double)logits[e] - mx);
-  for (int e = 0; e < E; ++e) probs[e] = (float)(exp((double)logits[e] - mx) / sum);
+  if (g_sum32) {
+    for (int e = 0; e < E; ++e) probs[e] = expf(logits[e] - (float)mx);
+    const float sum = psum32(probs, E);
+    for (int e = 0; e < E; ++e) probs[e] /= sum;
+  } else {
+    double sum = 0;
+    for (int e = 0; e < E; ++e) sum += exp((double)logits[e] - mx);
+    for (int e = 0; e < E; ++e) probs[e] = (float)(exp((double)logits[e] - mx) / sum);
+  }
   unsigned char* taken = (unsigned char*)calloc((size_t)E, 1);
   for (int j = 0; j < k; ++j) {
     int best = -1;
@@ -303,7 +368,7 @@ static void swiglu_expert(const orc_dims* d, const void* Wg, const void* Wu, con
   linear(d, Wg, I, H, y, nr, g);
   linear(d, Wu, I, H, y, nr, u);
   for (size_t i = 0; i < (size_t)nr * I; ++i) {
-    float gu = (float)(silu(g[i]) * (double)u[i]);
+    float gu = g_sum32 ? g[i] / (1.0f + expf(-g[i])) * u[i] : (float)(silu(g[i]) * (double)u[i]);
     act[i] = st_in(d, gu);
   }
 #pragma omp parallel for schedule(static)
@@ -378,7 +443,8 @@ static int moe_sublayer(const orc_dims* d, const orc_weights* w, int layer, int 
   for (int s = 0; s < S; ++s) {
     swiglu_expert(d, woff(d, shg, (size_t)s * I * H), woff(d, shg, (size_t)(S + s) * I * H), shd,
                   S * I, s * I, I, y, nr, tmp);
-    for (size_t i = 0; i < (size_t)nr * H; ++i) delta[i] += tmp[i];
+    for (size_t i = 0; i < (size_t)nr * H; ++i)
+      delta[i] = g_sum32 ? (double)((float)delta[i] + tmp[i]) : delta[i] + tmp[i];
   }
   /* routed experts, in ascending expert id, over the rows that chose them */
   int32_t* rows = (int32_t*)malloc(sizeof(int32_t) * (size_t)nr);
@@ -396,7 +462,11 @@ static int moe_sublayer(const orc_dims* d, const orc_weights* w, int layer, int 
     for (int t = 0; t < ne; ++t) {
       int r = rows[t];
       float p = pr[(size_t)r * E + e];
-      for (int i = 0; i < H; ++i) delta[(size_t)r * H + i] += (double)(float)((double)p * tmp[(size_t)t * H + i]);
+      for (int i = 0; i < H; ++i) {
+        const float c = (float)((double)p * tmp[(size_t)t * H + i]);
+        double* dv = delta + (size_t)r * H + i;
+        *dv = g_sum32 ? (double)((float)*dv + c) : *dv + c;
+      }
     }
   }
   for (int r = 0; r < nr; ++r) {
@@ -505,6 +575,41 @@ int orc_verify_rows(const orc_dims* d, const orc_weights* w, float* kv, int cap,
   free(h);
   free(b);
   return bad;
+}
+
+/* One verifier layer (attention sub-layer, then MoE sub-layer) for nr rows
+ * of one sequence at positions pos[r], from the layer input h [nr][H]
+ * (overwritten with the layer output) and the layer's KV slab kv_l =
+ * [2][nh][cap][dh] (the rows' K/V are written at their positions before
+ * any row attends; positions below must hold K/V).  follow [nr][k] (or
+ * NULL): routes adopted at near-ties up to tol, as in orc_verify_rows.
+ * Routing outputs for this layer only.  Returns the number of rejected
+ * route sets, or -1 on a bad position. */
+int orc_verify_layer(const orc_dims* d, const orc_weights* w, int layer, float* kv_l, int cap,
+                     int nr, const int32_t* pos, float* h, const int32_t* follow, float tol,
+                     int* n_followed, int32_t* route_idx, float* route_gap,
+                     float* router_logits) {
+  const int H = d->hidden, nhd = d->n_heads * d->head_dim;
+  for (int r = 0; r < nr; ++r)
+    if (pos[r] < 0 || pos[r] >= cap) return -1;
+  attn_sublayer(d, w->attn_norm + (size_t)layer * H, woff(d, w->wqkv, (size_t)layer * 3 * nhd * H),
+                woff(d, w->wo, (size_t)layer * H * nhd), kv_l, cap, nr, pos, h);
+  return moe_sublayer(d, w, layer, nr, h, follow, tol, n_followed, route_idx, NULL, route_gap,
+                      router_logits);
+}
+
+/* The verifier's head on nr residual rows h [nr][H]: b = final RMSNorm
+ * (b_out, optional), then the LM head and greedy argmax of every row
+ * (logits [nr][V] optional, amax, margin). */
+void orc_head(const orc_dims* d, const orc_weights* w, int nr, const float* h, float* b_out,
+              float* logits, int32_t* amax, float* margin) {
+  const int H = d->hidden;
+  float* b = (float*)malloc(sizeof(float) * (size_t)nr * H);
+  for (int r = 0; r < nr; ++r)
+    orc_rmsnorm(h + (size_t)r * H, w->final_norm, H, d->rms_eps, b + (size_t)r * H);
+  if (b_out) memcpy(b_out, b, sizeof(float) * (size_t)nr * H);
+  lm_head(d, w, b, nr, NULL, logits, amax, margin);
+  free(b);
 }
 
 /* ---------------------------------------------------------------- */

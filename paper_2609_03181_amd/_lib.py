@@ -9,13 +9,15 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmtp.so")
 
-MTP_OK, MTP_EINVAL, MTP_ECAPACITY, MTP_EHIP, MTP_EUNSUPPORTED, MTP_ETOKEN = 0, -1, -2, -3, -4, -5
+(MTP_OK, MTP_EINVAL, MTP_ECAPACITY, MTP_EHIP, MTP_EUNSUPPORTED, MTP_ETOKEN,
+ MTP_ERANGE) = 0, -1, -2, -3, -4, -5, -6
 MTP_F32, MTP_BF16 = 0, 1
 STATUS_NAMES = {0: "MTP_OK", -1: "MTP_EINVAL", -2: "MTP_ECAPACITY", -3: "MTP_EHIP",
-                -4: "MTP_EUNSUPPORTED", -5: "MTP_ETOKEN"}
+                -4: "MTP_EUNSUPPORTED", -5: "MTP_ETOKEN", -6: "MTP_ERANGE"}
 
 # every symbol include/mtp.h declares
-EXPORTS = ("mtp_create", "mtp_destroy", "mtp_workspace_bytes", "mtp_status_read",
+EXPORTS = ("mtp_create", "mtp_destroy", "mtp_context_bytes", "mtp_workspace_bytes",
+           "mtp_status_read",
            "mtp_status_clear", "mtp_prefill", "mtp_draft_k", "moe_verify_step",
            "greedy_accept", "kv_commit_rollback", "mtp_bench_override_drafts",
            "mtp_timing_start", "mtp_timing_stop")
@@ -64,13 +66,14 @@ def load():
     sig = {
         "mtp_create": ([P, P, P], I32),
         "mtp_destroy": ([P], None),
+        "mtp_context_bytes": ([P], SZ),
         "mtp_workspace_bytes": ([P, I32, I32], SZ),
         "mtp_status_read": ([P, P, P], I32),
         "mtp_status_clear": ([P, P, P], I32),
         "mtp_prefill": ([P, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, P, P, SZ,
                          P], I32),
-        "mtp_draft_k": ([P, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P], I32),
-        "moe_verify_step": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "mtp_draft_k": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "moe_verify_step": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "greedy_accept": ([I32, I32, P, P, P, P, P], I32),
         "kv_commit_rollback": ([P, I32, I32, P, P, P, P, P, P, P, P, P, I32, P, P], I32),
         "mtp_bench_override_drafts": ([I32, I32, P, I32, P, P, P], I32),
@@ -100,6 +103,10 @@ def mtp_destroy(ctx: int) -> None:
     load().mtp_destroy(ctx)
 
 
+def mtp_context_bytes(ctx: int) -> int:
+    return int(load().mtp_context_bytes(ctx))
+
+
 def mtp_workspace_bytes(ctx: int, batch: int, rows: int) -> int:
     return int(load().mtp_workspace_bytes(ctx, batch, rows))
 
@@ -123,17 +130,17 @@ def mtp_prefill(ctx, batch, k, n_rows, tok, vision, kv_cache, draft_kv, kv_len, 
 
 
 def mtp_draft_k(ctx, batch, k, hid, next_tok, n_rows, row_pos, draft_kv, draft_len, draft_tok,
-                draft_logits, ws, ws_bytes, stream):
+                draft_logits, draft_u, ws, ws_bytes, stream):
     _check("mtp_draft_k", load().mtp_draft_k(ctx, batch, k, hid, next_tok, n_rows, row_pos,
-                                             draft_kv, draft_len, draft_tok, draft_logits, ws,
-                                             ws_bytes, stream))
+                                             draft_kv, draft_len, draft_tok, draft_logits,
+                                             draft_u, ws, ws_bytes, stream))
 
 
 def moe_verify_step(ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_tok, hid, logits,
-                    margin, route_idx, route_gap, ws, ws_bytes, stream):
+                    margin, route_idx, route_gap, layer_h, ws, ws_bytes, stream):
     _check("moe_verify_step", load().moe_verify_step(
         ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_tok, hid, logits, margin,
-        route_idx, route_gap, ws, ws_bytes, stream))
+        route_idx, route_gap, layer_h, ws, ws_bytes, stream))
 
 
 def greedy_accept(batch, k, draft_tok, verify_tok, accept_len, commit_tok, stream):

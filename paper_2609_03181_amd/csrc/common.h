@@ -67,18 +67,6 @@ __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_f<0x143, 0xc>(-INFINITY, v));
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
-// reference reductions through LDS permutes (for checks)
-__device__ __forceinline__ float wave_sum_shfl(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, MTP_WAVE);
-  return v;
-}
-__device__ __forceinline__ float wave_max_shfl(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, MTP_WAVE));
-  return v;
-}
-
 // block-wide sum over blockDim.x threads (multiple of 64, <= 1024)
 __device__ __forceinline__ float block_sum(float v, float* red /* >= 16 floats */) {
   v = wave_sum(v);
@@ -184,6 +172,19 @@ __device__ __forceinline__ void lds_wait() { __builtin_amdgcn_s_waitcnt(0xc07f);
 // loaded with agent-scope atomic accesses (write-through stores and loads
 // that do not hit stale L2 lines); vmem_release() orders those stores
 // before a following flag atomic by waiting for their completion.
+//
+// The hand-off (a partial-result merge by the last block of a group):
+//   writer: st_agent partials; vmem_release (vmcnt(0): the write-through
+//           stores have completed); agent-scope fetch_add on the count.
+//   reader: the block whose fetch_add returned the last count waits for
+//           that return (vmcnt), passes a workgroup barrier, and only then
+//           issues its ld_agent loads -- agent-scope atomic loads, which
+//           read at the coherence point and so see every completed store.
+// An agent-scope acquire fence (buffer_inv sc1 on gfx950) is what makes
+// later *non-atomic* loads observe such stores; every cross-block read here
+// is an agent-scope atomic load issued after the count was observed, so
+// none is used -- in the last block it costs 1.2-1.5 us per launch of the
+// attention and MoE-down kernels (measured), on the step's critical path.
 __device__ __forceinline__ void st_agent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -194,6 +195,7 @@ __device__ __forceinline__ void vmem_release() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 }
+
 
 // sticky status: the first error code wins
 __device__ __forceinline__ void set_status(int32_t* status, int32_t code) {

@@ -1319,7 +1319,20 @@ __global__ void __launch_bounds__(256) k_s_gu_stream(int R, int H, int I, int SI
 // wave-summed partial (write-through); the last block of the strip adds the
 // NG partials and the rounded total to h.  ctr[H/16] must be zero at launch
 // (it is left at zero).
-__device__ __forceinline__ long long fx32(float x) { return __float2ll_rn(x * 4294967296.0f); }
+// Range: a contribution must be finite and below 2^24 in magnitude; with at
+// most 127 contributions per output (E <= 64 routed plus the shared
+// experts) the 64-bit sum then stays below 2^63.  Contributions outside
+// that range are dropped and set MTP_ERANGE.  Resolution is 2^-32 (finer
+// than a float32 ulp for |values| above 2^-9; below that the sum keeps
+// an absolute error under 2^-33 per contribution).
+constexpr float kFxMax = 16777216.0f;  // 2^24
+__device__ __forceinline__ long long fx32(float x, bool& bad) {
+  if (!(fabsf(x) < kFxMax)) {
+    bad = true;
+    return 0;
+  }
+  return __float2ll_rn(x * 4294967296.0f);
+}
 
 template <int NG>
 __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I, int S,
@@ -1336,7 +1349,8 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
                                                       const int32_t* __restrict__ n_touched,
                                                       unsigned long long* __restrict__ part,
                                                       int32_t* __restrict__ ctr,
-                                                      float* __restrict__ h) {
+                                                      float* __restrict__ h,
+                                                      int32_t* __restrict__ status) {
   __shared__ long long acc_l[4][SR_MAX][17];
   __shared__ int last;
   const int lane = threadIdx.x & 63;
@@ -1350,6 +1364,7 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
   __syncthreads();
   const int nkt = I / 32;
   const int t = lane & 15;
+  bool bad = false;
   for (int v = gq * 4 + w; v < nvirt; v += NG * 4) {
     const uint4* A;
     const uint16_t* xrow = nullptr;
@@ -1375,9 +1390,10 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
     const f32x4_t a = sk_range<8>(A, 0, nkt, xrow, f32x4_t{0.f, 0.f, 0.f, 0.f}, true);
     if (row >= 0) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += fx32(wt * a[q]);
+      for (int q = 0; q < 4; ++q) acc_l[w][row][4 * (lane >> 4) + q] += fx32(wt * a[q], bad);
     }
   }
+  if (bad) set_status(status, MTP_ERANGE);
   __syncthreads();
   const int rr = threadIdx.x >> 4, f = threadIdx.x & 15;
   unsigned long long* pp = part + ((size_t)gq * R + rr) * H + nt * 16 + f;

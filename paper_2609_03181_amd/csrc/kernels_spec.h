@@ -24,19 +24,24 @@ __global__ void k_accept(int B, int K, const int32_t* __restrict__ draft,
 
 // Commit of the m+1 rows: length update only (their K/V already sit at
 // their absolute positions; rows past the new length are dropped by the
-// length itself).  Finished sequences are frozen.
+// length itself).  Finished sequences are frozen.  An acceptance length
+// outside [0, K] sets MTP_ERANGE and leaves the sequence unchanged.
 __global__ void k_commit(int B, int K, const int32_t* __restrict__ accept_len,
                          const int32_t* __restrict__ commit, int32_t* __restrict__ kv_len,
                          int32_t* __restrict__ n_rows, int32_t* __restrict__ row_pos,
                          int32_t* __restrict__ pending, int32_t* __restrict__ next_tok,
                          const int32_t* __restrict__ max_new, int32_t* __restrict__ out_tok,
-                         int max_out, int32_t* __restrict__ n_out) {
+                         int max_out, int32_t* __restrict__ n_out, int32_t* __restrict__ status) {
   int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
   int limit = max_new ? min(max_new[b], max_out) : max_out;
   int no = n_out[b];
   if (no >= limit) return;
   int m = accept_len[b];
+  if (m < 0 || m > K) {
+    set_status(status, MTP_ERANGE);
+    return;
+  }
   const int32_t* c = commit + (size_t)b * (K + 1);
   int old = kv_len[b];
   kv_len[b] = old + m + 1;

@@ -43,8 +43,10 @@ struct Timing {
 struct mtp_ctx {
   mtp_config cfg;
   mtp_weights w;
-  float2* rope;  // [max_ctx][head_dim/2] (cos, sin)
-  Packed pk;     // bf16 models only
+  float2* rope;      // [max_ctx][head_dim/2] (cos, sin)
+  int32_t* dstatus;  // status word of the calls without a workspace
+  Packed pk;         // bf16 models only
+  size_t pk_bytes;   // bytes of the packed copy
   int n_split;   // attention key splits ...
   int spl;       // ... of spl positions each (multiple of 64)
   int n_cu;      // compute units of the device the context was created on
@@ -213,12 +215,23 @@ struct Model {
   // or on ws.head_row only.
   // embedded: ws.h already holds the input rows (the caller fused the
   // embedding into its row setup)
+  // layer_h (checks): h entering layer l at layer_h + l*R*H, the last
+  // layer's output at layer_h + L*R*H
+  void snap_h(float* layer_h, int l, int R) {
+    if (layer_h)
+      (void)hipMemcpyAsync(layer_h + (size_t)l * R * c.hidden, pk_h, (size_t)R * c.hidden * 4,
+                           hipMemcpyDeviceToDevice, s);
+  }
+  const float* pk_h = nullptr;  // ws.h of the current call (for snap_h)
+
   void verifier(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
                 float* hid, bool head_all, int32_t* tok, int per, int ostride, float* logits,
-                float* margin, int32_t* route_idx, float* route_gap, bool embedded = false) {
+                float* margin, int32_t* route_idx, float* route_gap, bool embedded = false,
+                float* layer_h = nullptr) {
+    pk_h = ws.h;
     if constexpr (BF) {
       verifier_mfma(ws, B, C, vision, vis_ld, vis_off, kv, hid, head_all, tok, per, ostride,
-                    logits, margin, route_idx, route_gap, embedded);
+                    logits, margin, route_idx, route_gap, embedded, layer_h);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -230,6 +243,7 @@ struct Model {
       k_embed<BF><<<R, 256, H * sizeof(float), s>>>(R, C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed,
                                                   vision, vis_ld, vis_off, ws.h, ws.status);
     for (int l = 0; l < L; ++l) {
+      snap_h(layer_h, l, R);
       attn_sublayer(ws, B, C, w.attn_norm + (size_t)l * H, wp(w.wqkv, (size_t)l * 3 * D * H),
                     wp(w.wo, (size_t)l * H * D), kv + (size_t)l * layer_stride, seq_stride);
       k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.ffn_norm + (size_t)l * H,
@@ -246,6 +260,7 @@ struct Model {
           R, k, H, I, SI, (const T*)ws.act, ws.ridx, ws.rw, wp(w.exp_down, (size_t)l * E * H * I),
           wp(w.sh_down, (size_t)l * H * SI), ws.h);
     }
+    snap_h(layer_h, L, R);
     k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.final_norm, (float)c.rms_eps, hid, H,
                                     nullptr, 0, 0);
     if (!tok) return;
@@ -431,7 +446,7 @@ struct Model {
   void verifier_mfma(const Ws& ws, int B, int C, const T* vision, int vis_ld, int vis_off, T* kv,
                      float* hid, bool head_all, int32_t* tok, int per, int ostride,
                      float* logits, float* margin, int32_t* route_idx, float* route_gap,
-                     bool embedded) {
+                     bool embedded, float* layer_h) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int L = c.n_layers, E = c.n_routed, k = c.top_k, I = c.moe_inter, S = c.n_shared;
     const int SI = S * I;
@@ -452,6 +467,7 @@ struct Model {
                                          (uint16_t*)ws.xin);
         xg = (const uint16_t*)ws.xin;
       }
+      snap_h(layer_h, l, R);  // after the previous layer's slots were added
       attn_mfma(ws, B, C, w.attn_norm + (size_t)l * H, xg, pk.wqkv + l * pk.wqkv_s,
                 pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
 #define MTP_ROUTER(M)                                                                           \
@@ -495,7 +511,7 @@ struct Model {
         launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_split<kDownSplit>, dim3(H / 16, kDownSplit),
                  dim3(256), 0, s, R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh, edn,
                  pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.touched,
-                 ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h);
+                 ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h, ws.status);
       else {
 #define MTP_DSLOT(M)                                                                            \
   launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot<M>, dim3(H / 16, E + 1, cdiv(G, cpb)), dim3(256),  \
@@ -510,6 +526,7 @@ struct Model {
       norm_rows(R, ws.h, nullptr, w.final_norm, hid, xh);
     else
       k_combine_norm<<<R, H / 4, 0, s>>>(H, k, ws.slot, ws.h, w.final_norm, eps, hid, xh);
+    snap_h(layer_h, L, R);
     if (!tok) return;
     if (head_all) {
       lm_mfma(ws, R, logits, c.vocab, per, ostride, 0, tok, margin);
@@ -597,6 +614,7 @@ mtp_status pack_weights(mtp_ctx* ctx) {
     p.base = nullptr;
     return MTP_EHIP;
   }
+  ctx->pk_bytes = total * sizeof(uint4);
   uint4* cur = p.base;
   auto pack = [&](const void* src, size_t src_stride, int count, int N, int K,
                   const uint4** dst) {
@@ -656,7 +674,9 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   ctx->cfg = c;
   ctx->w = *w;
   ctx->rope = nullptr;
+  ctx->dstatus = nullptr;
   ctx->pk = Packed{};
+  ctx->pk_bytes = 0;
   {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -693,6 +713,11 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
     return MTP_EHIP;
   }
   delete[] host;
+  if (hipMalloc(&ctx->dstatus, 256) != hipSuccess ||
+      hipMemset(ctx->dstatus, 0, 256) != hipSuccess) {
+    mtp_destroy(ctx);
+    return MTP_EHIP;
+  }
   if (c.dtype == MTP_BF16) {
     mtp_status st = pack_weights(ctx);
     if (st != MTP_OK) {
@@ -717,8 +742,15 @@ void mtp_destroy(mtp_ctx* ctx) {
   if (!ctx) return;
   timing_release(ctx->tm);
   if (ctx->rope) (void)hipFree(ctx->rope);
+  if (ctx->dstatus) (void)hipFree(ctx->dstatus);
   if (ctx->pk.base) (void)hipFree(ctx->pk.base);
   delete ctx;
+}
+
+size_t mtp_context_bytes(const mtp_ctx* ctx) {
+  if (!ctx) return 0;
+  return (size_t)ctx->cfg.max_ctx * (ctx->cfg.head_dim / 2) * sizeof(float2) + 256 +
+         ctx->pk_bytes;
 }
 
 size_t mtp_workspace_bytes(const mtp_ctx* ctx, int32_t batch, int32_t rows) {
@@ -727,14 +759,20 @@ size_t mtp_workspace_bytes(const mtp_ctx* ctx, int32_t batch, int32_t rows) {
 }
 
 mtp_status mtp_status_read(const mtp_ctx* ctx, const void* ws, int32_t* status) {
-  if (!ctx || !ws || !status) return MTP_EINVAL;
-  if (hipMemcpy(status, ws, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess) return MTP_EHIP;
+  if (!ctx || !status) return MTP_EINVAL;
+  int32_t w = 0, c = 0;
+  if (ws && hipMemcpy(&w, ws, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+    return MTP_EHIP;
+  if (hipMemcpy(&c, ctx->dstatus, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+    return MTP_EHIP;
+  *status = w != 0 ? w : c;
   return MTP_OK;
 }
 
 mtp_status mtp_status_clear(const mtp_ctx* ctx, void* ws, void* stream) {
-  if (!ctx || !ws) return MTP_EINVAL;
-  k_fill_i32<<<1, 64, 0, (hipStream_t)stream>>>((int32_t*)ws, 1, 0);
+  if (!ctx) return MTP_EINVAL;
+  if (ws) k_fill_i32<<<1, 64, 0, (hipStream_t)stream>>>((int32_t*)ws, 1, 0);
+  k_fill_i32<<<1, 64, 0, (hipStream_t)stream>>>(ctx->dstatus, 1, 0);
   return launch_status();
 }
 
@@ -808,7 +846,8 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
 mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
                        const int32_t* next_tok, const int32_t* n_rows, const int32_t* row_pos,
                        void* draft_kv, int32_t* draft_len, int32_t* draft_tok,
-                       float* draft_logits, void* ws, size_t ws_bytes, void* stream) {
+                       float* draft_logits, float* draft_u, void* ws, size_t ws_bytes,
+                       void* stream) {
   if (!ctx) return MTP_EINVAL;
   const mtp_config& c = ctx->cfg;
   if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k) return MTP_EINVAL;
@@ -840,8 +879,16 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
                                                  w.row_pos, w.row_valid, w.head_row, w.row_tok,
                                                  draft_len, w.status, w.att_ctr, w.n_ctr);
     }
+    // depth d's output state u (ws.ustate, [B][H]) into draft_u[b][d-1]
+    auto keep_u = [&](int d) {
+      if (draft_u)
+        (void)hipMemcpy2DAsync(draft_u + (size_t)(d - 1) * H, (size_t)k * H * sizeof(float),
+                               w.ustate, (size_t)H * sizeof(float), (size_t)H * sizeof(float),
+                               batch, hipMemcpyDeviceToDevice, s);
+    };
     m.draft(w, batch, C, hid, (size_t)C * H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k, 0,
             draft_logits, (size_t)k * V, BF, BF && k > 1);
+    keep_u(1);
     const unsigned nbp = m.lm_partials(batch);
     // depth d = 2..k: one row at (row_pos + n_rows - 1) + (d - 1), state u
     // of depth d-1 (read by the draft input before the head rewrites it),
@@ -865,6 +912,7 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
       m.draft(w, batch, 1, w.ustate, (size_t)H, nullptr, 0, 0, (T*)draft_kv, true, draft_tok, k,
               d - 1, draft_logits ? draft_logits + (size_t)(d - 1) * V : nullptr, (size_t)k * V,
               BF, BF && d < k);
+      keep_u(d);
     }
     return launch_status();
   };
@@ -875,8 +923,8 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
 mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t* pending,
                            const int32_t* draft_tok, const int32_t* kv_len, void* kv_cache,
                            int32_t* verify_tok, float* hid, float* logits, float* margin,
-                           int32_t* route_idx, float* route_gap, void* ws, size_t ws_bytes,
-                           void* stream) {
+                           int32_t* route_idx, float* route_gap, float* layer_h, void* ws,
+                           size_t ws_bytes, void* stream) {
   if (!ctx) return MTP_EINVAL;
   const mtp_config& c = ctx->cfg;
   if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k || !pending ||
@@ -894,7 +942,7 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
                                         c.hidden, c.vocab, (const T*)ctx->w.embed, w.row_pos,
                                         w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
     m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
-               margin, route_idx, route_gap, /*embedded=*/true);
+               margin, route_idx, route_gap, /*embedded=*/true, layer_h);
     return launch_status();
   };
   if (c.dtype == MTP_BF16) return run(std::true_type{});
@@ -924,7 +972,7 @@ mtp_status kv_commit_rollback(mtp_ctx* ctx, int32_t batch, int32_t k, const int3
     return MTP_EINVAL;
   k_commit<<<cdiv(batch, 256), 256, 0, (hipStream_t)stream>>>(
       batch, k, accept_len, commit_tok, kv_len, n_rows, row_pos, pending, next_tok, max_new,
-      out_tok, max_out, n_out);
+      out_tok, max_out, n_out, ctx->dstatus);
   return launch_status();
 }
 

@@ -94,10 +94,17 @@ class Session:
             self.margin = torch.zeros((batch, k + 1), dtype=torch.float32, device=dev)
             self.route_idx = torch.zeros((c.n_layers, R, c.top_k), **i32)
             self.route_gap = torch.zeros((c.n_layers, R), dtype=torch.float32, device=dev)
+            self.layer_h = torch.zeros((c.n_layers + 1, R, c.hidden), dtype=torch.float32,
+                                       device=dev)
             self.draft_logits = torch.zeros((batch, max(k, 1), c.vocab), dtype=torch.float32,
                                             device=dev)
+            self.drafted_tok = z(batch, max(k, 1))   # drafts before a forced override
+            self.draft_u = torch.zeros((batch, max(k, 1), c.hidden), dtype=torch.float32,
+                                       device=dev)
         else:
             self.logits = self.margin = self.route_idx = self.route_gap = None
+            self.layer_h = None
+            self.draft_u = None
             self.draft_logits = None
         self.override = None
         self.graph = None
@@ -134,12 +141,21 @@ class Session:
         self.override = (table.to(self.m.device, torch.int32).contiguous(),
                          torch.zeros(1, dtype=torch.int32, device=self.m.device))
 
+    def update_forced_drafts(self, table: torch.Tensor):
+        """Rewrites the forced-draft table in place (same shape) and restarts
+        it at its first row, so a step captured in a graph picks it up."""
+        t, ctr = self.override
+        t.copy_(table.to(t.device, torch.int32))
+        ctr.zero_()
+
     def draft(self):
         _lib.mtp_draft_k(self.m.ctx, self.B, self.K, _p(self.hid), _p(self.next_tok),
                          _p(self.n_rows), _p(self.row_pos), _p(self.dkv), _p(self.draft_len),
-                         _p(self.draft_tok), _p(self.draft_logits), _p(self.ws), self.ws_bytes,
-                         self.stream)
+                         _p(self.draft_tok), _p(self.draft_logits), _p(self.draft_u),
+                         _p(self.ws), self.ws_bytes, self.stream)
         if self.override is not None and self.K > 0:
+            if self.record:
+                self.drafted_tok.copy_(self.draft_tok)
             table, ctr = self.override
             _lib.mtp_bench_override_drafts(self.B, self.K, _p(table), table.shape[0], _p(ctr),
                                            _p(self.draft_tok), self.stream)
@@ -148,8 +164,8 @@ class Session:
         _lib.moe_verify_step(self.m.ctx, self.B, self.K, _p(self.pending),
                              _p(self.draft_tok) if self.K > 0 else None, _p(self.kv_len),
                              _p(self.kv), _p(self.verify_tok), _p(self.hid), _p(self.logits),
-                             _p(self.margin), _p(self.route_idx), _p(self.route_gap), _p(self.ws),
-                             self.ws_bytes, self.stream)
+                             _p(self.margin), _p(self.route_idx), _p(self.route_gap),
+                             _p(self.layer_h), _p(self.ws), self.ws_bytes, self.stream)
 
     def accept(self):
         _lib.greedy_accept(self.B, self.K, _p(self.draft_tok) if self.K > 0 else None,

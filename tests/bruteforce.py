@@ -101,8 +101,9 @@ class Ref:
         act = self.inp(g / (1.0 + np.exp(-g)) * u)
         return _f32(self.mm(act, wd))
 
-    def moe_block(self, h, l):
-        """dense evaluation of all routed experts, masked by top-k."""
+    def moe_block(self, h, l, force=None):
+        """dense evaluation of all routed experts, masked by top-k.
+        force {row: expert ids}: that row's selection instead of its top-k."""
         c = self.cfg
         E, k, S, I = c.n_routed, c.top_k, c.n_shared, c.moe_inter
         y = self.inp(self.rms(h, self.W("ffn_norm", l)))
@@ -114,8 +115,8 @@ class Ref:
         sel = np.zeros((n, k), dtype=np.int64)
         for r in range(n):
             order = np.lexsort((np.arange(E), -lg[r]))    # logit desc, then id asc
-            sel[r] = order[:k]
-            mask[r, order[:k]] = 1.0
+            sel[r] = order[:k] if not force or r not in force else force[r]
+            mask[r, sel[r]] = 1.0
         out = np.zeros_like(h)
         shg, shd = self.W("sh_gu", l), self.W("sh_down", l)
         for s in range(S):
@@ -142,15 +143,17 @@ class Ref:
         W = self.W("embed") if self.cfg.tie_lm_head else self.W("lm_head")
         return _f32(self.mm(self.inp(x), W))
 
-    def verifier(self, tok, emb=None):
-        """rows 0..n-1 at positions 0..n-1: returns b, logits, routes."""
+    def verifier(self, tok, emb=None, force=None):
+        """rows 0..n-1 at positions 0..n-1: returns b, logits, routes.
+        force {(layer, row): expert ids} overrides those selections."""
         c = self.cfg
         h = self.embed_rows(tok, emb)
         pos = np.arange(len(tok))
         routes, router_logits = [], []
         for l in range(c.n_layers):
             h = self.attn_block(h, pos, self.W("attn_norm", l), self.W("wqkv", l), self.W("wo", l))
-            h, sel, lg = self.moe_block(h, l)
+            fl = {r: e for (ll, r), e in (force or {}).items() if ll == l}
+            h, sel, lg = self.moe_block(h, l, fl)
             routes.append(sel)
             router_logits.append(lg)
         b = self.rms(h, self.W("final_norm"))

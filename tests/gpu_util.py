@@ -10,6 +10,7 @@ import torch
 import oracle
 import synth
 from paper_2609_03181_amd.session import Model, Session
+from tests import tolerances
 
 
 def log(*a):
@@ -53,10 +54,12 @@ def gpu_prefill(model, B, K, tok, vis, max_out, record=True, prefill_rows=0):
 def oracle_prefill(orc, cfg, tok_b, vis_b, cap, max_new, routes=None):
     """The oracle's prefill of one sequence; routes [L][P][k] (the GPU's
     prefill routing, Session.prefill_routes[:, b]) are followed at the
-    oracle's near-ties, and any other difference fails."""
+    oracle's near-ties (per-layer tolerances of tests/tolerances.py), and
+    any other difference fails."""
     nv = int((tok_b < 0).sum())
     st = oracle.prefill(orc, cap, vis_b[:nv] if nv else None, tok_b[nv:], max_new=max_new,
-                        follow_route=routes)
+                        follow_route=routes,
+                        route_tol=tolerances.route_tol(cfg) if routes is not None else None)
     assert st.prefill_routes_rejected == 0, (
         f"{st.prefill_routes_rejected} prefill routings are not near-ties of the oracle's")
     return st
@@ -75,6 +78,10 @@ def step_records(s: Session):
     lg = s.logits.cpu().numpy() if s.logits is not None else None
     dl = s.draft_logits.cpu().numpy() if s.draft_logits is not None else None
     ri = s.route_idx.cpu().numpy() if s.route_idx is not None else None
+    rg = s.route_gap.cpu().numpy() if s.route_gap is not None else None
+    lh = s.layer_h.cpu().numpy() if s.layer_h is not None else None
+    du = s.draft_u.cpu().numpy() if s.draft_u is not None else None
+    dd = s.drafted_tok.cpu().numpy() if (s.record and s.override is not None) else None
     for b in range(B):
         rec = dict(drafts=d[b, :K].tolist(), verify=v[b].tolist(), m=int(m[b]),
                    commit=c[b].tolist(), hid=hid[b])
@@ -84,6 +91,14 @@ def step_records(s: Session):
             rec["draft_logits"] = dl[b, :K]
         if ri is not None:
             rec["routes"] = ri[:, b * (K + 1):(b + 1) * (K + 1)]
+        if rg is not None:
+            rec["route_gap"] = rg[:, b * (K + 1):(b + 1) * (K + 1)]
+        if lh is not None:
+            rec["layer_h"] = lh[:, b * (K + 1):(b + 1) * (K + 1)]
+        if du is not None and K > 0:
+            rec["draft_u"] = du[b, :K]
+        if dd is not None:
+            rec["draft_tokens_drafted"] = dd[b, :K].tolist()
         recs.append(rec)
     return recs
 
@@ -140,3 +155,41 @@ def oracle_synthetic_state(orc, cfg, b, ctx_b, cap, kv, dkv, hid, pend):
                            hid=np.ascontiguousarray(hid[b:b + 1], np.float32),
                            next_tok=np.array([p], np.int32), n_rows=1, row_pos=ctx_b - 1,
                            draft_len=ctx_b - 1, out=[p])
+
+
+def pre_state(s: Session, seqs):
+    """The step state of the sequences in seqs before a step (host copies),
+    for the layer-local check."""
+    torch.cuda.synchronize()
+    g = {k: getattr(s, k).cpu().numpy() for k in ("kv_len", "pending", "n_rows", "row_pos",
+                                                   "hid", "next_tok")}
+    return {b: dict(kv_len=int(g["kv_len"][b]), pending=int(g["pending"][b]),
+                    n_rows=int(g["n_rows"][b]), row_pos=int(g["row_pos"][b]),
+                    hid=g["hid"][b].copy(), next_tok=g["next_tok"][b].copy())
+            for b in seqs}
+
+
+def post_caches(s: Session, b, n_pos, cap):
+    """Sequence b's verifier and draft caches after a step, positions
+    0..n_pos-1, as float32 slabs of capacity cap (the oracle's layout)."""
+    L = s.m.cfg.n_layers
+    kv = s.kv[:, b, :, :, :n_pos].cpu().numpy()
+    dkv = s.dkv[b, :, :, :n_pos].cpu().numpy()
+    if s.m.bf16:
+        kv = synth.bf16_bits_to_f32(kv.view(np.uint16))
+        dkv = synth.bf16_bits_to_f32(dkv.view(np.uint16))
+    okv = np.zeros((L,) + kv.shape[1:3] + (cap, kv.shape[-1]), np.float32)
+    okv[..., :n_pos, :] = kv
+    odkv = np.zeros(dkv.shape[:2] + (cap, dkv.shape[-1]), np.float32)
+    odkv[..., :n_pos, :] = dkv
+    return okv, odkv
+
+
+def local_check(orc, s: Session, pre, recs, K, stats):
+    """Layer-local check (replay.local_step) of the step just run for the
+    sequences in pre."""
+    from tests import replay
+    for b, p in pre.items():
+        n_pos = p["kv_len"] + K + 1
+        kv, dkv = post_caches(s, b, n_pos, n_pos + K + 1)
+        replay.local_step(orc, p, recs[b], kv, dkv, K, stats)

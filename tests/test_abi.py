@@ -44,9 +44,13 @@ def test_host_validation_without_gpu():
         _lib.MTP_EUNSUPPORTED
     assert lib.mtp_create(None, None, None) == _lib.MTP_EINVAL
     assert lib.greedy_accept(0, 3, None, None, None, None, None) == _lib.MTP_EINVAL
-    assert lib.moe_verify_step(None, 1, 3, *([None] * 11), 0, None) == _lib.MTP_EINVAL
-    assert lib.mtp_draft_k(None, 1, 3, *([None] * 9), 0, None) == _lib.MTP_EINVAL
+    assert lib.moe_verify_step(None, 1, 3, *([None] * 12), 0, None) == _lib.MTP_EINVAL
+    assert lib.mtp_draft_k(None, 1, 3, *([None] * 10), 0, None) == _lib.MTP_EINVAL
     assert lib.mtp_workspace_bytes(None, 1, 4) == 0
+    assert lib.mtp_context_bytes(None) == 0
+    st = ctypes.c_int32(0)
+    assert lib.mtp_status_read(None, None, ctypes.byref(st)) == _lib.MTP_EINVAL
+    assert lib.kv_commit_rollback(None, 1, 3, *([None] * 9), 0, None, None) == _lib.MTP_EINVAL
 
 
 def _param_types(name):

@@ -1,7 +1,10 @@
 """GPU parity of the HIP decode path against the CPU oracle, through the
 C ABI.  Integers (tokens, routes, m, commit lists, lengths) must match
-exactly except at the oracle's own near-ties; floats to 1e-4 (fp32 model)
-or 2e-2 (bf16 model)."""
+exactly except at the oracle's own near-ties (per-layer routing
+tolerances and the token margin of tests/tolerances.py); floats to 1e-4
+(fp32 model) or 2e-2 (bf16 logits).  Every replay prints and bounds the
+fraction of decisions that fell in the near-tie band."""
+import copy
 import itertools
 
 import numpy as np
@@ -12,13 +15,12 @@ import oracle
 import synth
 from paper_2609_03181_amd import _lib
 from paper_2609_03181_amd.session import Session
-from tests import replay
-from tests.gpu_util import (build_pair, finished, gpu_prefill, log, oracle_prefill,
-                            prefix_inputs, step_records, to_dev_storage)
+from tests import replay, tolerances
+from tests.gpu_util import (build_pair, finished, gpu_prefill, local_check, log, oracle_prefill,
+                            pre_state, prefix_inputs, step_records, to_dev_storage)
 
 pytestmark = pytest.mark.gpu
 
-TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
 def _kv_close(s, st, b, n, tol):
@@ -37,7 +39,7 @@ def _kv_close(s, st, b, n, tol):
 
 def _run_and_replay(name, B, K, n_vis, n_txt, max_out, cap, wkw=None, check_kv=True):
     cfg, w, model, orc = build_pair(name, B, cap, max(K, 1), **(wkw or {}))
-    tol = TOL[cfg.dtype]
+    tol, stol = tolerances.logit_tol(cfg), tolerances.state_tol(cfg)
     tok, vis = prefix_inputs(cfg, B, n_vis, n_txt)
     log(f"[{name}] prefill B={B} P={n_vis + n_txt} K={K}")
     s = gpu_prefill(model, B, K, tok, vis, max_out)
@@ -53,17 +55,19 @@ def _run_and_replay(name, B, K, n_vis, n_txt, max_out, cap, wkw=None, check_kv=T
             sts[b].pending = t
             sts[b].next_tok[0] = t
             sts[b].out[0] = t
-        np.testing.assert_allclose(hid0[b, 0], sts[b].hid[0], rtol=tol, atol=tol)
+        np.testing.assert_allclose(hid0[b, 0], sts[b].hid[0], rtol=stol, atol=stol)
         if check_kv:
             _kv_close(s, sts[b], b, sts[b].kv_len, tol)
-    stats = replay.new_stats()
+    stats, lstats = replay.new_stats(), replay.new_stats()
     n_steps = 0
     while not finished(s):
+        active = [b for b in range(B) if not sts[b].finished]
+        pre = pre_state(s, active)
         s.step()
         recs = step_records(s)
-        for b in range(B):
-            if not sts[b].finished:
-                replay.replay_step(orc, sts[b], K, recs[b], stats, tol)
+        for b in active:
+            replay.replay_step(orc, sts[b], K, recs[b], stats, tol, state_tol=stol)
+        local_check(orc, s, pre, recs, K, lstats)
         n_steps += 1
         assert n_steps < 4 * max_out
     assert s.status() == 0
@@ -73,7 +77,8 @@ def _run_and_replay(name, B, K, n_vis, n_txt, max_out, cap, wkw=None, check_kv=T
         assert int(s.kv_len[b]) == sts[b].kv_len
         if check_kv:
             _kv_close(s, sts[b], b, sts[b].kv_len, tol)
-    log(f"[{name}] {n_steps} steps ok, followed near-ties: {stats}")
+    log(f"[{name}] {n_steps} steps ok; end-to-end near-tie band: {replay.assert_band(stats)}; "
+        f"layer-local: {replay.assert_local_band(lstats)}")
     return s, sts, stats
 
 
@@ -188,6 +193,69 @@ def test_forced_acceptance_reaches_every_m_and_is_lossless():
         assert outs[b] == traj[b][:N]
 
 
+def forced_replay(name, B, K, n_vis, n_txt, n_steps, cap, wkw, check_kv=True):
+    """Speculative steps whose drafts are replaced, step by step, from the
+    oracle's own greedy continuation of the replayed state: the first m*
+    drafts are the greedy tokens, the next is wrong, m* cycling over 0..K
+    (seed 13).  The GPU's drafting itself (before the replacement) is
+    compared with the oracle's draft chain, token and logits -- including
+    the depth-1 catch-up over the m+1 rows of the previous commit, whose
+    draft K/V is compared after every step."""
+    cfg, w, model, orc = build_pair(name, B, cap, K, **wkw)
+    tol, stol = tolerances.logit_tol(cfg), tolerances.state_tol(cfg)
+    tok, vis = prefix_inputs(cfg, B, n_vis, n_txt)
+    s = gpu_prefill(model, B, K, tok, vis, n_steps * (K + 1) + 4)
+    pr = s.prefill_routes.cpu().numpy()
+    sts = [oracle_prefill(orc, cfg, tok[b], vis[b], cap, 1 << 30, routes=pr[:, b])
+           for b in range(B)]
+    for b in range(B):
+        t = replay.check_token(sts[b].last_logits, sts[b].pending, int(s.pending[b]),
+                               "prefill token", replay.new_stats())
+        sts[b].pending = t
+        sts[b].next_tok[0] = t
+        sts[b].out[0] = t
+    ms = synth.uniform_int(13, 71, n_steps * B, 0, K + 1)
+    stats, lstats = replay.new_stats(), replay.new_stats()
+    seen = set()
+    for i in range(n_steps):
+        table = np.zeros((1, B, K), np.int32)
+        m_star = []
+        for b in range(B):
+            ahead = copy.deepcopy(sts[b])
+            ahead.max_new = 1 << 30
+            traj = oracle.ar_decode(orc, ahead, len(ahead.out) + K)[len(sts[b].out):]
+            m = int(ms[i * B + b])
+            d = list(traj[:K])
+            if m < K:
+                d[m] = (d[m] + 1) % cfg.vocab
+            table[0, b] = d
+            m_star.append(m)
+        s.set_forced_drafts(torch.from_numpy(table))
+        pre = pre_state(s, range(B))
+        s.step()
+        recs = step_records(s)
+        for b in range(B):
+            got = replay.replay_step(orc, sts[b], K, recs[b], stats, tol,
+                                     forced=table[0, b].tolist(), state_tol=stol)
+            seen.add(got)
+            if check_kv:
+                _kv_close(s, sts[b], b, sts[b].kv_len, tol)
+        local_check(orc, s, pre, recs, K, lstats)
+        log(f"  step {i}: m* {m_star}, m {[r['m'] for r in recs]}")
+    assert s.status() == 0
+    assert seen == set(range(K + 1)), seen
+    log(f"[{name} forced] {n_steps} steps, m seen {sorted(seen)}; end-to-end near-tie band: "
+        f"{replay.assert_band(stats)}; layer-local: {replay.assert_local_band(lstats)}")
+
+
+def test_mid_bf16_forced_acceptance_replayed_against_oracle():
+    forced_replay("mid", 2, 3, 12, 10, 10, 96, dict(gain_jitter=0.1, zipf_s=1.1))
+
+
+def test_tiny_forced_acceptance_replayed_against_oracle():
+    forced_replay("tinyu", 2, 3, 8, 8, 10, 96, dict(gain_jitter=0.1))
+
+
 def test_greedy_accept_exhaustive_on_gpu():
     V, K = 3, 3
     cases = [(d, v) for d in itertools.product(range(V), repeat=K)
@@ -246,6 +314,32 @@ def test_commit_rollback_bookkeeping_and_max_new_clamp():
         assert (g["out"][b, n_out[b] + take:] == -7).all()
 
 
+def test_commit_rejects_out_of_range_accept_len():
+    """An acceptance length outside [0, k] (acceptance equation: 0 <= m <=
+    k) sets the context's status word and leaves the sequence unchanged."""
+    cfg, w, model, orc = build_pair("tiny", 2, 64, 3)
+    B, K, max_out = 2, 3, 8
+    T = lambda a: torch.tensor(a, dtype=torch.int32, device="cuda")
+    m = T([K + 1, -1])
+    commit = T([[1, 2, 3, 4], [5, 6, 7, 8]])
+    kv_len, nr, rp = T([10, 12]), T([1, 1]), T([9, 11])
+    pend, nt = T([0, 0]), torch.zeros((B, K + 1), dtype=torch.int32, device="cuda")
+    out, no = torch.full((B, max_out), -7, dtype=torch.int32, device="cuda"), T([0, 0])
+    before = [t.clone() for t in (kv_len, nr, rp, pend, nt, out, no)]
+    stream = torch.cuda.current_stream().cuda_stream
+    _lib.kv_commit_rollback(model.ctx, B, K, m.data_ptr(), commit.data_ptr(), kv_len.data_ptr(),
+                            nr.data_ptr(), rp.data_ptr(), pend.data_ptr(), nt.data_ptr(), None,
+                            out.data_ptr(), max_out, no.data_ptr(), stream)
+    torch.cuda.synchronize()
+    assert _lib.mtp_status_read(model.ctx, None) == _lib.MTP_ERANGE
+    for a, b in zip(before, (kv_len, nr, rp, pend, nt, out, no)):
+        assert torch.equal(a, b)
+    _lib.mtp_status_clear(model.ctx, None, stream)
+    torch.cuda.synchronize()
+    assert _lib.mtp_status_read(model.ctx, None) == _lib.MTP_OK
+    assert _lib.mtp_context_bytes(model.ctx) >= 64 * (cfg.head_dim // 2) * 8
+
+
 def test_capacity_overflow_sets_sticky_status_without_writes():
     cfg, w, model, orc = build_pair("tiny", 1, 40, 3)
     tok, vis = prefix_inputs(cfg, 1, 4, 4)
@@ -277,18 +371,18 @@ def test_host_argument_errors():
     with pytest.raises(_lib.MtpError) as e:
         _lib.moe_verify_step(model.ctx, 3, 3, s.pending.data_ptr(), s.draft_tok.data_ptr(),
                              s.kv_len.data_ptr(), s.kv.data_ptr(), s.verify_tok.data_ptr(),
-                             s.hid.data_ptr(), None, None, None, None, s.ws.data_ptr(),
+                             s.hid.data_ptr(), None, None, None, None, None, s.ws.data_ptr(),
                              s.ws_bytes, 0)
     assert e.value.code == _lib.MTP_EINVAL
     with pytest.raises(_lib.MtpError):
         _lib.mtp_draft_k(model.ctx, 2, 4, s.hid.data_ptr(), s.next_tok.data_ptr(),
                          s.n_rows.data_ptr(), s.row_pos.data_ptr(), s.dkv.data_ptr(),
-                         s.draft_len.data_ptr(), s.draft_tok.data_ptr(), None, s.ws.data_ptr(),
+                         s.draft_len.data_ptr(), s.draft_tok.data_ptr(), None, None, s.ws.data_ptr(),
                          s.ws_bytes, 0)
     with pytest.raises(_lib.MtpError):           # workspace too small
         _lib.moe_verify_step(model.ctx, 2, 3, s.pending.data_ptr(), s.draft_tok.data_ptr(),
                              s.kv_len.data_ptr(), s.kv.data_ptr(), s.verify_tok.data_ptr(),
-                             s.hid.data_ptr(), None, None, None, None, s.ws.data_ptr(), 1024, 0)
+                             s.hid.data_ptr(), None, None, None, None, None, s.ws.data_ptr(), 1024, 0)
 
 
 def test_steps_after_prefill_do_not_depend_on_workspace_history():

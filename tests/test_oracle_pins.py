@@ -352,3 +352,35 @@ def test_bf16_models_store_bf16_kv_and_inputs():
         bits = np.ascontiguousarray(arr).view(np.uint32)
         assert np.all((bits & 0xFFFF) == 0)
         assert np.any(bits != 0)
+
+
+@pytest.mark.parametrize("name", ["tinyu", "tinyb"])
+def test_layer_by_layer_equals_whole_model_bitwise(name):
+    """verify_layer over every layer, then head, gives exactly what one
+    verify_rows call gives (the per-layer entry is the same computation cut
+    at the layer boundaries), for a prefix call and then single rows."""
+    cfg, w, orc = _model(name, gain_jitter=0.1)
+    vis, txt = _prefix(cfg, 5, 7)
+    P = 12
+    tok = np.concatenate([np.full(5, -1, np.int32), txt])
+    emb = np.zeros((P, cfg.hidden), cfg.wdtype)
+    emb[:5] = vis
+    kv_a, kv_b = orc.new_kv(32), orc.new_kv(32)
+    calls = [(tok, emb, np.arange(P))] + [([int(t)], None, [P + i])
+                                          for i, t in enumerate(synth.text_tokens(cfg, 3, seed=7))]
+    E = orc.w["embed"]
+    for t, e, pos in calls:
+        whole = orc.verify_rows(kv_a, t, pos, emb=e, want_logits=True, want_routes=True)
+        rows = [E[int(x)] if x >= 0 else e[r] for r, x in enumerate(t)]
+        h = np.stack(rows)
+        h = synth.bf16_bits_to_f32(h) if h.dtype == np.uint16 else h.astype(np.float32)
+        for l in range(cfg.n_layers):
+            r = orc.verify_layer(l, kv_b[l], h, pos)
+            assert np.array_equal(r["route_idx"], whole["route_idx"][l])
+            assert np.array_equal(r["route_gap"], whole["route_gap"][l])
+            h = r["h"]
+        hd = orc.head(h)
+        assert np.array_equal(hd["b"], whole["b"])
+        assert np.array_equal(hd["logits"], whole["logits"])
+        assert np.array_equal(hd["amax"], whole["amax"])
+        assert np.array_equal(kv_a, kv_b)

@@ -1,15 +1,13 @@
-"""Where the decision tolerances come from.
+"""Where the decision tolerances come from (tests/tolerances.py).
 
-The GPU path rounds at the same storage points as the oracle but sums its
-products in another order (float32 MFMA accumulation vs float64).  These
-tests measure how far a change of summation order alone moves the outputs
-the decisions are taken on, using the brute-force reference evaluated once
-with float64 and once with float32 matrix products, on the small bf16
-model with gain jitter and the Zipf router bias.  The tolerances must lie
-above that drift (with a factor of two: a gap is a difference of two
-logits) -- and, for bf16 models, the drift must actually exceed the
-float32-model route tolerance, else the looser bf16 tolerance is not
-needed.
+The drift table tests/golden/route_drift.json is written by
+tests/golden/make_route_drift.py: the oracle against its own
+float32-summation mode on the same inputs and routes.  These tests check
+that the tolerances are what that table derives (no looser, no tighter),
+that the table reproduces from the committed script, and -- as a second,
+independent measurement -- that the brute-force reference evaluated with
+float32 instead of float64 matrix products moves the outputs by amounts of
+the same order.
 """
 import dataclasses
 
@@ -18,11 +16,96 @@ import pytest
 
 import oracle
 import synth
+from tests import tolerances
 from tests.bruteforce import Ref
+from tests.golden import make_route_drift as mrd
+
+BF16_MODELS = [synth.TINYB, synth.MID, synth.FULL]
+
+
+@pytest.mark.parametrize("cfg", BF16_MODELS, ids=lambda c: c.name)
+def test_route_tolerance_is_twice_the_measured_drift(cfg):
+    """A router gap is a difference of two order statistics of the logits,
+    so it moves by at most twice the logit drift: tol = max(floor, 2 D),
+    and never more than max(floor, 4 D)."""
+    D = tolerances.router_drift(cfg)
+    tol = tolerances.route_tol(cfg)
+    assert tol.shape == (cfg.n_layers,)
+    assert np.all(tol >= 2 * D * (1 - 1e-6))
+    assert np.all(tol >= tolerances.ROUTE_FLOOR)
+    assert np.all(tol <= np.maximum(tolerances.ROUTE_FLOOR, 4 * D) * (1 + 1e-6))
+
+
+def test_float32_models_use_the_stated_gating_margin():
+    for cfg in (synth.TINY, synth.TINYU):
+        assert np.all(tolerances.route_tol(cfg) == np.float32(1e-3))
+        assert tolerances.logit_tol(cfg) == 1e-4
+
+
+@pytest.mark.parametrize("cfg", BF16_MODELS, ids=lambda c: c.name)
+def test_bf16_drift_exceeds_the_float32_margin(cfg):
+    """The looser bf16 tolerance is needed: summation order alone moves a
+    router gap past the 1e-3 gating margin somewhere in the model."""
+    assert 2 * tolerances.router_drift(cfg).max() > tolerances.ROUTE_FLOOR
+
+
+@pytest.mark.parametrize("cfg", BF16_MODELS, ids=lambda c: c.name)
+def test_comparison_tolerances_cover_the_drift(cfg):
+    e = [v for v in tolerances.drift_table().values() if v["config"] == cfg.name]
+    assert tolerances.logit_tol(cfg) >= 2 * max(v["logits"] for v in e) - 1e-9
+    assert tolerances.state_tol(cfg) >= 2 * max(v["state"] for v in e) - 1e-9
+    assert tolerances.logit_tol(cfg) >= tolerances.FLOAT_TOL["bf16"]
+
+
+def test_small_bf16_models_keep_the_stated_logit_tolerance():
+    """Where the drift allows, logits are compared at the 2e-2 the workload
+    statement fixes (final-norm states, which it does not mention, at
+    max(2e-2, twice their drift))."""
+    for cfg in (synth.TINYB, synth.MID):
+        assert tolerances.logit_tol(cfg) == 2e-2
+        assert tolerances.state_tol(cfg) <= 2.5e-2
+
+
+@pytest.mark.parametrize("key", ["tinyb", "mid"])
+def test_drift_table_reproduces(key):
+    """The stored drift of the small models is what the committed script
+    measures (the oracle is deterministic)."""
+    want = tolerances.drift_table()[key]
+    got = mrd.measure(key)
+    assert got["router"] == want["router"]
+    assert (got["logits"], got["state"]) == (want["logits"], want["state"])
+    assert got["local"] == want["local"]
+
+
+@pytest.mark.parametrize("cfg", BF16_MODELS, ids=lambda c: c.name)
+def test_layer_local_tolerances(cfg):
+    """Layer-local tolerances: twice the layer-local drift, floored at the
+    1e-3 gating margin (routing) and 1e-3 (floats); no looser than the
+    end-to-end ones, and the routing ones within the stated 1e-3 .. 1e-2."""
+    lt = tolerances.local_tol(cfg)
+    loc = [v["local"] for v in tolerances.drift_table().values() if v["config"] == cfg.name]
+    D = np.max([v["router"] for v in loc], axis=0)
+    assert np.allclose(lt["route"], np.maximum(1e-3, 2 * D), rtol=1e-6)
+    assert np.all(lt["route"] <= tolerances.route_tol(cfg) * (1 + 1e-6))
+    assert np.all(lt["route"] <= 1e-2)
+    assert lt["logits"] <= tolerances.FLOAT_TOL["bf16"]
+    assert np.all(lt["draft_logits"] >= 1e-3) and np.all(lt["draft_u"] >= 1e-3)
+    assert lt["kv_atol"] >= tolerances.KV_FLOOR
+
+
+@pytest.mark.slow
+def test_full_shape_drift_reproduces():
+    """One full-shape workload (12 layers; synthetic 2048-position contexts,
+    two verify passes of four rows) re-measured: the stored value."""
+    want = tolerances.drift_table()["full"]["workloads"][1]
+    got = mrd.measure("full", only=1)["workloads"][0]
+    assert got["recipe"] == want["recipe"]
+    assert got["router"] == want["router"]
+    assert (got["logits"], got["state"]) == (want["logits"], want["state"])
 
 
 @pytest.fixture(scope="module")
-def drift():
+def bruteforce_drift():
     cfg = dataclasses.replace(synth.MID, n_layers=2)
     w = synth.make_weights(cfg, 0, 1, gain_jitter=0.1, zipf_s=1.1)
     tok = synth.text_tokens(cfg, 32)
@@ -33,19 +116,10 @@ def drift():
                 logits=float(np.abs(la - lb).max()), b=float(np.abs(ba - bb).max()), cfg=cfg)
 
 
-def test_route_tolerance_covers_summation_order_drift(drift):
-    tol = oracle.route_tolerances(drift["cfg"])
-    assert np.all(2 * drift["router"] < tol), (drift["router"], tol)
-
-
-def test_bf16_route_drift_exceeds_float32_tolerance(drift):
-    assert drift["router"].max() > oracle.ROUTE_TOL, drift["router"]
-
-
-def test_argmax_tolerance_covers_summation_order_drift(drift):
-    assert 2 * drift["logits"] < oracle.ARGMAX_TOL, drift["logits"]
-
-
-def test_state_drift_within_bf16_comparison_tolerance(drift):
-    # the GPU parity tests compare bf16-model states and logits at 2e-2
-    assert drift["b"] < 2e-2 / 2, drift["b"]
+def test_bruteforce_float32_products_within_the_tolerances(bruteforce_drift):
+    """A second float32 evaluation (numpy BLAS products, routes left to
+    differ) stays inside the tolerances derived from the oracle's own."""
+    d = bruteforce_drift
+    assert np.all(2 * d["router"] <= tolerances.route_tol(d["cfg"])), d["router"]
+    assert 2 * d["logits"] < oracle.ARGMAX_TOL, d["logits"]
+    assert d["b"] < tolerances.state_tol(d["cfg"]) / 2, d["b"]
