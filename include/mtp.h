@@ -190,6 +190,25 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
                            int32_t* route_idx, float* route_gap, float* layer_h, void* ws,
                            size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, serving
+ * loops, harnesses that forbid hipMalloc): moe_verify_step with the same
+ * arguments, outputs and kernels, but no workspace -- its scratch is a
+ * static 16 MiB device array inside the library, one per device, looked up
+ * and zero-filled by the first mtp_create on that device.  The call
+ * allocates nothing.  Device conditions set the context's status word
+ * (mtp_status_read with ws = NULL).  A batch whose scratch
+ * (mtp_workspace_bytes(ctx, batch, k+1)) exceeds 16 MiB returns
+ * MTP_EUNSUPPORTED and enqueues nothing (at the full shape: up to 16 rows,
+ * batch x (k+1) <= 16, at any max_ctx).  Every call on a device shares that
+ * device's scratch: calls that overlap in time on one device race and must
+ * be ordered (one stream, or events); counters in it are left at zero by
+ * each call and the array keeps the last call's contents. */
+mtp_status moe_verify_step_static(mtp_ctx* ctx, int32_t batch, int32_t k,
+                                  const int32_t* pending, const int32_t* draft_tok,
+                                  const int32_t* kv_len, void* kv_cache, int32_t* verify_tok,
+                                  float* hid, float* logits, float* margin, int32_t* route_idx,
+                                  float* route_gap, float* layer_h, void* stream);
+
 /* Acceptance equation: accept_len[b] = m, the longest r <= k with
  * draft_tok[b][s] == verify_tok[b][s] for all s < r; commit_tok[b] =
  * [draft_tok[b][0..m-1], verify_tok[b][m]] followed by -1 padding to k+1. */

@@ -19,6 +19,7 @@ STATUS_NAMES = {0: "MTP_OK", -1: "MTP_EINVAL", -2: "MTP_ECAPACITY", -3: "MTP_EHI
 EXPORTS = ("mtp_create", "mtp_destroy", "mtp_context_bytes", "mtp_workspace_bytes",
            "mtp_status_read",
            "mtp_status_clear", "mtp_prefill", "mtp_draft_k", "moe_verify_step",
+           "moe_verify_step_static",
            "greedy_accept", "kv_commit_rollback", "mtp_bench_override_drafts",
            "mtp_timing_start", "mtp_timing_stop")
 
@@ -74,6 +75,7 @@ def load():
                          P], I32),
         "mtp_draft_k": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "moe_verify_step": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "moe_verify_step_static": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P], I32),
         "greedy_accept": ([I32, I32, P, P, P, P, P], I32),
         "kv_commit_rollback": ([P, I32, I32, P, P, P, P, P, P, P, P, P, I32, P, P], I32),
         "mtp_bench_override_drafts": ([I32, I32, P, I32, P, P, P], I32),
@@ -141,6 +143,13 @@ def moe_verify_step(ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_
     _check("moe_verify_step", load().moe_verify_step(
         ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_tok, hid, logits, margin,
         route_idx, route_gap, layer_h, ws, ws_bytes, stream))
+
+
+def moe_verify_step_static(ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_tok, hid,
+                           logits, margin, route_idx, route_gap, layer_h, stream):
+    _check("moe_verify_step_static", load().moe_verify_step_static(
+        ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_tok, hid, logits, margin,
+        route_idx, route_gap, layer_h, stream))
 
 
 def greedy_accept(batch, k, draft_tok, verify_tok, accept_len, commit_tok, stream):

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "common.h"
@@ -45,6 +46,7 @@ struct mtp_ctx {
   mtp_weights w;
   float2* rope;      // [max_ctx][head_dim/2] (cos, sin)
   int32_t* dstatus;  // status word of the calls without a workspace
+  void* scratch;     // device address of this device's static scratch
   Packed pk;         // bf16 models only
   size_t pk_bytes;   // bytes of the packed copy
   int n_split;   // attention key splits ...
@@ -66,7 +68,36 @@ inline void launch_k(Timing* tm, int kc, void (*k)(KA...), dim3 grid, dim3 block
   }
 }
 
+// Static scratch of moe_verify_step_static: the workspace of the callers
+// that cannot allocate.  Each device the library runs on holds its own
+// copy until the process ends.  Host code never passes the array's name to
+// a kernel (on the host it is a stand-in, not a device address): it uses
+// the per-device address hipGetSymbolAddress returns (scratch_addr).
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // per device: address of `scratch`, once zero-filled
+
+// Address of the current device's static scratch (looked up and
+// zero-filled on the first call for the device; the caller synchronises).
+mtp_status scratch_addr(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MTP_EHIP;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MTP_EHIP;
+    k_fill_i32<<<1024, 256>>>((int32_t*)p, (int)(kScratchBytes / 4), 0);
+    if (hipGetLastError() != hipSuccess || hipDeviceSynchronize() != hipSuccess) return MTP_EHIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return MTP_OK;
+}
 
 constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
 constexpr int kDownSplit = 8;  // blocks per output strip of the small-batch MoE down
@@ -675,6 +706,7 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   ctx->w = *w;
   ctx->rope = nullptr;
   ctx->dstatus = nullptr;
+  ctx->scratch = nullptr;
   ctx->pk = Packed{};
   ctx->pk_bytes = 0;
   {
@@ -714,7 +746,7 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
   }
   delete[] host;
   if (hipMalloc(&ctx->dstatus, 256) != hipSuccess ||
-      hipMemset(ctx->dstatus, 0, 256) != hipSuccess) {
+      hipMemset(ctx->dstatus, 0, 256) != hipSuccess || scratch_addr(&ctx->scratch) != MTP_OK) {
     mtp_destroy(ctx);
     return MTP_EHIP;
   }
@@ -938,6 +970,42 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
     Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
+    k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
+                                        c.hidden, c.vocab, (const T*)ctx->w.embed, w.row_pos,
+                                        w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
+    m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
+               margin, route_idx, route_gap, /*embedded=*/true, layer_h);
+    return launch_status();
+  };
+  if (c.dtype == MTP_BF16) return run(std::true_type{});
+  return run(std::false_type{});
+}
+
+mtp_status moe_verify_step_static(mtp_ctx* ctx, int32_t batch, int32_t k,
+                                  const int32_t* pending, const int32_t* draft_tok,
+                                  const int32_t* kv_len, void* kv_cache, int32_t* verify_tok,
+                                  float* hid, float* logits, float* margin, int32_t* route_idx,
+                                  float* route_gap, float* layer_h, void* stream) {
+  if (!ctx || !ctx->scratch) return MTP_EINVAL;
+  const mtp_config& c = ctx->cfg;
+  if (batch < 1 || batch > c.max_batch || k < 0 || k > c.max_k || !pending ||
+      (k > 0 && !draft_tok) || !kv_len || !kv_cache || !verify_tok || !hid)
+    return MTP_EINVAL;
+  if (carve(c, batch, k + 1, nullptr, ctx->n_split).bytes > kScratchBytes) {
+    fprintf(stderr,
+            "moe_verify_step_static: %d sequences x %d rows need %zu scratch bytes, more than "
+            "the %zu of the static scratch\n",
+            batch, k + 1, carve(c, batch, k + 1, nullptr, ctx->n_split).bytes, kScratchBytes);
+    return MTP_EUNSUPPORTED;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  auto run = [&](auto tag) -> mtp_status {
+    constexpr bool BF = decltype(tag)::value;
+    using T = typename St<BF>::T;
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
+    const int C = k + 1, R = batch * C;
+    Ws w = carve(c, batch, C, ctx->scratch, ctx->n_split);
+    w.status = ctx->dstatus;  // device conditions go to the context's status word
     k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
                                         c.hidden, c.vocab, (const T*)ctx->w.embed, w.row_pos,
                                         w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
