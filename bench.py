@@ -81,6 +81,8 @@ KERNEL_CLASSES = {  # timing-hook class -> kernel name as the profiler lists it
     5: ("RMSNorm + QKV + RoPE + KV append", "mtp::k_s_qkv"),
     6: ("RMSNorm + router + top-k", "mtp::k_s_router"),
     7: ("draft FFN gate/up + SwiGLU", "mtp::k_s_gu<1,"),
+    8: ("verify MoE sub-layer in one launch (RMSNorm + router + top-k, gate/up + SwiGLU, "
+        "down; up to 16 rows)", "mtp::k_s_moe"),
 }
 
 
@@ -124,6 +126,9 @@ def class_cost(cfg, B, K, kv_len, draft_len, routes, kc):
         return L * (E * H * es + R * H * (4 + es)), L * R * E * H * 2, L
     if kc == 7:
         return K * 2 * F * H * es, K * B * (K + 1) * 2 * F * H * 2, K
+    if kc == 8:   # the three steps of classes 6, 2 and 3 in one launch per layer
+        parts = [class_cost(cfg, B, K, kv_len, draft_len, routes, c) for c in (6, 2, 3)]
+        return sum(p[0] for p in parts), sum(p[1] for p in parts), L
     raise ValueError(kc)
 
 

@@ -56,9 +56,12 @@ typedef enum {
   MTP_EHIP = -3,         /* a HIP call failed */
   MTP_EUNSUPPORTED = -4, /* shape outside what the kernels support */
   MTP_ETOKEN = -5,       /* device: a token id outside [0, vocab) */
-  MTP_ERANGE = -6        /* device: a value outside its range (an acceptance length
+  MTP_ERANGE = -6,       /* device: a value outside its range (an acceptance length
                             outside [0, k]; a MoE contribution past the fixed-point
                             range of the small-batch down projection) */
+  MTP_ESTALL = -7        /* device: a bounded wait between the blocks of a persistent
+                            kernel expired (an internal error: the call's outputs are
+                            invalid) */
 } mtp_status;
 
 enum { MTP_F32 = 0, MTP_BF16 = 1 };
@@ -257,7 +260,9 @@ typedef enum {
   MTP_KC_LM_HEAD = 4,    /* LM head partial argmax (verifier and draft) */
   MTP_KC_QKV = 5,        /* fused RMSNorm + QKV + RoPE + K/V append */
   MTP_KC_ROUTER = 6,     /* fused RMSNorm + router + top-k */
-  MTP_KC_DRAFT_FFN = 7   /* draft block FFN gate/up + SwiGLU */
+  MTP_KC_DRAFT_FFN = 7,  /* draft block FFN gate/up + SwiGLU */
+  MTP_KC_MOE = 8         /* verifier MoE sub-layer of up to 16 rows in one launch
+                            (RMSNorm + router + top-k, gate/up + SwiGLU, down) */
 } mtp_kernel_class;
 mtp_status mtp_timing_start(mtp_ctx* ctx, int32_t kernel_class, int32_t max_launches);
 mtp_status mtp_timing_stop(mtp_ctx* ctx, float* total_ms /* (host) */,

@@ -10,10 +10,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmtp.so")
 
 (MTP_OK, MTP_EINVAL, MTP_ECAPACITY, MTP_EHIP, MTP_EUNSUPPORTED, MTP_ETOKEN,
- MTP_ERANGE) = 0, -1, -2, -3, -4, -5, -6
+ MTP_ERANGE, MTP_ESTALL) = 0, -1, -2, -3, -4, -5, -6, -7
 MTP_F32, MTP_BF16 = 0, 1
 STATUS_NAMES = {0: "MTP_OK", -1: "MTP_EINVAL", -2: "MTP_ECAPACITY", -3: "MTP_EHIP",
-                -4: "MTP_EUNSUPPORTED", -5: "MTP_ETOKEN", -6: "MTP_ERANGE"}
+                -4: "MTP_EUNSUPPORTED", -5: "MTP_ETOKEN", -6: "MTP_ERANGE",
+                -7: "MTP_ESTALL"}
 
 # every symbol include/mtp.h declares
 EXPORTS = ("mtp_create", "mtp_destroy", "mtp_context_bytes", "mtp_workspace_bytes",
@@ -24,7 +25,7 @@ EXPORTS = ("mtp_create", "mtp_destroy", "mtp_context_bytes", "mtp_workspace_byte
            "mtp_timing_start", "mtp_timing_stop")
 
 # kernel classes of the timing hook (mtp_kernel_class)
-KC_ATTN, KC_MOE_GU, KC_MOE_DOWN, KC_LM_HEAD, KC_QKV, KC_ROUTER, KC_DRAFT_FFN = range(1, 8)
+KC_ATTN, KC_MOE_GU, KC_MOE_DOWN, KC_LM_HEAD, KC_QKV, KC_ROUTER, KC_DRAFT_FFN, KC_MOE = range(1, 9)
 
 
 class MtpError(RuntimeError):

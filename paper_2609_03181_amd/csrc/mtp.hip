@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -14,6 +15,7 @@
 #include "kernels_rows.h"
 #include "kernels_mfma.h"
 #include "kernels_small.h"
+#include "kernels_fused.h"
 #include "kernels_spec.h"
 
 // 16-entry chunks a routed MoE block takes when a pass has 8 or more row
@@ -52,6 +54,7 @@ struct mtp_ctx {
   int n_split;   // attention key splits ...
   int spl;       // ... of spl positions each (multiple of 64)
   int n_cu;      // compute units of the device the context was created on
+  int moe_blocks;  // resident blocks of the fused small-batch MoE (0: three launches)
   Timing tm;
 };
 
@@ -101,6 +104,28 @@ mtp_status scratch_addr(void** out) {
 
 constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
 constexpr int kDownSplit = 8;  // blocks per output strip of the small-batch MoE down
+constexpr int kMoeSpinMax = 1 << 20;  // polls of a fused-MoE wait before it gives up
+
+// Blocks of the fused small-batch MoE that the device holds at once (its
+// waits need every block resident), or 0 when the shape is outside what it
+// covers or MTP_FUSED_MOE=0 selects the three-launch form.
+int moe_resident_blocks(const mtp_config& c, int n_cu) {
+  const int H = c.hidden;
+  if (c.dtype != MTP_BF16 || c.moe_inter > H ||
+      moe_normed(c.n_routed, c.n_shared, H) + kMoeMaxBlocks > kMoeSyncWords)
+    return 0;
+  const char* env = getenv("MTP_FUSED_MOE");
+  if (env && env[0] == '0') return 0;
+  int occ = 0;
+  hipError_t e = hipErrorInvalidValue;
+  const size_t lds = (size_t)SR_MAX * (H + XPAD) * 2;
+#define MTP_OCC(M) \
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k_s_moe<M>, 256, lds)
+  MTP_MAXT_DISPATCH(H / 128, MTP_OCC);
+#undef MTP_OCC
+  if (e != hipSuccess || occ < 1) return 0;
+  return occ * n_cu < kMoeMaxBlocks ? occ * n_cu : kMoeMaxBlocks;
+}
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -117,6 +142,8 @@ struct Ws {
   int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr, *dn_ctr;
   int32_t* cbp;  // chunk-block prefix of the compact MoE grids [E + 2]
   unsigned long long* dn_part;  // MoE down split partials [kDownSplit][R][H], fixed point (R <= 16)
+  float* lg;                    // router logits of the fused MoE [R][E] (R <= 16)
+  int32_t* moe_sync;            // fused MoE: kMoeSyncWords per layer (inside the zeroed counters)
   uint16_t* act_sh;
   int n_ctr;  // entries of att_ctr (zeroed at the start of each call)
   size_t bytes;
@@ -164,7 +191,17 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
   size_t act_cols = (size_t)(k + 1) * SI;
   if ((size_t)c.draft_inter > act_cols) act_cols = c.draft_inter;
   if (c.dtype == MTP_BF16) act_cols = (size_t)k * c.moe_inter;  // routed entries only
-  w.act = take(R * act_cols * es);
+  size_t act_bytes = R * act_cols * es;
+  // The fused small-batch MoE runs on any pass of up to 16 rows -- also the
+  // last, shorter chunk of a prefill carved for longer chunks -- so every
+  // bf16 carve holds its buffers, sized for min(R, 16) rows.
+  const bool fused_rows = c.dtype == MTP_BF16;
+  const int R16 = R < SR_MAX ? (int)R : SR_MAX;
+  if (fused_rows) {  // tile-major gate/up outputs of the fused MoE
+    const size_t fb = (size_t)(c.moe_inter / 16) * moe_entry_cap(R16, k, c.n_routed) * 16 * 2;
+    if (fb > act_bytes) act_bytes = fb;
+  }
+  w.act = take(act_bytes);
   w.xhead = take(R * H * es);
   if (c.dtype == MTP_BF16) {
     w.part = (float*)take(R * c.n_heads * (size_t)n_split * (c.head_dim + 2) * 4);
@@ -178,17 +215,27 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.n_touched = (int32_t*)take(4);
     w.cbp = (int32_t*)take(((size_t)c.n_routed + 2) * 4);
     // attention split counters then MoE-down strip counters, one region
-    w.att_ctr = (int32_t*)take((R * c.n_heads + (size_t)H / 16) * 4);
+    const size_t n_sync = fused_rows ? (size_t)c.n_layers * kMoeSyncWords : 0;
+    w.att_ctr = (int32_t*)take((R * c.n_heads + (size_t)H / 16 + n_sync) * 4);
     w.dn_ctr = w.att_ctr + R * c.n_heads;
-    w.n_ctr = (int)(R * c.n_heads + H / 16);
-    w.dn_part = (unsigned long long*)take((size_t)kDownSplit * (R < 16 ? R : 16) * H * 8);
+    w.moe_sync = fused_rows ? w.dn_ctr + H / 16 : nullptr;
+    w.n_ctr = (int)(R * c.n_heads + H / 16 + n_sync);
+    size_t part_rows = (size_t)kDownSplit * R16;
+    if (moe_part_rows(R16, k, c.n_routed, c.n_shared) > part_rows)
+      part_rows = moe_part_rows(R16, k, c.n_routed, c.n_shared);
+    w.dn_part = (unsigned long long*)take(part_rows * H * 8);
     const size_t shw = (size_t)(SI > c.draft_inter ? SI : c.draft_inter);
-    w.act_sh = (uint16_t*)take(R * shw * 2);
+    size_t sh_bytes = R * shw * 2;
+    if (fused_rows && (size_t)SI * 16 * 2 > sh_bytes) sh_bytes = (size_t)SI * 16 * 2;
+    w.act_sh = (uint16_t*)take(sh_bytes);
+    w.lg = (float*)take((size_t)R16 * c.n_routed * 4);
   } else {
     w.part = w.slot = w.ent_w = nullptr;
     w.cnt = w.off = w.ent_row = w.ent_slot = w.touched = w.n_touched = w.att_ctr = nullptr;
     w.cbp = nullptr;
     w.act_sh = nullptr;
+    w.lg = nullptr;
+    w.moe_sync = nullptr;
   }
   w.bytes = off;
   return w;
@@ -208,6 +255,7 @@ struct Model {
   int spl;
   Timing* tm;
   int n_cu;              // compute units of the device (persistent grids)
+  int moe_blocks = 0;    // fused small-batch MoE: grid that is resident at once (0: off)
   bool prefill = false;  // prefill calls launch the prefill-tagged kernel instances
 
   const T* wp(const void* p, size_t off_elems) const { return (const T*)p + off_elems; }
@@ -501,6 +549,24 @@ struct Model {
       snap_h(layer_h, l, R);  // after the previous layer's slots were added
       attn_mfma(ws, B, C, w.attn_norm + (size_t)l * H, xg, pk.wqkv + l * pk.wqkv_s,
                 pk.wo + l * pk.wo_s, (uint16_t*)kv + (size_t)l * layer_stride, seq_stride);
+      if (small && moe_blocks > 0 && ws.moe_sync && ws.lg) {  // router, gate/up, down: one launch
+        const unsigned items = (unsigned)((E + 15) / 16 + SI / 16 + E * (I / 16) +
+                                          (E + S) * ((H / 16 + 3) / 4));
+        const unsigned grid = (unsigned)moe_blocks < items ? (unsigned)moe_blocks : items;
+#define MTP_MOE(M)                                                                              \
+  launch_k(tm, MTP_KC_MOE, k_s_moe<M>, dim3(grid), dim3(256), lds_rows(R, H), s, R,  \
+           H, E, k, I, S, ws.h, w.ffn_norm + (size_t)l * H, eps, pk.router + l * pk.router_s,    \
+           w.router_bias ? w.router_bias + (size_t)l * E : nullptr,                              \
+           pk.exp_gu + (size_t)l * E * pk.exp_gu_s, pk.exp_gu_s, pk.sh_gu + l * pk.sh_gu_s,      \
+           pk.exp_down + (size_t)l * E * pk.exp_down_s, pk.exp_down_s,                           \
+           pk.sh_down + l * pk.sh_down_s, ws.lg, (uint16_t*)ws.act, ws.act_sh, ws.dn_part,       \
+           ws.moe_sync + (size_t)l * kMoeSyncWords,                                              \
+           route_idx ? route_idx + (size_t)l * R * k : nullptr,                                  \
+           route_gap ? route_gap + (size_t)l * R : ws.rgap, ws.status, kMoeSpinMax)
+        MTP_MAXT_DISPATCH(H / 128, MTP_MOE);
+#undef MTP_MOE
+        continue;
+      }
 #define MTP_ROUTER(M)                                                                           \
   launch_k(tm, MTP_KC_ROUTER, k_s_router<M>, dim3(G), dim3(1024), lds_rows(R, H), s, R, H, E, k, \
            ws.h, w.ffn_norm + (size_t)l * H, eps, (uint16_t*)ws.xin, pk.router + l * pk.router_s, \
@@ -750,12 +816,14 @@ mtp_status mtp_create(const mtp_config* cfg, const mtp_weights* w, mtp_ctx** out
     mtp_destroy(ctx);
     return MTP_EHIP;
   }
+  ctx->moe_blocks = 0;
   if (c.dtype == MTP_BF16) {
     mtp_status st = pack_weights(ctx);
     if (st != MTP_OK) {
       mtp_destroy(ctx);
       return st;
     }
+    ctx->moe_blocks = moe_resident_blocks(c, ctx->n_cu);
   }
   *out = ctx;
   return MTP_OK;
@@ -833,7 +901,7 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu, ctx->moe_blocks};
     m.prefill = true;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     for (int c0 = 0; c0 < n_rows; c0 += C) {
@@ -891,7 +959,7 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu, ctx->moe_blocks};
     const int C = k + 1, R = batch * C, H = c.hidden, V = c.vocab;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     const float eps = (float)c.rms_eps;
@@ -967,7 +1035,7 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu, ctx->moe_blocks};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
@@ -1002,7 +1070,7 @@ mtp_status moe_verify_step_static(mtp_ctx* ctx, int32_t batch, int32_t k,
   auto run = [&](auto tag) -> mtp_status {
     constexpr bool BF = decltype(tag)::value;
     using T = typename St<BF>::T;
-    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu};
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu, ctx->moe_blocks};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ctx->scratch, ctx->n_split);
     w.status = ctx->dstatus;  // device conditions go to the context's status word
@@ -1053,7 +1121,7 @@ mtp_status mtp_bench_override_drafts(int32_t batch, int32_t k, const int32_t* ta
 }
 
 mtp_status mtp_timing_start(mtp_ctx* ctx, int32_t kernel_class, int32_t max_launches) {
-  if (!ctx || kernel_class < MTP_KC_ATTN || kernel_class > MTP_KC_DRAFT_FFN || max_launches < 1 ||
+  if (!ctx || kernel_class < MTP_KC_ATTN || kernel_class > MTP_KC_MOE || max_launches < 1 ||
       ctx->tm.kclass != 0)
     return MTP_EINVAL;
   Timing t;
