@@ -49,6 +49,10 @@ WORKLOADS = {
     # tiny fp32 case
     "tiny": dict(model="tiny", B=1, K=3, n_vis=64, n_txt=16, synthetic=False, forced=False,
                  zipf=0.0),
+    # Gundam-mode page: the largest visual prefix (256 + 100 n, n = 9: 1156
+    # rows) + 512 prompt tokens prefilled in one pass, then batch-1 steps
+    "gundam": dict(model="full", B=1, K=3, n_vis=1156, n_txt=512, synthetic=False, forced=False,
+                   zipf=0.0),
     # page loop: 32 pages (256 vision rows + 32 prompt tokens), 2048 new
     # tokens each; timed: prefill + graph-replayed steps until every page is done
     "pages": dict(model="full", B=32, K=3, n_vis=256, n_txt=32, synthetic=False, forced=False,
@@ -463,14 +467,115 @@ def _setup(name, args, steps_needed):
         vv = torch.from_numpy(vis.view(np.int16) if cfg.dtype == "bf16" else vis)
         pin = (torch.from_numpy(tok), vv)
         torch.cuda.synchronize()
-        tp = time.perf_counter()
-        s.prefill(*pin)
+        s.prefill(*pin)   # first call: kernel code objects load
         torch.cuda.synchronize()
-        log(f"[{name}] prefill {B}x{P} rows in one pass: {1e3 * (time.perf_counter() - tp):.1f} ms")
+        s.prefill_ms = _time_prefill(s, pin) if not pages else None
+        log(f"[{name}] prefill {B}x{P} rows in one pass: {s.prefill_ms} ms")
     if wl["forced"]:
         s.set_forced_drafts(torch.from_numpy(_forced_table(s, cfg, B, K, steps_needed)))
     assert s.status() == 0
     return wl, cfg, w, model, s, ctx, pin
+
+
+def _time_prefill(s, pin, n=3):
+    """Milliseconds of one prefill pass (event-timed on the session's
+    stream; the prefill is repeated over the same rows, which rewrites the
+    same caches and step state)."""
+    import torch
+    st = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(st)
+    for _ in range(n):
+        s.prefill(*pin)
+    b.record(st)
+    b.synchronize()
+    return round(a.elapsed_time(b) / n, 3)
+
+
+def prefill_flops(cfg, P):
+    """Algorithmic FLOPs of a one-pass prefill of P rows: every row through
+    the verifier's active parameters (no LM head but the last row's) and
+    causal attention over the rows before it, plus the draft-block prefill
+    of P - 1 rows (embedding/state projection, attention, dense FFN)."""
+    H, D, I, S, E, k = (cfg.hidden, cfg.n_heads * cfg.head_dim, cfg.moe_inter, cfg.n_shared,
+                        cfg.n_routed, cfg.top_k)
+    L, V, F = cfg.n_layers, cfg.vocab, cfg.draft_inter
+    per_row = L * (3 * D * H + H * D + E * H + (k + S) * 3 * I * H)
+    attn = L * P * (P + 1) // 2 * 2 * D
+    draft_row = 2 * H * H + 3 * D * H + H * D + 3 * F * H
+    draft_attn = (P - 1) * P // 2 * 2 * D
+    return 2 * (P * per_row + V * H + (P - 1) * draft_row) + 2 * (attn + draft_attn)
+
+
+def objective_flops(cfg, T, K):
+    """Algorithmic FLOPs of the objective forward of T rows and K depths:
+    per depth the draft block over T-1 rows (causal attention among them)
+    and the LM head of every row, plus the LM head of the verifier states
+    b_{p+1} once."""
+    H, D, V, F = cfg.hidden, cfg.n_heads * cfg.head_dim, cfg.vocab, cfg.draft_inter
+    n = T - 1
+    draft = n * (2 * H * H + 3 * D * H + H * D + 3 * F * H) + n * (n + 1) // 2 * 2 * D
+    return 2 * (K * (draft + n * V * H) + n * V * H)
+
+
+def run_objective(args):
+    """FastMTP draft-head objective forward at the full shape: one sequence
+    of 256 vision + 512 prompt + 512 response rows (loss rows: the
+    response), K = 3 depths; synthetic verifier states b ~ N(0, 1)."""
+    import torch
+    import synth
+    from paper_2609_03181_amd import _lib
+    from paper_2609_03181_amd.session import Model
+    cfg = synth.FULL
+    n_vis, n_prompt_txt, n_resp, K = 256, 512, 512, 3
+    T, n_prompt = n_vis + n_prompt_txt + n_resp, n_vis + n_prompt_txt
+    w = synth.make_weights(cfg, 0, 1)
+    model = Model(cfg, w, 1, T + 8, 3)
+    tok = np.concatenate([np.full(n_vis, -1, np.int32),
+                          synth.text_tokens(cfg, n_prompt_txt + n_resp, seed=11)])
+    vis = np.zeros((T, cfg.hidden), cfg.wdtype)
+    vis[:n_vis] = synth.vision_prefix(cfg, n_vis, seed=10)
+    b = np.random.default_rng(17).standard_normal((T, cfg.hidden)).astype(np.float32)
+    dev = "cuda"
+    tok_d = torch.from_numpy(tok).to(dev)
+    vis_d = torch.from_numpy(vis.view(np.int16)).to(dev)
+    b_d = torch.from_numpy(b).to(dev)
+    wsb = _lib.mtp_objective_workspace_bytes(model.ctx, T)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=dev)
+    dkv = torch.zeros((K, 2, cfg.n_heads, model.max_ctx, cfg.head_dim), dtype=torch.int16,
+                      device=dev)
+    loss = torch.zeros(3 * K + 1, dtype=torch.float64, device=dev)
+    st = torch.cuda.current_stream()
+
+    def call():
+        _lib.mtp_objective(model.ctx, T, n_prompt, K, tok_d.data_ptr(), vis_d.data_ptr(),
+                           b_d.data_ptr(), dkv.data_ptr(), None, None, loss.data_ptr(),
+                           ws.data_ptr(), wsb, st.cuda_stream)
+    call()
+    torch.cuda.synchronize()
+    n = 5
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(n):
+        call()
+    e1.record(st)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / n
+    assert _lib.mtp_status_read(model.ctx, ws.data_ptr()) == 0
+    fl = objective_flops(cfg, T, K)
+    tf = fl / (ms * 1e-3) / 1e12
+    model.close()
+    return {"value": round(K * (T - 1) / (ms * 1e-3), 1), "unit": "training-grid rows/s",
+            "ms_per_sequence": round(ms, 3),
+            "config": {"workload": "FastMTP objective forward (L_CE, L_KL, L_MSE over the "
+                                   "position x depth grid), full shape, one sequence of 256 "
+                                   "vision + 512 prompt + 512 response rows, K=3",
+                       "rows": T, "loss_rows": n_resp - 2, "k": K},
+            "loss": [round(float(x), 6) for x in loss.cpu().numpy()],
+            "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(tf / MFMA_PEAK_TFLOPS, 4),
+                         "traffic": None, "kernel": "mtp_objective (whole call)",
+                         "flops_per_call": int(fl), "us_per_call": round(1e3 * ms, 1)}}
 
 
 def probe_verify(name, args):
@@ -687,6 +792,12 @@ def run_workload(name, args, cpu=False):
         rec["config"]["pages_per_s"] = round(B / dt, 4)
         rec["config"]["new_tokens_per_page"] = wl["new"]
         rec["config"]["job_s"] = round(dt, 3)
+    pms = getattr(s, "prefill_ms", None)
+    if pms:  # the one-pass prefill of the prompt (the step before the hot path)
+        P = wl["n_vis"] + wl["n_txt"]
+        pf = prefill_flops(cfg, P) * B
+        rec["prefill"] = {"rows": P * B, "ms": pms, "TFLOP_s": round(pf / (pms * 1e-3) / 1e12, 1),
+                          "frac_of_mfma_peak": round(pf / (pms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4)}
     if cpu and not pages:
         ctx_cpu = int(min(int(ctx[0]), 768))
         rec["cpu_baseline"] = cpu_baseline(cfg, w, K, ctx_cpu)
@@ -712,9 +823,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default=None, choices=sorted(WORKLOADS) + ["ksweep"],
-                    help="one workload only (default: batch 1 headline with the batch-16 "
-                         "and batch-64 workloads as sub-records)")
+    ap.add_argument("--workload", default=None, choices=sorted(WORKLOADS) + ["ksweep", "objective"],
+                    help="one workload only (default: batch 1 headline with the batch-16, "
+                         "batch-64, Gundam and objective workloads as sub-records)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches, not a HIP graph")
     ap.add_argument("--probe", choices=["verify"],
@@ -756,6 +867,9 @@ def main():
     if args.workload == "ksweep":
         ksweep(args)
         return
+    if args.workload == "objective":
+        print(json.dumps(run_objective(args)), flush=True)
+        return
     if args.probe:
         probe_verify(args.workload or "b1", args)
         return
@@ -765,11 +879,12 @@ def main():
         return
     out = run_workload("b1", args, cpu=not args.no_cpu_baseline)
     out["sub_records"] = {}
-    for name in ("b16", "b64"):
+    for name in ("b16", "b64", "gundam"):
         r = run_workload(name, args)
         keep = ("value", "unit", "ms_per_step", "config", "roofline", "roofline_dominant_kernel",
-                "verify_pass", "grouped_gemm", "breakdown_ms", "kernels")
+                "verify_pass", "grouped_gemm", "breakdown_ms", "prefill", "kernels")
         out["sub_records"][name] = {k: r[k] for k in keep if k in r}
+    out["sub_records"]["objective"] = run_objective(args)
     print(json.dumps(out), flush=True)
 
 
@@ -781,6 +896,9 @@ def _wl_name(name, wl):
         return "full shape, batch 16, cached ctx U{1024..2048}, forced acceptance 0.2/0.2/0.25/0.35"
     if name == "b64":
         return "full shape, batch 64, cached ctx U{512..4096}, Zipf(1.1) router bias"
+    if name == "gundam":
+        return ("full shape, batch 1, Gundam-mode page: 1156 vision rows (256 + 100 x 9) + 512 "
+                "prompt rows prefilled in one pass, K=3")
     if name == "pages":
         return ("full shape, page loop: 32 pages x (256 vision rows + 32 prompt tokens), "
                 "2048 new tokens per page, K=3; timed = prefill + steps until all pages finish")

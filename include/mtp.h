@@ -212,6 +212,36 @@ mtp_status moe_verify_step_static(mtp_ctx* ctx, int32_t batch, int32_t k,
                                   float* hid, float* logits, float* margin, int32_t* route_idx,
                                   float* route_gap, float* layer_h, void* stream);
 
+/* FastMTP draft-head objective, forward only (Section "Draft-head
+ * objective", Eq. draft-loss and Eq. objective, over the training grid of
+ * Section "Draft-head architecture").  One sequence of n_rows rows: row p
+ * is the token tok[p], or when tok[p] < 0 the vision row vision[p]
+ * ([n_rows][H] storage dtype; NULL when every tok >= 0); b_states
+ * [n_rows][H] f32 are the verifier's post-norm states b_p (detached inputs,
+ * e.g. from a verifier pass over the rows).  For each depth d = 1..k the
+ * draft block runs over rows p = 0..n_rows-2 (next input row p+1,
+ * position p, causal attention among the rows of that depth in its own
+ * draft cache: draft_kv is [k][2][nh][max_ctx][dh], overwritten) with state
+ * b_p at depth 1 and on prompt rows p < n_prompt, else u_{p-1}^(d-1).
+ * Loss rows are p = n_prompt..n_rows-3 (response rows with a target
+ * x_{p+2}; every target must be a token).  Outputs (device):
+ *   loss [3k+1] f64: the means over the loss rows of CE_d, KL_d(Q||P),
+ *     MSE_d for d = 1..k, then L = sum_d alpha_d (0.85 CE_d + 0.45 KL_d
+ *     + 0.45 MSE_d), alpha_d = 0.6^(d-1) / sum_r 0.6^(r-1);
+ *   row_terms [k][n_rows][3] f32 or NULL: each row's (CE, KL, MSE), zero
+ *     outside the loss rows;
+ *   u_out [k][n_rows][H] f32 or NULL: the draft outputs u_p^(d) (row
+ *     n_rows-1 zero; for checks).
+ * Requires 1 <= n_prompt <= n_rows - 3, n_rows <= max_ctx, 1 <= k <= 8 and
+ * a workspace of mtp_objective_workspace_bytes(ctx, n_rows) bytes; device
+ * conditions set the workspace's status word (MTP_ETOKEN for a target or
+ * input outside the vocabulary). */
+size_t mtp_objective_workspace_bytes(const mtp_ctx* ctx, int32_t n_rows);
+mtp_status mtp_objective(mtp_ctx* ctx, int32_t n_rows, int32_t n_prompt, int32_t k,
+                         const int32_t* tok, const void* vision, const float* b_states,
+                         void* draft_kv, float* row_terms, float* u_out, double* loss, void* ws,
+                         size_t ws_bytes, void* stream);
+
 /* Acceptance equation: accept_len[b] = m, the longest r <= k with
  * draft_tok[b][s] == verify_tok[b][s] for all s < r; commit_tok[b] =
  * [draft_tok[b][0..m-1], verify_tok[b][m]] followed by -1 padding to k+1. */

@@ -89,6 +89,7 @@ def _L():
                                          vp, vp]
         lib.orc_verify_layer.restype = i32
         lib.orc_head.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp]
+        lib.orc_lm_logits.argtypes = [vp, vp, i32, vp, vp]
         lib.orc_rmsnorm.argtypes = [vp, vp, i32, dbl, vp]
         lib.orc_rope.argtypes = [vp, i32, i32, dbl]
         lib.orc_attend.argtypes = [vp, vp, vp, i32, i32, vp]
@@ -229,6 +230,15 @@ class Oracle:
         if rc < 0:
             raise ValueError("oracle: position outside the draft KV capacity")
         return dict(u=u, amax=amax, margin=margin, logits=logits)
+
+    def lm_logits(self, x):
+        """LM-head logits of post-norm rows x [n][H] (no final norm)."""
+        c = self.cfg
+        x = _c(x, np.float32)
+        logits = np.empty((x.shape[0], c.vocab), np.float32)
+        _L().orc_lm_logits(ctypes.byref(self.dims), ctypes.byref(self.wts), x.shape[0], _p(x),
+                           _p(logits))
+        return logits
 
     # -- building blocks (for the pins) ------------------------------------
     def moe_sublayer(self, layer, h):

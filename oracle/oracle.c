@@ -612,6 +612,14 @@ void orc_head(const orc_dims* d, const orc_weights* w, int nr, const float* h, f
   free(b);
 }
 
+/* LM head on given post-norm rows x [nr][H] (no final norm): logits
+ * [nr][V] = W_lm in(x).  The draft-head objective's verifier distribution
+ * Q_p is the softmax of these logits of b_{p+1}. */
+void orc_lm_logits(const orc_dims* d, const orc_weights* w, int nr, const float* x,
+                   float* logits) {
+  lm_head(d, w, x, nr, NULL, logits, NULL, NULL);
+}
+
 /* ---------------------------------------------------------------- */
 /* FastMTP draft rows (state-shift equation)                          */
 /* ---------------------------------------------------------------- */

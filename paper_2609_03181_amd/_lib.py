@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "MTP_OK", -1: "MTP_EINVAL", -2: "MTP_ECAPACITY", -3: "MTP_EHI
 EXPORTS = ("mtp_create", "mtp_destroy", "mtp_context_bytes", "mtp_workspace_bytes",
            "mtp_status_read",
            "mtp_status_clear", "mtp_prefill", "mtp_draft_k", "moe_verify_step",
-           "moe_verify_step_static",
+           "moe_verify_step_static", "mtp_objective_workspace_bytes", "mtp_objective",
            "greedy_accept", "kv_commit_rollback", "mtp_bench_override_drafts",
            "mtp_timing_start", "mtp_timing_stop")
 
@@ -77,6 +77,8 @@ def load():
         "mtp_draft_k": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "moe_verify_step": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "moe_verify_step_static": ([P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P], I32),
+        "mtp_objective_workspace_bytes": ([P, I32], SZ),
+        "mtp_objective": ([P, I32, I32, I32, P, P, P, P, P, P, P, P, SZ, P], I32),
         "greedy_accept": ([I32, I32, P, P, P, P, P], I32),
         "kv_commit_rollback": ([P, I32, I32, P, P, P, P, P, P, P, P, P, I32, P, P], I32),
         "mtp_bench_override_drafts": ([I32, I32, P, I32, P, P, P], I32),
@@ -151,6 +153,17 @@ def moe_verify_step_static(ctx, batch, k, pending, draft_tok, kv_len, kv_cache, 
     _check("moe_verify_step_static", load().moe_verify_step_static(
         ctx, batch, k, pending, draft_tok, kv_len, kv_cache, verify_tok, hid, logits, margin,
         route_idx, route_gap, layer_h, stream))
+
+
+def mtp_objective_workspace_bytes(ctx, n_rows):
+    return int(load().mtp_objective_workspace_bytes(ctx, n_rows))
+
+
+def mtp_objective(ctx, n_rows, n_prompt, k, tok, vision, b_states, draft_kv, row_terms, u_out,
+                  loss, ws, ws_bytes, stream):
+    _check("mtp_objective", load().mtp_objective(ctx, n_rows, n_prompt, k, tok, vision, b_states,
+                                                 draft_kv, row_terms, u_out, loss, ws, ws_bytes,
+                                                 stream))
 
 
 def greedy_accept(batch, k, draft_tok, verify_tok, accept_len, commit_tok, stream):

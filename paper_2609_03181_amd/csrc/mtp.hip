@@ -16,6 +16,7 @@
 #include "kernels_mfma.h"
 #include "kernels_small.h"
 #include "kernels_fused.h"
+#include "kernels_objective.h"
 #include "kernels_spec.h"
 
 // 16-entry chunks a routed MoE block takes when a pass has 8 or more row
@@ -633,6 +634,22 @@ struct Model {
     }
   }
 
+  // Draft-head objective: u = N_o(z) of n rows of ws.h (float32 to u) with
+  // the LM-head input in ws.xhead, and LM-head logits of the n rows of
+  // ws.xhead ([n][V], row stride V; the argmax goes to ws.tok_stage)
+  void obj_final(const Ws& ws, int n, float* u) {
+    if constexpr (BF) {
+      norm_rows(n, ws.h, nullptr, w.final_norm, u, (uint16_t*)ws.xhead);
+    } else {
+      k_rmsnorm<BF><<<n, 256, 0, s>>>(c.hidden, ws.h, c.hidden, nullptr, w.final_norm,
+                                      (float)c.rms_eps, u, c.hidden, (T*)ws.xhead, c.hidden, 0);
+    }
+  }
+  void obj_logits(const Ws& ws, int n, float* logits) {
+    if constexpr (BF) lm_mfma(ws, n, logits, c.vocab, 1, 1, 0, ws.tok_stage, nullptr);
+    else lm_head(ws, n, logits, c.vocab, 1, 1, 0, ws.tok_stage, nullptr);
+  }
+
   void draft_mfma(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
                   int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
                   float* logits, size_t ldl, bool xin_ready, bool defer_argmax) {
@@ -1079,6 +1096,110 @@ mtp_status moe_verify_step_static(mtp_ctx* ctx, int32_t batch, int32_t k,
                                         w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
     m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
                margin, route_idx, route_gap, /*embedded=*/true, layer_h);
+    return launch_status();
+  };
+  if (c.dtype == MTP_BF16) return run(std::true_type{});
+  return run(std::false_type{});
+}
+
+// ---------------------------------------------------------------- objective
+constexpr int kObjMaxK = 8;     // depths of the objective
+constexpr int kObjChunk = 256;  // draft rows per pass (the LM head's GEMM reads its weights once per pass)
+
+struct ObjWs {
+  Ws w;                           // the draft pass over up to kObjChunk rows
+  float *a, *u, *lp, *lq, *terms;
+  size_t bytes;
+};
+
+// u: every depth's outputs [kObjMaxK][n_rows][H] (a depth's rows shift into
+// the next depth's states across chunk boundaries)
+ObjWs obj_carve(const mtp_config& c, int n_rows, void* base, int n_split) {
+  const int C = n_rows - 1 < kObjChunk ? n_rows - 1 : kObjChunk;
+  ObjWs o{};
+  o.w = carve(c, 1, C, base, n_split);
+  size_t off = align_up(o.w.bytes);
+  char* p = (char*)base;
+  auto take = [&](size_t bytes) {
+    float* r = p ? (float*)(p + off) : nullptr;
+    off += align_up(bytes);
+    return r;
+  };
+  const size_t H = c.hidden, V = c.vocab;
+  o.a = take((size_t)C * H * 4);
+  o.u = take((size_t)kObjMaxK * n_rows * H * 4);
+  o.lp = take((size_t)C * V * 4);
+  o.lq = take((size_t)C * V * 4);
+  o.terms = take((size_t)kObjMaxK * n_rows * 3 * 4);
+  o.bytes = off;
+  return o;
+}
+
+size_t mtp_objective_workspace_bytes(const mtp_ctx* ctx, int32_t n_rows) {
+  if (!ctx || n_rows < 4 || n_rows > ctx->cfg.max_ctx) return 0;
+  return obj_carve(ctx->cfg, n_rows, nullptr, ctx->n_split).bytes;
+}
+
+mtp_status mtp_objective(mtp_ctx* ctx, int32_t n_rows, int32_t n_prompt, int32_t k,
+                         const int32_t* tok, const void* vision, const float* b_states,
+                         void* draft_kv, float* row_terms, float* u_out, double* loss, void* ws,
+                         size_t ws_bytes, void* stream) {
+  if (!ctx) return MTP_EINVAL;
+  const mtp_config& c = ctx->cfg;
+  if (n_rows < 4 || n_rows > c.max_ctx || n_prompt < 1 || n_prompt > n_rows - 3 || k < 1 ||
+      k > kObjMaxK || !tok || !b_states || !draft_kv || !loss || !ws ||
+      obj_carve(c, n_rows, nullptr, ctx->n_split).bytes > ws_bytes)
+    return MTP_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  auto run = [&](auto tag) -> mtp_status {
+    constexpr bool BF = decltype(tag)::value;
+    using T = typename St<BF>::T;
+    Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu,
+                ctx->moe_blocks};
+    m.prefill = true;
+    ObjWs o = obj_carve(c, n_rows, ws, ctx->n_split);
+    Ws& w = o.w;
+    const int H = c.hidden, V = c.vocab, C = n_rows - 1 < kObjChunk ? n_rows - 1 : kObjChunk;
+    const size_t cache = (size_t)2 * c.n_heads * c.max_ctx * c.head_dim;  // one depth's cache
+    k_fill_i32<<<1, 64, 0, s>>>(w.status, 1, 0);
+    k_fill_i32<<<cdiv((size_t)kObjMaxK * n_rows * 3, 256), 256, 0, s>>>(
+        (int32_t*)o.terms, kObjMaxK * n_rows * 3, 0);  // (+0.f)
+    // chunks of rows in order; inside a chunk the depths in order, each
+    // with its own draft cache, so the verifier logits Q of the chunk's
+    // rows are computed once for every depth
+    for (int c0 = 0; c0 < n_rows - 1; c0 += C) {
+      const int Cc = n_rows - 1 - c0 < C ? n_rows - 1 - c0 : C;
+      k_obj_rows_in<BF><<<Cc, 256, 0, s>>>(H, b_states + (size_t)(c0 + 1) * H, (T*)w.xhead);
+      m.obj_logits(w, Cc, o.lq);
+      for (int d = 1; d <= k; ++d) {
+        float* u_d = o.u + (size_t)(d - 1) * n_rows * H;
+        k_fill_i32<<<1, 64, 0, s>>>(w.chain_pos, 1, Cc);
+        k_rows_setup<<<cdiv(Cc, 256), 256, 0, s>>>(1, Cc, nullptr, c0, w.chain_pos, c.max_ctx,
+                                                    w.row_pos, w.row_valid, w.head_row, w.status,
+                                                    w.att_ctr, w.n_ctr);
+        k_row_tokens<<<cdiv(Cc, 256), 256, 0, s>>>(1, Cc, tok, n_rows, c0 + 1, w.row_tok);
+        k_obj_states<<<Cc, 256, 0, s>>>(c0, H, d, n_prompt, b_states,
+                                        d > 1 ? u_d - (size_t)n_rows * H : nullptr, o.a);
+        m.draft(w, 1, Cc, o.a, (size_t)H, (const T*)vision, n_rows, c0 + 1,
+                (T*)draft_kv + (size_t)(d - 1) * cache, false, nullptr, 0, 0, nullptr, 0);
+        m.obj_final(w, Cc, u_d + (size_t)c0 * H);
+        m.obj_logits(w, Cc, o.lp);
+        k_obj_terms<<<Cc, 256, 0, s>>>(c0, n_rows, n_prompt, V, H, o.lp, o.lq, u_d, b_states,
+                                       tok, o.terms + (size_t)(d - 1) * n_rows * 3, w.status);
+      }
+    }
+    k_obj_loss<<<1, 256, 0, s>>>(k, n_rows, n_prompt, 0.6, o.terms, loss);
+    if (row_terms)
+      (void)hipMemcpyAsync(row_terms, o.terms, (size_t)k * n_rows * 3 * 4,
+                           hipMemcpyDeviceToDevice, s);
+    if (u_out)
+      for (int d = 0; d < k; ++d) {
+        float* dst = u_out + (size_t)d * n_rows * H;
+        (void)hipMemcpyAsync(dst, o.u + (size_t)d * n_rows * H, (size_t)(n_rows - 1) * H * 4,
+                             hipMemcpyDeviceToDevice, s);
+        k_fill_i32<<<cdiv(H, 256), 256, 0, s>>>((int32_t*)(dst + (size_t)(n_rows - 1) * H), H,
+                                               0);  // (+0.f; no memset node under capture)
+      }
     return launch_status();
   };
   if (c.dtype == MTP_BF16) return run(std::true_type{});

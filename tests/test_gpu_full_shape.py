@@ -17,7 +17,9 @@ whole step captured in a HIP graph and replayed), against the oracle:
 * batch 64: cached contexts U{512..4096} (seed 12), Zipf(1.1) router bias,
   every sequence with a synthetic cache; 8 sequences replayed;
 * batch 1 at a long context: 30,000 cached positions of a 32,768-position
-  cache (RoPE base 1e6; decode attention in 64 key splits of 512).
+  cache (RoPE base 1e6; decode attention in 64 key splits of 512);
+* a Gundam-mode page: 1156 vision rows + 64 prompt tokens prefilled in one
+  pass, then graph-replayed steps.
 
 Tolerances come from tests/tolerances.py (per-layer routing tolerances and
 float tolerances derived from the measured float32-summation drift of
@@ -203,6 +205,39 @@ def test_full_shape_batch1_one_pass_prefill_forced_and_natural_steps(plain):
     log(f"[full B=1] {n_forced} forced + {n_nat} natural steps ok; end-to-end near-tie band "
         f"(prefill included): {replay.assert_band(stats)}; layer-local: "
         f"{replay.assert_local_band(lstats)}")
+
+
+def test_full_shape_gundam_prefix_one_pass(plain):
+    """Gundam-mode page (Table "Model specification": 256 + 100 n visual
+    rows, n = 9 -> 1156, the largest) + 64 prompt tokens prefilled in one
+    pass of 1220 rows, then graph-replayed steps: prefill token, state,
+    every verifier K/V position and the draft cache against the oracle."""
+    w, model, orc = plain
+    K, n_vis, n_txt, n_steps = 3, 1156, 64, 3
+    P = n_vis + n_txt
+    tok, vis = prefix_inputs(CFG, 1, n_vis, n_txt)
+    log(f"[gundam] GPU prefill of {P} rows in one pass")
+    s = gpu_prefill(model, 1, K, tok, vis, n_steps * (K + 1) + 4, prefill_rows=P)
+    assert s.status() == 0
+    log("[gundam] oracle prefill")
+    st = oracle_prefill(orc, CFG, tok[0], vis[0], P + n_steps * (K + 1) + 8, 1 << 30,
+                        routes=s.prefill_routes.cpu().numpy()[:, 0])
+    stats, lstats = replay.new_stats(), replay.new_stats()
+    replay.count_routes(stats, st.prefill_route_gap, tolerances.route_tol(CFG),
+                        st.prefill_routes_followed)
+    t = replay.check_token(st.last_logits, st.pending, int(s.pending[0]), "prefill token", stats)
+    st.pending = t
+    st.next_tok[0] = t
+    st.out[0] = t
+    np.testing.assert_allclose(s.hid.cpu().numpy()[0, 0], st.hid[0], rtol=TOL, atol=STATE_TOL)
+    kv = s.kv[:, 0, :, :, :P].cpu().numpy().view(np.uint16)
+    np.testing.assert_allclose(synth.bf16_bits_to_f32(kv), st.kv[:, :, :, :P], rtol=TOL, atol=TOL)
+    dkv = s.dkv[0, :, :, :P - 1].cpu().numpy().view(np.uint16)
+    np.testing.assert_allclose(synth.bf16_bits_to_f32(dkv), st.dkv[:, :, :P - 1], rtol=TOL,
+                               atol=TOL)
+    _replay_steps(orc, s, {0: st}, K, n_steps, stats, lstats)
+    log(f"[gundam] {P}-row prefill + {n_steps} steps ok; end-to-end near-tie band: "
+        f"{replay.assert_band(stats)}; layer-local: {replay.assert_local_band(lstats)}")
 
 
 def test_full_shape_batch1_spec_equals_greedy_bitwise(plain):
