@@ -1,0 +1,205 @@
+// Flash-style causal attention for prefill passes (many query rows of a
+// sequence against its cache), 128-dim heads.  Both products on MFMA
+// (16x16x32 bf16): the scores S = K Q^T with the float32 query split into
+// bf16 high and low parts (two products per k-step, as the decode kernel
+// does: the scores keep ~16 mantissa bits of the query), the values
+// O^T = V^T P^T with the float32 probabilities split the same way (so the
+// weighted sum keeps ~16 bits of each weight before its float32
+// accumulation).  Online softmax in float32 per row.
+#pragma once
+#include "kernels_small.h"
+
+namespace mtp {
+
+// two bf16 parts (high, low) of 8 floats, packed as MFMA operands
+__device__ __forceinline__ void split8(const float (&x)[8], uint4& hi, uint4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint16_t h0 = f2bf(x[2 * e]), h1 = f2bf(x[2 * e + 1]);
+    const uint16_t l0 = f2bf(x[2 * e] - bf2f(h0)), l1 = f2bf(x[2 * e + 1] - bf2f(h1));
+    h[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    l[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+// Block = 4 waves = 64 query rows (wave w: rows 16w..16w+15 of tile
+// blockIdx.x) of head blockIdx.y of sequence blockIdx.z; the C rows of each
+// sequence sit at row_pos[b*C + i] (invalid rows: zeros).  Keys run in
+// 64-key tiles up to the largest position of the block's valid rows; each
+// row masks keys past its own position.
+//
+// Layouts (lane l, g = l/16, i = l%16):
+//   S tile q (keys 16q..16q+15 of the key tile): A = K rows (lane: key i,
+//     dims 8g.. of the k-step, straight from the cache), B = Q (lane: row i,
+//     same dims) -> lane holds S[key 16q + 4g + t][row i], t = 0..3;
+//   PV over 32 keys c (S tiles 2c, 2c+1): the contraction order pairs the
+//     lane's own scores with the keys it holds, position 8g + j ->
+//     key 32c + 4g + j (j < 4) or 32c + 16 + 4g + j - 4 (j >= 4), so
+//     B = P needs no data movement and A = V^T reads two 8-byte runs of the
+//     V tile, stored transposed in LDS ([dim][key]); the result lane holds
+//     O[row i][dim 16d + 4g + t] for dim tile d.
+template <int DH>
+__global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
+                                                       const float* __restrict__ q,
+                                                       const uint16_t* __restrict__ cache,
+                                                       size_t seq_stride, int cap,
+                                                       const int32_t* __restrict__ row_pos,
+                                                       const int32_t* __restrict__ row_valid,
+                                                       float scale, uint16_t* __restrict__ out) {
+  static_assert(DH == 128, "four k-steps of 32 dims");
+  constexpr int NS = DH / 32, ND = DH / 16, VL = 64 + 8;
+  __shared__ __align__(16) uint16_t vt[DH * VL];  // V tile transposed: [dim][key]
+  __shared__ int s_kmax;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int i16 = lane & 15, g = lane >> 4;
+  const int h = blockIdx.y, b = blockIdx.z, D = nh * DH;
+  const int r = blockIdx.x * 64 + 16 * w + i16;  // this lane's query row (of the sequence)
+  const bool rv = r < C && row_valid[(size_t)b * C + r];
+  const int rp = rv ? row_pos[(size_t)b * C + r] : -1;
+  if (threadIdx.x == 0) s_kmax = 0;
+  __syncthreads();
+  if (rv) atomicMax(&s_kmax, rp + 1);
+  // query operands (high / low parts) of the four k-steps
+  uint4 qh[NS], ql[NS];
+  {
+    const float* qp = q + ((size_t)b * C + (r < C ? r : 0)) * D + (size_t)h * DH + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks) {
+      float x[8];
+      const float4 a = rv ? ld_f4(qp + 32 * ks) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 c = rv ? ld_f4(qp + 32 * ks + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+      x[4] = c.x; x[5] = c.y; x[6] = c.z; x[7] = c.w;
+      split8(x, qh[ks], ql[ks]);
+    }
+  }
+  __syncthreads();
+  const int kmax = s_kmax < cap ? s_kmax : cap;
+  const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
+  const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
+  float m = -INFINITY, lsum = 0.f;
+  f32x4_t o[ND];
+#pragma unroll
+  for (int d = 0; d < ND; ++d) o[d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // tiles in flight: this wave's K operands (straight from the cache) and
+  // this thread's share of the V tile (16-byte pieces: 8 dims of one key;
+  // consecutive lanes take consecutive keys, so the transposed LDS writes
+  // of a wave fall on consecutive 2-byte addresses);
+  // keys past the capacity clamp to its last row and are masked below.
+  // The next tile's loads are issued as soon as the current tile's
+  // registers are free, so they fly during its softmax and P.V.
+  constexpr int VP = 64 * DH / 8 / 256;
+  uint4 ka[4][NS], vr[VP];
+  auto load_k = [&](int k0) {
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      const int key = min(k0 + 16 * qq + i16, cap - 1);
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks)
+        ka[qq][ks] = *(const uint4*)(Kc + (size_t)key * DH + 32 * ks + 8 * g);
+    }
+  };
+  auto load_v = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < VP; ++u) {
+      const int c = threadIdx.x + 256 * u;
+      const int key = min(k0 + (c & 63), cap - 1);
+      vr[u] = *(const uint4*)(Vc + (size_t)key * DH + (c >> 6) * 8);
+    }
+  };
+  if (kmax > 0) {
+    load_k(0);
+    load_v(0);
+  }
+  for (int k0 = 0; k0 < kmax; k0 += 64) {
+    const bool more = k0 + 64 < kmax;
+    __syncthreads();  // the previous tile's P.V is done with the V tile
+#pragma unroll
+    for (int u = 0; u < VP; ++u) {  // V tile into LDS, transposed
+      const int c = threadIdx.x + 256 * u;
+      const int kk = c & 63, part = c >> 6;
+      const uint32_t vv[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt[(part * 8 + 2 * e) * VL + kk] = (uint16_t)(vv[e] & 0xffffu);
+        vt[(part * 8 + 2 * e + 1) * VL + kk] = (uint16_t)(vv[e] >> 16);
+      }
+    }
+    if (more) load_v(k0 + 64);
+    // scores, scaled and masked
+    float s[4][4];
+    float mx = m;
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks) {
+        acc = mfma16(ka[qq][ks], qh[ks], acc);
+        acc = mfma16(ka[qq][ks], ql[ks], acc);
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int kp = k0 + 16 * qq + 4 * g + t;
+        s[qq][t] = (kp <= rp) ? acc[t] * scale : -INFINITY;
+        mx = fmaxf(mx, s[qq][t]);
+      }
+    }
+    if (more) load_k(k0 + 64);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, MTP_WAVE));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, MTP_WAVE));
+    const float corr = (mx == -INFINITY) ? 1.f : __expf(m - mx);
+    float ps = 0.f;
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float p = (mx == -INFINITY) ? 0.f : __expf(s[qq][t] - mx);
+        s[qq][t] = p;
+        ps += p;
+      }
+    lsum = __builtin_fmaf(lsum, corr, ps);
+    m = mx;
+#pragma unroll
+    for (int d = 0; d < ND; ++d) o[d] *= corr;
+    __syncthreads();  // the V tile is in LDS
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float x[8];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        x[t] = s[2 * c][t];
+        x[4 + t] = s[2 * c + 1][t];
+      }
+      uint4 ph, pl;
+      split8(x, ph, pl);
+#pragma unroll
+      for (int d = 0; d < ND; ++d) {
+        const uint16_t* vp = vt + (16 * d + i16) * VL + 32 * c + 4 * g;
+        const uint2 a0 = *(const uint2*)vp;
+        const uint2 a1 = *(const uint2*)(vp + 16);
+        const uint4 av = make_uint4(a0.x, a0.y, a1.x, a1.y);
+        o[d] = mfma16(av, ph, o[d]);
+        o[d] = mfma16(av, pl, o[d]);
+      }
+    }
+  }
+  // the row's sum over its four lanes, then O / l as bf16
+  float lt = lsum + __shfl_xor(lsum, 16, MTP_WAVE);
+  lt += __shfl_xor(lt, 32, MTP_WAVE);
+  if (r < C) {
+    uint16_t* op = out + ((size_t)b * C + r) * D + (size_t)h * DH + 4 * g;
+    const float inv = (rv && lt > 0.f) ? 1.f / lt : 0.f;
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      uint2 pk;
+      pk.x = (uint32_t)f2bf(o[d][0] * inv) | ((uint32_t)f2bf(o[d][1] * inv) << 16);
+      pk.y = (uint32_t)f2bf(o[d][2] * inv) | ((uint32_t)f2bf(o[d][3] * inv) << 16);
+      *(uint2*)(op + 16 * d) = pk;
+    }
+  }
+}
+
+}  // namespace mtp

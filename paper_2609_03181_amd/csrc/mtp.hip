@@ -17,6 +17,7 @@
 #include "kernels_small.h"
 #include "kernels_fused.h"
 #include "kernels_objective.h"
+#include "kernels_flash.h"
 #include "kernels_spec.h"
 
 // 16-entry chunks a routed MoE block takes when a pass has 8 or more row
@@ -106,6 +107,8 @@ mtp_status scratch_addr(void** out) {
 constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
 constexpr int kDownSplit = 8;  // blocks per output strip of the small-batch MoE down
 constexpr int kMoeSpinMax = 1 << 20;  // polls of a fused-MoE wait before it gives up
+constexpr int kFlashRows = 64;  // prefill passes of at least this many rows per sequence use
+                                // the flash-style attention
 
 // Blocks of the fused small-batch MoE that the device holds at once (its
 // waits need every block resident), or 0 when the shape is outside what it
@@ -453,6 +456,12 @@ struct Model {
   }
   template <int DH>
   void sattn(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
+    if (DH == 128 && prefill && C >= kFlashRows) {  // prefill passes: flash-style, both products on MFMA
+      launch_k(tm, MTP_KC_ATTN, k_flash_prefill<128>, dim3(cdiv(C, 64), c.n_heads, B), dim3(256),
+               0, s, C, c.n_heads, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos, ws.row_valid,
+               1.0f / sqrtf(128.f), (uint16_t*)ws.attn);
+      return;
+    }
     if (DH == 128) sattn4(ws, B, C, cache, seq_stride);
     else if (C <= 1) sattn_launch<DH, 1>(ws, B, C, cache, seq_stride);
     else if (C <= 2) sattn_launch<DH, 2>(ws, B, C, cache, seq_stride);
