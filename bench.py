@@ -79,8 +79,8 @@ def verify_bytes(cfg, B, K, kv_len, routes):
 
 KERNEL_CLASSES = {  # timing-hook class -> kernel name as the profiler lists it
     1: ("decode attention", "mtp::k_s_attn"),
-    2: ("verify MoE gate/up + SwiGLU", "mtp::k_s_gu<0,"),
-    3: ("verify MoE down", "mtp::k_s_down"),
+    2: ("verify MoE gate/up + SwiGLU", "mtp::k_gu_gemm<0>"),
+    3: ("verify MoE down", "mtp::k_down_gemm"),
     4: ("LM head + partial argmax", "mtp::k_s_lm"),
     5: ("RMSNorm + QKV + RoPE + KV append", "mtp::k_s_qkv"),
     6: ("RMSNorm + router + top-k", "mtp::k_s_router"),
@@ -96,6 +96,8 @@ def class_kernel(kc, rows):
     form)."""
     if kc == 2 and rows <= 16:
         return "mtp::k_s_gu_stream"
+    if kc == 3 and rows <= 16:
+        return "mtp::k_s_down_split"
     return KERNEL_CLASSES[kc][1]
 
 
@@ -786,7 +788,7 @@ def run_workload(name, args, cpu=False):
                                "frac_of_own_roofline": round(tf / ceil, 4),
                                "counters": {k.split("(")[0]: v for k, v in
                                             (_mfma_counters(name) or {}).items()
-                                            if k.startswith(("mtp::k_s_gu<0,", "mtp::k_s_down",
+                                            if k.startswith(("mtp::k_gu_gemm<0>", "mtp::k_down_gemm",
                                                              "mtp::k_lm_gemm"))} or None}
     if pages:
         rec["config"]["pages_per_s"] = round(B / dt, 4)

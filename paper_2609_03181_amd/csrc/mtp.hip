@@ -18,6 +18,7 @@
 #include "kernels_fused.h"
 #include "kernels_objective.h"
 #include "kernels_flash.h"
+#include "kernels_gemm.h"
 #include "kernels_spec.h"
 
 // 16-entry chunks a routed MoE block takes when a pass has 8 or more row
@@ -586,10 +587,12 @@ struct Model {
            ws.ent_slot, ws.ent_w, ws.touched, ws.n_touched)
       MTP_MAXT_DISPATCH(H / 128, MTP_ROUTER);
 #undef MTP_ROUTER
-      const int cpb = G >= 8 ? MTP_MOE_CPB : 1;  // 16-entry chunks per MoE block
+      // more than 16 rows: grouping with 64-entry chunk blocks (the grouped
+      // GEMMs' row tile)
       if (G > 1)
         k_group<<<1, 1024, 0, s>>>(R, E, k, ws.ridx, ws.rw, ws.cnt, ws.off, ws.ent_row,
-                                   ws.ent_slot, ws.ent_w, cpb, ws.cbp);
+                                   ws.ent_slot, ws.ent_w, kGemmM / 16, ws.cbp);
+      const unsigned chunks = (unsigned)(E + cdiv((size_t)R * k, kGemmM)) + cdiv(R, kGemmM);
       if (G == 1) {  // persistent streaming form: two blocks per compute unit
         const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
         const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
@@ -599,18 +602,14 @@ struct Model {
            ws.touched, ws.n_touched, (uint16_t*)ws.act, ws.act_sh)
         MTP_MAXT_DISPATCH(H / 128, MTP_GU);
 #undef MTP_GU
-      } else {  // compact grid: at most E + R*k/(16*cpb) routed chunk blocks
-        const unsigned nblk = (E + cdiv((size_t)R * k, 16 * cpb)) * (I / 16) +
-                              cdiv(R, 16 * cpb) * (SI / 16);
-        const uint4* egu = pk.exp_gu + (size_t)l * E * pk.exp_gu_s;
-        const uint4* sgu = pk.sh_gu + l * pk.sh_gu_s;
-#define MTP_GU(M)                                                                             \
-  launch_k(tm, MTP_KC_MOE_GU, prefill ? k_s_gu<GU_PREFILL, M> : k_s_gu<GU_VERIFY, M>,         \
-           dim3(nblk), dim3(256), 0, s, cpb, R, H, E, I, SI, (const uint16_t*)ws.xin, nullptr,  \
-           nullptr, eps, egu, pk.exp_gu_s, sgu, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act, \
-           ws.act_sh, ws.cbp)
-        MTP_MAXT_DISPATCH(H / 128, MTP_GU);
-#undef MTP_GU
+      } else {  // grouped GEMM on the compact grid (blocks past the last item exit)
+        const unsigned nblk = (unsigned)(E + cdiv((size_t)R * k, kGemmM)) * (I / kGemmN) +
+                              cdiv(R, kGemmM) * (SI / kGemmN);
+        launch_k(tm, MTP_KC_MOE_GU, prefill ? k_gu_gemm<GU_PREFILL> : k_gu_gemm<GU_VERIFY>,
+                 dim3(nblk), dim3(256), 0, s, R, H, E, I, SI, (const uint16_t*)ws.xin,
+                 pk.exp_gu + (size_t)l * E * pk.exp_gu_s, pk.exp_gu_s,
+                 pk.sh_gu + l * pk.sh_gu_s, ws.cnt, ws.off, ws.ent_row, (uint16_t*)ws.act,
+                 ws.act_sh, ws.cbp);
       }
       const uint4* edn = pk.exp_down + (size_t)l * E * pk.exp_down_s;
       const uint4* sdn = pk.sh_down + l * pk.sh_down_s;
@@ -619,14 +618,10 @@ struct Model {
                  dim3(256), 0, s, R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh, edn,
                  pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.touched,
                  ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h, ws.status);
-      else {
-#define MTP_DSLOT(M)                                                                            \
-  launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot<M>, dim3(H / 16, E + 1, cdiv(G, cpb)), dim3(256),  \
-           0, s, cpb, R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn,                \
-           pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot)
-        MTP_MAXT_DISPATCH(I / 128, MTP_DSLOT);
-#undef MTP_DSLOT
-      }
+      else
+        launch_k(tm, MTP_KC_MOE_DOWN, k_down_gemm, dim3(chunks * (H / kGemmN)), dim3(256), 0, s,
+                 R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn,
+                 ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot, ws.cbp);
     }
     uint16_t* xh = (tok && head_all) ? (uint16_t*)ws.xhead : nullptr;
     if (small)
