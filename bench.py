@@ -90,14 +90,21 @@ KERNEL_CLASSES = {  # timing-hook class -> kernel name as the profiler lists it
 }
 
 
-def class_kernel(kc, rows):
-    """Profiler name prefix of class kc's kernel for a verify pass of `rows`
-    rows (up to 16 rows the MoE gate/up runs in its persistent streaming
-    form)."""
+def class_kernel(kc, B, K):
+    """Profiler name prefix of class kc's kernel in a step of batch B with K
+    draft tokens: verify passes of B*(K+1) rows, draft passes of B rows.  Up
+    to 16 rows the MoE gate/up and down run in their streaming forms and
+    QKV and the draft FFN in their split-K forms; more rows run the tiled
+    GEMMs (the dense ones with a reduce launch when K is split)."""
+    rows = B * (K + 1)
     if kc == 2 and rows <= 16:
         return "mtp::k_s_gu_stream"
     if kc == 3 and rows <= 16:
         return "mtp::k_s_down_split"
+    if kc == 5 and rows > 16:
+        return "mtp::k_dense_gemm<2>"
+    if kc == 7 and B > 16:
+        return "mtp::k_dense_gemm<3>"
     return KERNEL_CLASSES[kc][1]
 
 
@@ -704,7 +711,7 @@ def run_workload(name, args, cpu=False):
     # stream), with the class's algorithmic bytes and FLOPs
     kernels = {}
     for kc, (what, _) in KERNEL_CLASSES.items():
-        kname = class_kernel(kc, B * (K + 1))
+        kname = class_kernel(kc, B, K)
         tot_ms = tot_b = tot_f = 0.0
         n_l = 0
         for _ in range(nk):
@@ -768,7 +775,7 @@ def run_workload(name, args, cpu=False):
             "frac": round(kd["GB_s"] / HBM_PEAK_GBS, 4), "traffic": _traffic(name, dom),
             "kernel": dom, "what": kd["what"], "bytes_per_launch": kd["bytes_per_launch"],
             "us_per_launch": kd["us_per_launch"]}
-    gu, dn = class_kernel(2, B * (K + 1)), class_kernel(3, B * (K + 1))
+    gu, dn = class_kernel(2, B, K), class_kernel(3, B, K)
     if gu in kernels and dn in kernels and B * (K + 1) > 16:
         # the grouped MoE GEMM (gate/up + down): algorithmic FLOPs over its
         # measured time, against the bf16 MFMA peak and against its own

@@ -1,46 +1,72 @@
-// Grouped MoE products for passes of more than 16 rows (prefill, large
-// verify batches): per expert a GEMM over its entries, tiled so that each
-// weight tile feeds 64 entries and each staged row tile feeds 128 output
-// features.
+// Tiled products for passes of more than 16 rows (prefill, large verify and
+// draft batches): the grouped MoE gate/up and down (per expert a GEMM over
+// its entries) and the dense projections (QKV with RoPE and the K/V append,
+// O / eh / FFN-down with the residual, the draft FFN gate/up), the latter
+// with an optional K split over blocks when there are few tiles.
 //
-// Block = 4 waves = 128 output features (wave w: two 16-wide strips,
-// features 32w..32w+31 of the block) x 64 entries (four MFMA row tiles).
-// The entries' rows are staged through LDS in K chunks of 128 columns,
-// double-buffered (the next chunk's global loads fly during the current
-// chunk's products); each wave loads its own weight tiles (the packed
-// operand tiles of kernels_mfma.h) straight from memory.  Per k-step a
-// wave issues 4 (down: 2) weight-tile loads and 4 LDS row reads for 16
-// (down: 8) MFMAs.  K is summed in one chain per output tile, in order.
+// Block = 4 waves = 128 output features (wave w: two 16-wide strips) x 64
+// rows (four MFMA row tiles).  The rows are staged through LDS in K chunks
+// of 128 columns, double-buffered; each wave loads its own weight tiles
+// (the packed operand tiles of kernels_mfma.h) straight from memory, one K
+// chunk ahead of its products, so a chunk's weight loads fly during the
+// previous chunk's MFMAs.  Per k-step a wave issues 2 weight-tile loads per
+// matrix and 4 LDS row reads for 8 MFMAs per matrix.  K is summed in one
+// chain per output tile, in order.
 //
-// Work items come from the compact grid of k_group (cbp with 64-entry
-// chunk blocks): the routed chunk blocks x the N-blocks of one expert, then
-// the shared experts' chunk blocks x theirs.
+// Work items: (weight slab = 128 features of one matrix, 64-row chunk),
+// ordered with the chunks of a slab consecutive; blocks are dispatched to
+// the 8 XCDs round-robin, so block b takes item xcd_item(b): each XCD takes
+// a contiguous run of items, and the chunks that share a weight slab run
+// together on one XCD and read it through one L2.
 #pragma once
 #include "kernels_small.h"
 
 namespace mtp {
 
-constexpr int kGemmM = 64;             // entries per block
+constexpr int kGemmM = 64;             // rows (entries) per block
 constexpr int kGemmN = 128;            // output features per block
 constexpr int kGemmKC = 128;           // K columns per LDS stage
 constexpr int kGemmLd = kGemmKC + 8;   // LDS row stride (bf16)
+constexpr int kXcd = 8;                // XCDs the blocks are spread over
 
-// item b: expert e (E = the shared experts), chunk z of 64 entries, N-block
-// nb; false past the last item
+// Logical item of block b among `total`: XCD x = b mod 8 takes items
+// [x*P, (x+1)*P), P = ceil(total / 8), in dispatch order.  Returns total
+// for a block past the last item (the grid is 8 * ceil(bound / 8) for a
+// bound >= total).
+__device__ __forceinline__ int xcd_item(int b, int total) {
+  const int P = (total + kXcd - 1) / kXcd, x = b % kXcd, s = b / kXcd;
+  return s < P ? min(x * P + s, total) : total;
+}
+
+// Grouped item b (cbp: the grouping kernel's prefix of 64-entry chunk
+// blocks, cbp[E] the routed total, cbp[E+1] with the shared rows' chunks):
+// expert e (E = the shared experts), chunk z, N-block nb; nbr / nbs
+// N-blocks per routed / shared slab.  The items of one expert are its nz
+// chunks x nbr N-blocks, chunk fastest.  false past the last item.
 __device__ __forceinline__ bool gemm_item(int b, int E, int nbr, int nbs,
                                           const int32_t* __restrict__ cbp, int& e, int& z,
                                           int& nb) {
-  const int nr = cbp[E] * nbr;
-  if (b < nr) {
-    nb = b % nbr;
-    e = chunk_block_expert(b / nbr, E, cbp, z);
-    return true;
+  const int lane = threadIdx.x & 63;
+  const int pv = lane < E ? cbp[lane] : 0x7fffffff;
+  const int pe = cbp[E], nzs = cbp[E + 1] - pe;
+  const int nr = pe * nbr, total = nr + nzs * nbs;
+  const int L = xcd_item(b, total);
+  if (L >= total) return false;
+  if (L < nr) {
+    const int c = L / nbr;  // some chunk block of the expert
+    e = __popcll(__ballot(pv <= c)) - 1;
+    const int c0 = __shfl(pv, e, MTP_WAVE);
+    const int c1 = e + 1 < E ? __shfl(pv, e + 1, MTP_WAVE) : pe;
+    const int local = L - c0 * nbr, nz = c1 - c0;
+    nb = local / nz;
+    z = local % nz;
+  } else {
+    e = E;
+    const int local = L - nr;
+    nb = local / nzs;
+    z = local % nzs;
   }
-  const int bb = b - nr;
-  e = E;
-  nb = bb % nbs;
-  z = bb / nbs;
-  return cbp[E] + z < cbp[E + 1];
+  return true;
 }
 
 // The 64 rows x 128 columns of one K chunk: thread piece u (of 4) is row
@@ -61,10 +87,100 @@ struct RowStage {
   }
 };
 
-// Grouped gate/up + SwiGLU.  Routed expert e: entries off[e].. (rows
+// Row piece u of this thread: row of the chunk and column offset
+__device__ __forceinline__ int stage_row(int u) { return (threadIdx.x + 256 * u) >> 4; }
+__device__ __forceinline__ int stage_col(int u) { return 8 * ((threadIdx.x + 256 * u) & 15); }
+
+// acc[a][j][mt] = sum over K of matrix a's strip j (tile stream Wt[a][j],
+// lane offset included) times row tile mt of the staged rows.  K is a
+// multiple of kGemmKC; st.src is set; xs0 / xs1 are the two LDS stages.
+// PF: the weight tiles of chunk kc + 1 are loaded during chunk kc's
+// products (two register sets); else each chunk's tiles are loaded at its
+// start (one set: with two matrices, two waves per SIMD fit instead of one,
+// and the other wave covers the load latency).
+template <int NA, bool PF>
+__device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K, bool once,
+                                          RowStage& st, uint16_t* xs0, uint16_t* xs1,
+                                          f32x4_t (&acc)[NA][2][4]) {
+  const int lane = threadIdx.x & 63, i16 = lane & 15, g = lane >> 4;
+  const int nch = K / kGemmKC;
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[a][j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  uint4 wa[NA][4][2];
+  auto load_w = [&](uint4 (&wt)[NA][4][2], int kc) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) wt[a][ks][j] = ld_tile(Wt[a][j] + (size_t)(kc * 4 + ks) * 64, once);
+  };
+  auto mma = [&](const uint4 (&wt)[NA][4][2], const uint16_t* xs) {
+    const uint16_t* xb = xs + i16 * kGemmLd + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      uint4 bx[4];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) bx[mt] = *(const uint4*)(xb + mt * 16 * kGemmLd + 32 * ks);
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt) acc[a][j][mt] = mfma16(wt[a][ks][j], bx[mt], acc[a][j][mt]);
+    }
+  };
+  st.load(0);
+  load_w(wa, 0);
+  st.store(xs0);
+  if constexpr (!PF) {
+    for (int kc = 0; kc < nch; ++kc) {
+      uint16_t* cur = (kc & 1) ? xs1 : xs0;
+      if (kc > 0) load_w(wa, kc);
+      if (kc + 1 < nch) st.load((kc + 1) * kGemmKC);
+      __syncthreads();  // cur holds chunk kc; every wave is done reading the other stage
+      mma(wa, cur);
+      if (kc + 1 < nch) st.store((kc & 1) ? xs0 : xs1);
+    }
+    return;
+  }
+  uint4 wb[NA][4][2];
+  for (int kc = 0; kc < nch; kc += 2) {
+    // chunk kc: weights wa, rows xs0; chunk kc + 1's loads in flight
+    if (kc + 1 < nch) {
+      load_w(wb, kc + 1);
+      st.load((kc + 1) * kGemmKC);
+    }
+    __syncthreads();  // xs0 holds chunk kc; every wave is done reading xs1
+    mma(wa, xs0);
+    if (kc + 1 >= nch) break;
+    st.store(xs1);
+    if (kc + 2 < nch) {
+      load_w(wa, kc + 2);
+      st.load((kc + 2) * kGemmKC);
+    }
+    __syncthreads();  // xs1 holds chunk kc + 1; every wave is done reading xs0
+    mma(wb, xs1);
+    if (kc + 2 < nch) st.store(xs0);
+  }
+}
+
+// Packed bf16 of four floats
+__device__ __forceinline__ uint2 pack4(float a, float b, float c, float d) {
+  uint2 p;
+  p.x = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  p.y = (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16);
+  return p;
+}
+
+// Grouped gate/up + SwiGLU: routed expert e: entries off[e].. (rows
 // ent_row[]) of xg (normalised bf16 rows [R][H]) -> act[entry][I]; shared
 // (e == E): rows 0..R-1 -> act_sh[row][SI] (the shared experts as one
-// width-SI SwiGLU).  ROLE only names the instance.
+// width-SI SwiGLU).  ROLE only names the instance (decode or prefill).
 template <int ROLE>
 __global__ void __launch_bounds__(256) k_gu_gemm(int R, int H, int E, int I, int SI,
                                                  const uint16_t* __restrict__ xg,
@@ -86,55 +202,22 @@ __global__ void __launch_bounds__(256) k_gu_gemm(int R, int H, int E, int I, int
   if (t0 >= n) return;
   const int W = dense ? SI : I, ns = W / 16, nkt = H / 32;
   const uint4* base = dense ? sgu : egu + (size_t)e * e_stride;
-  const int s0 = nb * (kGemmN / 16) + 2 * w;  // this wave's first gate strip
-  const uint4* Ag = base + (size_t)s0 * nkt * 64 + lane;
-  const uint4* Au = base + (size_t)(ns + s0) * nkt * 64 + lane;
-  const bool once = n <= kGemmM;  // the expert's tiles are read by this chunk only
+  const int s0 = nb * (kGemmN / 16) + 2 * w;  // this wave's first strip
+  const uint4* Wt[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    Wt[0][j] = base + (size_t)(s0 + j) * nkt * 64 + lane;       // gate
+    Wt[1][j] = base + (size_t)(ns + s0 + j) * nkt * 64 + lane;  // up
+  }
   RowStage st;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int t = t0 + ((threadIdx.x + 256 * u) >> 4);
+    const int t = t0 + stage_row(u);
     const int row = t < n ? (dense ? t : ent_row[o + t]) : -1;
-    st.src[u] = row >= 0 ? xg + (size_t)row * H + 8 * ((threadIdx.x + 256 * u) & 15) : nullptr;
+    st.src[u] = row >= 0 ? xg + (size_t)row * H + stage_col(u) : nullptr;
   }
-  st.load(0);
-  st.store(xs[0]);
-  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  f32x4_t cg[2][4], cu[2][4];
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) cg[j][mt] = cu[j][mt] = z4;
-  const int nch = H / kGemmKC;
-  for (int kc = 0; kc < nch; ++kc) {
-    const int buf = kc & 1;
-    uint4 ag[4][2], au[4][2];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const size_t tt = (size_t)j * nkt * 64 + (size_t)(kc * 4 + ks) * 64;
-        ag[ks][j] = ld_tile(Ag + tt, once);
-        au[ks][j] = ld_tile(Au + tt, once);
-      }
-    if (kc + 1 < nch) st.load((kc + 1) * kGemmKC);
-    __syncthreads();  // chunk kc is in xs[buf]; everyone is done with xs[buf ^ 1]
-    const uint16_t* xb = xs[buf] + i16 * kGemmLd + 8 * g;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      uint4 bx[4];
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) bx[mt] = *(const uint4*)(xb + mt * 16 * kGemmLd + 32 * ks);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-          cg[j][mt] = mfma16(ag[ks][j], bx[mt], cg[j][mt]);
-          cu[j][mt] = mfma16(au[ks][j], bx[mt], cu[j][mt]);
-        }
-    }
-    if (kc + 1 < nch) st.store(xs[buf ^ 1]);
-  }
+  f32x4_t acc[2][2][4];
+  gemm_core<2, false>(Wt, H, n <= kGemmM, st, xs[0], xs[1], acc);
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
     const int t = t0 + mt * 16 + i16;
@@ -142,11 +225,9 @@ __global__ void __launch_bounds__(256) k_gu_gemm(int R, int H, int E, int I, int
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int f = (s0 + j) * 16 + 4 * g;
-      uint2 pk;
-      pk.x = (uint32_t)f2bf(silu(cg[j][mt][0]) * cu[j][mt][0]) |
-             ((uint32_t)f2bf(silu(cg[j][mt][1]) * cu[j][mt][1]) << 16);
-      pk.y = (uint32_t)f2bf(silu(cg[j][mt][2]) * cu[j][mt][2]) |
-             ((uint32_t)f2bf(silu(cg[j][mt][3]) * cu[j][mt][3]) << 16);
+      const f32x4_t cg = acc[0][j][mt], cu = acc[1][j][mt];
+      const uint2 pk = pack4(silu(cg[0]) * cu[0], silu(cg[1]) * cu[1], silu(cg[2]) * cu[2],
+                             silu(cg[3]) * cu[3]);
       if (dense) *(uint2*)(act_sh + (size_t)t * SI + f) = pk;
       else *(uint2*)(act + (size_t)(o + t) * I + f) = pk;
     }
@@ -179,47 +260,19 @@ __global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H
   if (t0 >= n) return;
   const int K = dense ? SI : I, nkt = K / 32;
   const int s0 = nb * (kGemmN / 16) + 2 * w;  // this wave's first output strip
-  const uint4* A = (dense ? sdn : edn + (size_t)e * e_stride) + (size_t)s0 * nkt * 64 + lane;
-  const bool once = n <= kGemmM;
+  const uint4* base = dense ? sdn : edn + (size_t)e * e_stride;
+  const uint4* Wt[1][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) Wt[0][j] = base + (size_t)(s0 + j) * nkt * 64 + lane;
   RowStage st;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int t = t0 + ((threadIdx.x + 256 * u) >> 4);
+    const int t = t0 + stage_row(u);
     const uint16_t* rowp = dense ? act_sh + (size_t)t * SI : act + (size_t)(o + t) * I;
-    st.src[u] = t < n ? rowp + 8 * ((threadIdx.x + 256 * u) & 15) : nullptr;
+    st.src[u] = t < n ? rowp + stage_col(u) : nullptr;
   }
-  st.load(0);
-  st.store(xs[0]);
-  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  f32x4_t acc[2][4];
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) acc[j][mt] = z4;
-  const int nch = K / kGemmKC;
-  for (int kc = 0; kc < nch; ++kc) {
-    const int buf = kc & 1;
-    uint4 a[4][2];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        a[ks][j] = ld_tile(A + (size_t)j * nkt * 64 + (size_t)(kc * 4 + ks) * 64, once);
-    if (kc + 1 < nch) st.load((kc + 1) * kGemmKC);
-    __syncthreads();
-    const uint16_t* xb = xs[buf] + i16 * kGemmLd + 8 * g;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      uint4 bx[4];
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) bx[mt] = *(const uint4*)(xb + mt * 16 * kGemmLd + 32 * ks);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) acc[j][mt] = mfma16(a[ks][j], bx[mt], acc[j][mt]);
-    }
-    if (kc + 1 < nch) st.store(xs[buf ^ 1]);
-  }
+  f32x4_t acc[1][2][4];
+  gemm_core<1, true>(Wt, K, n <= kGemmM, st, xs[0], xs[1], acc);
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
     const int t = t0 + mt * 16 + i16;
@@ -233,10 +286,217 @@ __global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H
     }
     float* dst = slot + ((size_t)row * (topk + 1) + sl) * H + 4 * g;
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      *(float4*)(dst + (s0 + j) * 16) =
-          make_float4(wt * acc[j][mt][0], wt * acc[j][mt][1], wt * acc[j][mt][2], wt * acc[j][mt][3]);
+    for (int j = 0; j < 2; ++j) {
+      const f32x4_t a = acc[0][j][mt];
+      *(float4*)(dst + (s0 + j) * 16) = make_float4(wt * a[0], wt * a[1], wt * a[2], wt * a[3]);
+    }
   }
+}
+
+// ---------------------------------------------------------------- dense
+// Dense products of the normalised rows X (bf16 [R][ldx]) with a packed
+// weight matrix, one epilogue per MODE:
+//   DG_SET / DG_ADD: Y[r][n] (=|+=) X[r] . W[n]        (Y float32, stride ldy)
+//   DG_SWIGLU: act[r][f] = silu(X[r] . G[f]) * (X[r] . U[f]) (bf16 [R][N]; W
+//              holds the N gate strips, then the N up strips)
+//   DG_QKV:    [q | k | v] = X . Wqkv^T, RoPE (rotate-half) on q and k,
+//              q -> q_out (float32 [R][D]), k and v -> the cache at the row
+//              position (valid rows); a block's 128 features lie in one of
+//              q, k, v, and wave w takes the strips of dims d and d + dh/2
+//              of one head, so the rotation pairs are in its registers.
+// With few tiles the K range is split over S blocks per tile (split sk
+// takes K chunks [sk*cps, (sk+1)*cps)): each writes its float32 partial
+// sums to part[sk][r][col] and k_dense_reduce adds the S partials in order
+// and applies the epilogue.  S = 1 applies it directly.
+enum { DG_SET = 0, DG_ADD = 1, DG_QKV = 2, DG_SWIGLU = 3 };
+struct DenseOut {
+  float* y;            // DG_SET / DG_ADD
+  int ldy;
+  uint16_t* act;       // DG_SWIGLU
+  int C, nh, dh, cap;  // DG_QKV: rows per sequence, heads, head size, cache capacity
+  size_t seq_stride;
+  const float2* rope;
+  const int32_t* row_pos;
+  const int32_t* row_valid;
+  uint16_t* cache;
+  float* q_out;
+};
+
+// Partial columns per row: 2N for DG_SWIGLU (gate, then up), else N
+template <int MODE>
+__host__ __device__ constexpr int dense_cols(int N) { return MODE == DG_SWIGLU ? 2 * N : N; }
+
+// Epilogue of row r at feature f (a multiple of 4): x0 = the sums of
+// features f..f+3; x1 = the up sums (DG_SWIGLU) or those of f + dh/2..
+// (DG_QKV, f in the first half of a head), else unused.
+template <int MODE>
+__device__ __forceinline__ void dense_out(const DenseOut& o, int N, int r, int f,
+                                          const float (&x0)[4], const float (&x1)[4]) {
+  if constexpr (MODE == DG_SET || MODE == DG_ADD) {
+    float* y = o.y + (size_t)r * o.ldy + f;
+    float4 v = make_float4(x0[0], x0[1], x0[2], x0[3]);
+    if (MODE == DG_ADD) {
+      const float4 y0 = ld_f4(y);
+      v.x += y0.x;
+      v.y += y0.y;
+      v.z += y0.z;
+      v.w += y0.w;
+    }
+    *(float4*)y = v;
+  } else if constexpr (MODE == DG_SWIGLU) {
+    *(uint2*)(o.act + (size_t)r * N + f) = pack4(silu(x0[0]) * x1[0], silu(x0[1]) * x1[1],
+                                                 silu(x0[2]) * x1[2], silu(x0[3]) * x1[3]);
+  } else {
+    const int D = o.nh * o.dh, half = o.dh / 2;
+    const int sec = f / D, fs = f - sec * D, hh = fs / o.dh, i = fs % o.dh;  // i < dh/2
+    const int valid = o.row_valid[r], pos = o.row_pos[r], b = r / o.C;
+    if (sec < 2) {
+      const float2* cs = o.rope + (size_t)(valid ? pos : 0) * half + i;
+      float y0[4], y1[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float2 c = cs[t];
+        y0[t] = x0[t] * c.x - x1[t] * c.y;
+        y1[t] = x1[t] * c.x + x0[t] * c.y;
+      }
+      if (sec == 0) {
+        float* qr = o.q_out + (size_t)r * D + hh * o.dh + i;
+        *(float4*)qr = make_float4(y0[0], y0[1], y0[2], y0[3]);
+        *(float4*)(qr + half) = make_float4(y1[0], y1[1], y1[2], y1[3]);
+      } else if (valid) {
+        uint16_t* kc = o.cache + (size_t)b * o.seq_stride + ((size_t)hh * o.cap + pos) * o.dh + i;
+        *(uint2*)kc = pack4(y0[0], y0[1], y0[2], y0[3]);
+        *(uint2*)(kc + half) = pack4(y1[0], y1[1], y1[2], y1[3]);
+      }
+    } else if (valid) {
+      uint16_t* vc =
+          o.cache + (size_t)b * o.seq_stride + ((size_t)(o.nh + hh) * o.cap + pos) * o.dh + i;
+      *(uint2*)vc = pack4(x0[0], x0[1], x0[2], x0[3]);
+      *(uint2*)(vc + half) = pack4(x1[0], x1[1], x1[2], x1[3]);
+    }
+  }
+}
+
+__device__ __forceinline__ void to4(const f32x4_t a, float (&x)[4]) {
+  x[0] = a[0];
+  x[1] = a[1];
+  x[2] = a[2];
+  x[3] = a[3];
+}
+
+// N output features (multiples of 128), K (multiple of 128); items = the
+// row chunks x N-blocks x S splits, chunk fastest, then split.
+template <int MODE>
+__global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
+                                                    const uint16_t* __restrict__ X, int ldx,
+                                                    const uint4* __restrict__ Wp, int S,
+                                                    float* __restrict__ part, DenseOut o) {
+  constexpr int NA = MODE == DG_SWIGLU ? 2 : 1;
+  __shared__ __align__(16) uint16_t xs[2][kGemmM * kGemmLd];
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int i16 = lane & 15, g = lane >> 4;
+  const int nz = (R + kGemmM - 1) / kGemmM, nbn = N / kGemmN;
+  const int L = xcd_item(blockIdx.x, nz * nbn * S);
+  if (L >= nz * nbn * S) return;
+  const int z = L % nz, sk = (L / nz) % S, nb = L / nz / S;
+  const int t0 = z * kGemmM, nkt = K / 32, nch = K / kGemmKC;
+  const int cps = (nch + S - 1) / S, kc0 = sk * cps, nkc = min(cps, nch - kc0);
+  // this wave's two strips: a rotate-half pair of one head (DG_QKV), else
+  // strips 2w, 2w + 1 of the block
+  int sa, sb;
+  if (MODE == DG_QKV) {
+    const int tph = o.dh / 32, ls = (w / tph) * 2 * tph + w % tph;
+    sa = nb * (kGemmN / 16) + ls;
+    sb = sa + tph;
+  } else {
+    sa = nb * (kGemmN / 16) + 2 * w;
+    sb = sa + 1;
+  }
+  const uint4* Wt[NA][2];
+#pragma unroll
+  for (int a = 0; a < NA; ++a) {
+    Wt[a][0] = Wp + ((size_t)(a * (N / 16) + sa) * nkt + kc0 * 4) * 64 + lane;
+    Wt[a][1] = Wp + ((size_t)(a * (N / 16) + sb) * nkt + kc0 * 4) * 64 + lane;
+  }
+  RowStage st;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int t = t0 + stage_row(u);
+    st.src[u] = t < R ? X + (size_t)t * ldx + kc0 * kGemmKC + stage_col(u) : nullptr;
+  }
+  f32x4_t acc[NA][2][4];
+  gemm_core<NA, NA == 1>(Wt, nkc * kGemmKC, nz == 1, st, xs[0], xs[1], acc);
+  const int fa = sa * 16 + 4 * g, fb = sb * 16 + 4 * g;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) {
+    const int r = t0 + mt * 16 + i16;
+    if (r >= R) continue;
+    if (S > 1) {  // float32 partials of this split
+      float* pr = part + ((size_t)sk * R + r) * dense_cols<MODE>(N);
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const f32x4_t v = acc[a][j][mt];
+          *(float4*)(pr + a * N + (j ? fb : fa)) = make_float4(v[0], v[1], v[2], v[3]);
+        }
+      continue;
+    }
+    float x0[4], x1[4];
+    if (MODE == DG_QKV) {
+      to4(acc[0][0][mt], x0);
+      to4(acc[0][1][mt], x1);
+      dense_out<MODE>(o, N, r, fa, x0, x1);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        to4(acc[0][j][mt], x0);
+        to4(acc[NA - 1][j][mt], x1);
+        dense_out<MODE>(o, N, r, j ? fb : fa, x0, x1);
+      }
+    }
+  }
+}
+
+// The S partials of k_dense_gemm summed in split order, then the
+// epilogue: one thread per (row, 4 features) -- for DG_QKV per (row, 4
+// dims of the first half of a head and their rotate-half partners).
+template <int MODE>
+__global__ void __launch_bounds__(256) k_dense_reduce(int R, int N, int S,
+                                                      const float* __restrict__ part,
+                                                      DenseOut o) {
+  const int upr = MODE == DG_QKV ? N / 8 : N / 4;  // units per row
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (size_t)R * upr) return;
+  const int r = (int)(idx / upr), u = (int)(idx % upr);
+  int f, f1;  // the x0 and x1 columns
+  if (MODE == DG_QKV) {
+    const int D = o.nh * o.dh, qg = o.dh / 8;  // 4-dim groups in half a head
+    const int sec = u / (D / 8), rem = u % (D / 8);
+    f = sec * D + (rem / qg) * o.dh + 4 * (rem % qg);
+    f1 = f + o.dh / 2;
+  } else {
+    f = 4 * u;
+    f1 = MODE == DG_SWIGLU ? N + f : f;
+  }
+  const size_t rs = (size_t)R * dense_cols<MODE>(N);  // floats per split
+  const float* p = part + (size_t)r * dense_cols<MODE>(N);
+  float x0[4] = {0.f, 0.f, 0.f, 0.f}, x1[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < S; ++s) {
+    const float4 a = ld_f4(p + s * rs + f);
+    x0[0] += a.x;
+    x0[1] += a.y;
+    x0[2] += a.z;
+    x0[3] += a.w;
+    if (MODE == DG_SWIGLU || MODE == DG_QKV) {
+      const float4 b = ld_f4(p + s * rs + f1);
+      x1[0] += b.x;
+      x1[1] += b.y;
+      x1[2] += b.z;
+      x1[3] += b.w;
+    }
+  }
+  dense_out<MODE>(o, N, r, f, x0, x1);
 }
 
 }  // namespace mtp

@@ -1048,144 +1048,50 @@ __global__ void __launch_bounds__(1024) k_s_router(int R, int H, int E, int topk
   }
 }
 
-// Compact MoE grids (more than 16 rows): cbp[y] (y <= E) is the number of
-// 16*cpb-entry chunk blocks of the experts before y (the shared experts are
-// y = E, with R entries), cbp[E+1] the total (written by k_group).  Chunk
-// block c lies in expert y = the last one with cbp[y] <= c; returns y and
-// z = c - cbp[y].  Every wave of the block computes it (no barrier).
-__device__ __forceinline__ int chunk_block_expert(int c, int E, const int32_t* __restrict__ cbp,
-                                                  int& z) {
-  const int lane = threadIdx.x & 63;
-  const int pv = lane < E ? cbp[lane] : 0x7fffffff;
-  const int pe = cbp[E];
-  int y = __popcll(__ballot(pv <= c)) - 1;
-  if (c >= pe) y = E;
-  z = c - (y == E ? pe : __shfl(pv, y, MTP_WAVE));
-  return y;
-}
-
-// ---------------------------------------------------------------- MoE gate/up
-// Block = (16-wide intermediate tile, expert y, cpb 16-entry chunks from
-// z*16*cpb): routed expert y < E over its entries (blocks past cnt[y] exit
-// after one load), or y == E: the dense SwiGLU over rows (the shared
-// experts as one width-SI SwiGLU, or the draft FFN).  The weight tiles are
-// loaded once and applied to the block's chunks in turn.  K split over 4 waves; weight tiles
-// are loaded first.  With g != NULL the B rows are RMSNorm(h; g) computed
-// into LDS (dense mode), else the bf16 rows xg.  ROLE only names the
-// instance (so profiles separate decode from prefill launches); the draft
-// roles are the dense-only form (the draft block's FFN, launched with E = 0).
+// ---------------------------------------------------------------- draft FFN gate/up
+// The draft block's FFN gate/up + SwiGLU for up to 16 rows: block = one
+// 16-wide intermediate tile (blockIdx.x) of the width-F SwiGLU sgu (gate
+// strips, then up strips), K split over 4 waves.  Each wave's first row is
+// loaded ahead of the weight tiles and normalised while they are in
+// flight; the block then computes RMSNorm(h; g) of its rows into LDS.
+// ROLE only names the instance (so profiles separate decode from prefill
+// launches; GU_VERIFY / GU_PREFILL name the MoE gate/up of many rows).
 enum { GU_VERIFY = 0, GU_DRAFT = 1, GU_PREFILL = 2, GU_DRAFT_PREFILL = 3 };
-template <int ROLE, int MAXT, bool EARLY = false>
-__global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int I, int SI,
-                                              const uint16_t* __restrict__ xg,
-                                              const float* __restrict__ h,
+template <int ROLE, int MAXT>
+__global__ void __launch_bounds__(256) k_s_gu(int R, int H, int F, const float* __restrict__ h,
                                               const float* __restrict__ g, float eps,
-                                              const uint4* __restrict__ egu, size_t e_stride,
                                               const uint4* __restrict__ sgu,
-                                              const int32_t* __restrict__ cnt,
-                                              const int32_t* __restrict__ off,
-                                              const int32_t* __restrict__ ent_row,
-                                              uint16_t* __restrict__ act,
-                                              uint16_t* __restrict__ act_sh,
-                                              const int32_t* __restrict__ cbp) {
+                                              uint16_t* __restrict__ act_sh) {
   extern __shared__ __align__(16) uint16_t xs[];
   __shared__ f32x4_t red[2 * 4 * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int it = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
-  if (cbp) {  // compact grid (1-D): I/16 tiles per routed chunk block, SI/16 per shared one
-    const int nI = I / 16, nr = cbp[E] * nI, b = blockIdx.x;
-    int z;
-    if (b < nr) {
-      e = chunk_block_expert(b / nI, E, cbp, z);
-      it = b % nI;
-    } else {
-      e = E;
-      it = (b - nr) % (SI / 16);
-      z = (b - nr) / (SI / 16);
-      if (cbp[E] + z >= cbp[E + 1]) return;  // past the shared chunk blocks
-    }
-    tb = z * 16 * cpb;
-  }
-  const bool dense = (ROLE & 1) || e == E;
-  const int width = dense ? SI : I;
-  if (it * 16 >= width) return;
-  int n = R, o = 0;
-  if (!dense) {
-    n = cnt[e];
-    o = off[e];
-  }
-  if (tb >= n) return;
-  const int nkt = H / 32, per = nkt / 4, ldl = H + XPAD;
-  const uint4 *G, *U;
-  if (dense) {
-    G = sgu + (size_t)it * nkt * 64;
-    U = sgu + (size_t)(SI / 16 + it) * nkt * 64;
-  } else {
-    const uint4* base = egu + (size_t)e * e_stride;
-    G = base + (size_t)it * nkt * 64;
-    U = base + (size_t)(I / 16 + it) * nkt * 64;
-  }
+  const int it = blockIdx.x, nkt = H / 32, per = nkt / 4, ldl = H + XPAD;
+  const uint4* G = sgu + (size_t)it * nkt * 64;
+  const uint4* U = sgu + (size_t)(F / 16 + it) * nkt * 64;
   constexpr int NV = MTP_NV(MAXT);
-  // EARLY (draft roles, prologue mode, one chunk): each wave's first row is
-  // loaded ahead of the weight tiles and normalised while they are in flight
   NormRow<NV> nr0;
-  const bool early = EARLY && (ROLE & 1) != 0 && g && cpb == 1 && w < min(16, n - tb);
-  if (early) norm_row_load<NV>(H, h + (size_t)(tb + w) * H, g, nr0);
+  const bool early = w < R;
+  if (early) norm_row_load<NV>(H, h + (size_t)w * H, g, nr0);
   uint4 ag_[MAXT], au_[MAXT];
-  const bool once = n <= 16 * cpb;  // the expert's tiles are read by this block only
-  preload<MAXT>(G, w * per, per, ag_, once);
-  preload<MAXT>(U, w * per, per, au_, once);
-  if (cpb == 1) {  // one chunk (with the RMSNorm prologue when g != NULL)
-    const int t0 = tb, t = t0 + (lane & 15);  // entry (routed) or row (dense)
-    const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-    f32x4_t cg = z4, cu = z4;
-    if ((ROLE & 1) != 0 && g) {  // draft roles, few rows: RMSNorm(h; g) prologue
-      if (early) norm_row_store<NV>(H, eps, nr0, xs + w * ldl);
-      norm_rows_lds<NV>(min(16, n - t0), H, h + (size_t)t0 * H, g, eps, xs, ldl, EARLY);
-      __syncthreads();
-      // B rows in LDS (lanes past n read a tile row; their columns are not stored)
-      mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per,
-                                                         xs + (lane & 15) * ldl, cg, cu);
-    } else {
-      const uint16_t* xrow = t < n ? xg + (size_t)(dense ? t : ent_row[o + t]) * H : nullptr;
-      mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
-    }
-    cg = block_acc_sum<4>(cg, red);
-    cu = block_acc_sum<4>(cu, red + 4 * 64);
-    if (w != 0 || t >= n) return;
-    const int i = it * 16 + 4 * (lane >> 4);
-    uint2 pk;
-    pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
-    pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
-    if (dense)
-      *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
-    else
-      *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
-    return;
-  }
-  // several chunks (bf16 rows xg): weight tiles kept in registers
-  for (int c = 0; c < cpb; ++c) {
-    const int t0 = tb + 16 * c;
-    if (t0 >= n) break;  // block-uniform
-    if (c > 0) __syncthreads();  // red of the previous chunk is consumed
-    const int t = t0 + (lane & 15);
-    const uint16_t* xrow = t < n ? xg + (size_t)(dense ? t : ent_row[o + t]) * H : nullptr;
-    const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-    f32x4_t cg = z4, cu = z4;
-    mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per, xrow, cg, cu);
-    cg = block_acc_sum<4>(cg, red);
-    cu = block_acc_sum<4>(cu, red + 4 * 64);
-    if (w == 0 && t < n) {
-      const int i = it * 16 + 4 * (lane >> 4);
-      uint2 pk;
-      pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
-      pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
-      if (dense)
-        *(uint2*)(act_sh + (size_t)t * SI + i) = pk;
-      else
-        *(uint2*)(act + (size_t)(o + t) * I + i) = pk;
-    }
-  }
+  preload<MAXT>(G, w * per, per, ag_, true);
+  preload<MAXT>(U, w * per, per, au_, true);
+  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t cg = z4, cu = z4;
+  if (early) norm_row_store<NV>(H, eps, nr0, xs + w * ldl);
+  norm_rows_lds<NV>(R, H, h, g, eps, xs, ldl, true);
+  __syncthreads();
+  // B rows in LDS (lanes past R read a tile row; their columns are not stored)
+  mma_pre2<MAXT, (MAXT % 2 == 0 ? MAXT / 2 : MAXT)>(ag_, au_, w * per, per,
+                                                     xs + (lane & 15) * ldl, cg, cu);
+  cg = block_acc_sum<4>(cg, red);
+  cu = block_acc_sum<4>(cu, red + 4 * 64);
+  const int t = lane & 15;
+  if (w != 0 || t >= R) return;
+  const int i = it * 16 + 4 * (lane >> 4);
+  uint2 pk;
+  pk.x = (uint32_t)f2bf(silu(cg[0]) * cu[0]) | ((uint32_t)f2bf(silu(cg[1]) * cu[1]) << 16);
+  pk.y = (uint32_t)f2bf(silu(cg[2]) * cu[2]) | ((uint32_t)f2bf(silu(cg[3]) * cu[3]) << 16);
+  *(uint2*)(act_sh + (size_t)t * F + i) = pk;
 }
 
 // MoE gate/up for up to 16 rows, persistent streaming form.  Work items:
@@ -1197,7 +1103,7 @@ __global__ void __launch_bounds__(256) k_s_gu(int cpb, int R, int H, int E, int 
 // item's loads are in flight during this item's reduction and store (with
 // one block per item, blocks that do not fit on the machine at once start
 // only when a resident block has finished, after its loads have drained).
-// Sums are taken in the same order as k_s_gu's one-chunk path.
+// Sums are taken in the same order as k_s_gu's.
 template <int MAXT>
 __global__ void __launch_bounds__(256) k_s_gu_stream(int R, int H, int I, int SI,
                                                      const uint16_t* __restrict__ xg,
@@ -1420,108 +1326,14 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
   }
 }
 
-// ---------------------------------------------------------------- MoE down (slots)
-// More than 16 rows: block = (16 output features, expert y, cpb 16-entry
-// chunks from z*16*cpb), K split over 4 waves.  A routed expert's wave tiles
-// (I/128 <= MAXT) are loaded once and applied to the block's chunks in
-// turn; the shared block (K = SI) streams its tiles per chunk (the shared
-// weights stay in L2), so the registers are sized for one expert's K.
-// Routed y < E: slot[(row*(k+1) + slot)][n] = w * (Wd_y[n] . act_t);
-// y == E: slot[(r*(k+1) + k)][n] = Wsd[n] . act_sh[r] (the shared experts
-// as one width-SI SwiGLU).  k_combine_norm then adds the k+1 slots of
-// each row to h in a fixed order.
-template <int MAXT>
-__global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int topk, int H,
-                                                     int I, int SI,
-                                                     const uint16_t* __restrict__ act,
-                                                     const uint16_t* __restrict__ act_sh,
-                                                     const uint4* __restrict__ edn,
-                                                     size_t e_stride,
-                                                     const uint4* __restrict__ sdn,
-                                                     const int32_t* __restrict__ cnt,
-                                                     const int32_t* __restrict__ off,
-                                                     const int32_t* __restrict__ ent_row,
-                                                     const int32_t* __restrict__ ent_slot,
-                                                     const float* __restrict__ ent_w,
-                                                     float* __restrict__ slot) {
-  __shared__ f32x4_t red[4 * 64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int nt = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
-  const bool dense = e == E;
-  int n = R, o = 0;
-  if (!dense) {
-    n = cnt[e];
-    o = off[e];
-  }
-  if (tb >= n) return;
-  const int K = dense ? SI : I, nkt = K / 32, per = nkt / 4;
-  const uint4* A = dense ? sdn + (size_t)nt * nkt * 64
-                         : edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
-  // Chunk c's rows: entries tb + 16c + (lane & 15).
-  auto chunk_rows = [&](int c, const uint16_t*& xrow, int& row, int& sl, float& wt) {
-    const int t = tb + 16 * c + (lane & 15);
-    xrow = nullptr;
-    row = 0;
-    sl = topk;
-    wt = 1.f;
-    if (t < n) {
-      if (dense) {
-        xrow = act_sh + (size_t)t * SI;
-        row = t;
-      } else {
-        xrow = act + (size_t)(o + t) * I;
-        row = ent_row[o + t];
-        sl = ent_slot[o + t];
-        wt = ent_w[o + t];
-      }
-    }
-  };
-  auto store = [&](int c, f32x4_t acc, int row, int sl, float wt) {
-    const int t = tb + 16 * c + (lane & 15);
-    if (w == 0 && t < n) {
-      float4* dst =
-          (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
-      *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
-    }
-  };
-  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
-  if (dense) {  // the shared block streams its tiles per chunk (double-buffered)
-    for (int c = 0; c < cpb; ++c) {
-      if (tb + 16 * c >= n) break;  // block-uniform
-      if (c > 0) __syncthreads();
-      const uint16_t* xrow;
-      int row, sl;
-      float wt;
-      chunk_rows(c, xrow, row, sl, wt);
-      f32x4_t acc = sk_range<4>(A, w * per, (w + 1) * per, xrow, z4, n <= 16 * cpb);
-      acc = block_acc_sum<4>(acc, red);
-      store(c, acc, row, sl, wt);
-    }
-    return;
-  }
-  // a routed expert's wave tiles (I/128 <= MAXT) stay in registers; each
-  // chunk's B operands are all loaded before its products
-  uint4 a[MAXT];
-  preload<MAXT>(A, w * per, per, a, n <= 16 * cpb);  // read by this block only
-  for (int c = 0; c < cpb; ++c) {
-    if (tb + 16 * c >= n) break;  // block-uniform
-    if (c > 0) __syncthreads();
-    const uint16_t* xrow;
-    int row, sl;
-    float wt;
-    chunk_rows(c, xrow, row, sl, wt);
-    f32x4_t acc = mma_pre<MAXT>(a, w * per, per, xrow, z4);
-    acc = block_acc_sum<4>(acc, red);
-    store(c, acc, row, sl, wt);
-  }
-}
-
 // Grouping of (row, slot) pairs by expert for any number of rows: counts,
 // offsets (ascending expert id), one entry per pair, and the chunk-block
-// prefix cbp of the compact MoE grids (chunks of 16*cpb entries).  Entries of one
-// expert are placed through LDS atomics, so their order inside the expert
-// varies between runs; every value computed from them does not (an entry's
-// row and slot travel with it and the MFMA columns are independent).
+// prefix cbp of the grouped GEMMs' work items (chunks of 16*cpb entries;
+// cbp[E + 1] adds the chunks of the R rows through the shared experts).
+// Entries of one expert are placed through LDS atomics, so their order
+// inside the expert varies between runs; every value computed from them
+// does not (an entry's row and slot travel with it and the MFMA columns
+// are independent).
 __global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
                                                 const int32_t* __restrict__ ridx,
                                                 const float* __restrict__ rw,

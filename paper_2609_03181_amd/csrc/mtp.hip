@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -145,7 +146,8 @@ struct Ws {
   // bf16 fast path
   float *part, *slot, *ent_w;
   int32_t *cnt, *off, *ent_row, *ent_slot, *touched, *n_touched, *att_ctr, *dn_ctr;
-  int32_t* cbp;  // chunk-block prefix of the compact MoE grids [E + 2]
+  int32_t* cbp;  // chunk-block prefix of the grouped MoE GEMMs' items [E + 2]
+  float* gpart;  // K-split partials of the dense tiled products (more than 16 rows)
   unsigned long long* dn_part;  // MoE down split partials [kDownSplit][R][H], fixed point (R <= 16)
   float* lg;                    // router logits of the fused MoE [R][E] (R <= 16)
   int32_t* moe_sync;            // fused MoE: kMoeSyncWords per layer (inside the zeroed counters)
@@ -153,6 +155,37 @@ struct Ws {
   int n_ctr;  // entries of att_ctr (zeroed at the start of each call)
   size_t bytes;
 };
+
+// K splits of a dense tiled product of R rows, N outputs and K inputs: with
+// few tiles (64-row chunks x 128-wide N-blocks) the K range is split so that
+// about 384 blocks run, with at least two K chunks per split; 1 with 256
+// tiles or more.
+inline int dense_splits(int R, int N, int K) {
+  const int tiles = ((R + kGemmM - 1) / kGemmM) * (N / kGemmN), nch = K / kGemmKC;
+  if (tiles >= 256 || nch < 4) return 1;
+  const int want = (384 + tiles - 1) / tiles;
+  const int cps = std::max(2, (nch + want - 1) / want);
+  return (nch + cps - 1) / cps;
+}
+
+// Floats of the K-split partials of the dense products (QKV, O, eh, draft
+// FFN gate/up and down) of any pass of 17..R rows: S * rows * columns, the
+// largest over the products; within a 64-row chunk count S is fixed, so
+// the chunk's last row count is the largest.
+inline size_t dense_part_floats(const mtp_config& c, size_t R) {
+  if (c.dtype != MTP_BF16) return 0;
+  const int H = c.hidden, D = c.n_heads * c.head_dim, F = c.draft_inter;
+  const int shape[5][3] = {{3 * D, H, 3 * D}, {H, D, H}, {H, 2 * H, H}, {H, F, H}, {F, H, 2 * F}};
+  size_t best = 0;
+  for (size_t r0 = SR_MAX; r0 < R; r0 = (r0 / kGemmM + 1) * kGemmM) {
+    const size_t r = std::min(R, (r0 / kGemmM + 1) * kGemmM);
+    for (const auto& sh : shape) {
+      const int S = dense_splits((int)r, sh[0], sh[1]);
+      if (S > 1) best = std::max(best, (size_t)S * r * sh[2]);
+    }
+  }
+  return best;
+}
 
 Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
   const size_t R = (size_t)B * C;
@@ -234,6 +267,8 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     if (fused_rows && (size_t)SI * 16 * 2 > sh_bytes) sh_bytes = (size_t)SI * 16 * 2;
     w.act_sh = (uint16_t*)take(sh_bytes);
     w.lg = (float*)take((size_t)R16 * c.n_routed * 4);
+    const size_t gp = dense_part_floats(c, R);
+    w.gpart = gp ? (float*)take(gp * 4) : nullptr;
   } else {
     w.part = w.slot = w.ent_w = nullptr;
     w.cnt = w.off = w.ent_row = w.ent_slot = w.touched = w.n_touched = w.att_ctr = nullptr;
@@ -241,6 +276,7 @@ Ws carve(const mtp_config& c, int B, int C, void* base, int n_split) {
     w.act_sh = nullptr;
     w.lg = nullptr;
     w.moe_sync = nullptr;
+    w.gpart = nullptr;
   }
   w.bytes = off;
   return w;
@@ -404,11 +440,35 @@ struct Model {
     return 4;
   }
   static unsigned groups(int R) { return (unsigned)((R + 15) / 16); }
+  // grid of an XCD-ordered tiled launch for at most `items` work items
+  static unsigned grid_xcd(size_t items) { return (unsigned)(cdiv(items, kXcd) * kXcd); }
   static size_t lds_rows(int R, int H) { return (size_t)(R < 16 ? R : 16) * (H + XPAD) * 2; }
 
   // Y (=|+=) X . W^T over R rows (16-row groups)
-  void smm(int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp, float* Y, int ldy,
-           bool add) {
+  // Dense tiled product of R > 16 rows (kernels_gemm.h), K split over
+  // blocks when there are few tiles (then a reduce launch adds the splits)
+  template <int MODE>
+  void dense(const Ws& ws, int kc, int R, int N, int K, const uint16_t* X, int ldx,
+             const uint4* Wp, const DenseOut& o) {
+    const int S = dense_splits(R, N, K);
+    launch_k(tm, kc, k_dense_gemm<MODE>, dim3(grid_xcd((size_t)cdiv(R, kGemmM) * (N / kGemmN) * S)),
+             dim3(256), 0, s, R, N, K, X, ldx, Wp, S, ws.gpart, o);
+    if (S > 1)
+      launch_k(tm, kc, k_dense_reduce<MODE>,
+               dim3(cdiv((size_t)R * (MODE == DG_QKV ? N / 8 : N / 4), 256)), dim3(256), 0, s, R, N,
+               S, (const float*)ws.gpart, o);
+  }
+
+  void smm(const Ws& ws, int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp,
+           float* Y, int ldy, bool add) {
+    if (R > SR_MAX && N % kGemmN == 0 && K % kGemmKC == 0) {  // tiled GEMM, rows in LDS
+      DenseOut o{};
+      o.y = Y;
+      o.ldy = ldy;
+      if (add) dense<DG_ADD>(ws, 0, R, N, K, X, ldx_, Wp, o);
+      else dense<DG_SET>(ws, 0, R, N, K, X, ldx_, Wp, o);
+      return;
+    }
     const int nkt = K / 32, nw = nw_for(nkt), per = nkt / nw;
     const dim3 g(cdiv(N, 16), groups(R));
 #define MTP_SMM_T(NW, M)                                                                   \
@@ -475,16 +535,31 @@ struct Model {
   void attn_mfma(const Ws& ws, int B, int C, const float* g, const uint16_t* xg,
                  const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
+    if (xg && R > SR_MAX) {  // tiled GEMM over the normalised rows
+      DenseOut o{};
+      o.C = C;
+      o.nh = nh;
+      o.dh = dh;
+      o.cap = c.max_ctx;
+      o.seq_stride = seq_stride;
+      o.rope = rope;
+      o.row_pos = ws.row_pos;
+      o.row_valid = ws.row_valid;
+      o.cache = cache;
+      o.q_out = ws.q;
+      dense<DG_QKV>(ws, MTP_KC_QKV, R, 3 * D, H, xg, H, wqkv, o);
+    } else {
 #define MTP_QKV(M)                                                                          \
   launch_k(tm, MTP_KC_QKV, (!xg && groups(R) == 1) ? k_s_qkv<M, true> : k_s_qkv<M, false>,   \
            dim3(D / 8, groups(R)), dim3(256),                                                 \
            xg ? 0 : lds_rows(R, H), s, R, C, H, nh, dh, ws.h, g, (float)c.rms_eps, xg, wqkv, \
            rope, ws.row_pos, ws.row_valid, cache, seq_stride, c.max_ctx, ws.q)
-    MTP_MAXT_DISPATCH(H / 128, MTP_QKV);
+      MTP_MAXT_DISPATCH(H / 128, MTP_QKV);
 #undef MTP_QKV
+    }
     if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
     else sattn<64>(ws, B, C, cache, seq_stride);
-    smm(R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
+    smm(ws, R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
   }
 
   // LM head over nr rows of ws.xhead (bf16, normalised), greedy argmax
@@ -603,8 +678,8 @@ struct Model {
         MTP_MAXT_DISPATCH(H / 128, MTP_GU);
 #undef MTP_GU
       } else {  // grouped GEMM on the compact grid (blocks past the last item exit)
-        const unsigned nblk = (unsigned)(E + cdiv((size_t)R * k, kGemmM)) * (I / kGemmN) +
-                              cdiv(R, kGemmM) * (SI / kGemmN);
+        const unsigned nblk = grid_xcd((E + cdiv((size_t)R * k, kGemmM)) * (I / kGemmN) +
+                                       cdiv(R, kGemmM) * (SI / kGemmN));
         launch_k(tm, MTP_KC_MOE_GU, prefill ? k_gu_gemm<GU_PREFILL> : k_gu_gemm<GU_VERIFY>,
                  dim3(nblk), dim3(256), 0, s, R, H, E, I, SI, (const uint16_t*)ws.xin,
                  pk.exp_gu + (size_t)l * E * pk.exp_gu_s, pk.exp_gu_s,
@@ -619,7 +694,7 @@ struct Model {
                  pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.touched,
                  ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h, ws.status);
       else
-        launch_k(tm, MTP_KC_MOE_DOWN, k_down_gemm, dim3(chunks * (H / kGemmN)), dim3(256), 0, s,
+        launch_k(tm, MTP_KC_MOE_DOWN, k_down_gemm, dim3(grid_xcd(chunks * (H / kGemmN))), dim3(256), 0, s,
                  R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn,
                  ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot, ws.cbp);
     }
@@ -665,7 +740,7 @@ struct Model {
       k_draft_in<BF><<<R, 256, 2 * H * sizeof(float), s>>>(
           C, H, c.vocab, ws.row_valid, ws.row_tok, (const T*)w.embed, vision, vis_ld, vis_off, a,
           a_ld, w.d_enorm, w.d_hnorm, eps, (T*)ws.xin, ws.status);
-    smm(R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
+    smm(ws, R, H, 2 * H, (const uint16_t*)ws.xin, 2 * H, pk.d_eh, ws.h, H, false);
     // Up to 16 rows the products normalise their rows in a prologue; with
     // several row groups the rows are normalised once (bf16, into xin) and
     // the products read them, each weight tile applied to cpb groups.
@@ -675,17 +750,19 @@ struct Model {
     if (pre) norm_rows(R, ws.h, nullptr, w.d_attn_norm, nullptr, (uint16_t*)ws.xin);
     attn_mfma(ws, B, C, w.d_attn_norm, xn, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
     if (pre) norm_rows(R, ws.h, nullptr, w.d_ffn_norm, nullptr, (uint16_t*)ws.xin);
-    const int cpb = G >= 8 ? 4 : 1;
-#define MTP_DFFN(M)                                                                           \
-  launch_k(tm, MTP_KC_DRAFT_FFN,                                                              \
-           prefill ? (pre ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT_PREFILL, M, true>)  \
-                   : (pre ? k_s_gu<GU_DRAFT, M> : k_s_gu<GU_DRAFT, M, true>),                 \
-           dim3(F / 16, 1, cdiv(G, cpb)), dim3(256), pre ? 0 : lds_rows(R, H), s, cpb, R, H, 0, \
-           F, F, xn, pre ? nullptr : ws.h, pre ? nullptr : w.d_ffn_norm, eps, nullptr, 0,       \
-           pk.d_gu, nullptr, nullptr, nullptr, nullptr, ws.act_sh, (const int32_t*)nullptr)
-    MTP_MAXT_DISPATCH(H / 128, MTP_DFFN);
+    if (pre) {  // tiled GEMM over the normalised rows
+      DenseOut o{};
+      o.act = ws.act_sh;
+      dense<DG_SWIGLU>(ws, MTP_KC_DRAFT_FFN, R, F, H, xn, H, pk.d_gu, o);
+    } else {
+#define MTP_DFFN(M)                                                                             \
+  launch_k(tm, MTP_KC_DRAFT_FFN, prefill ? k_s_gu<GU_DRAFT_PREFILL, M> : k_s_gu<GU_DRAFT, M>,   \
+           dim3(F / 16), dim3(256), lds_rows(R, H), s, R, H, F, ws.h, w.d_ffn_norm, eps, pk.d_gu, \
+           ws.act_sh)
+      MTP_MAXT_DISPATCH(H / 128, MTP_DFFN);
 #undef MTP_DFFN
-    smm(R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
+    }
+    smm(ws, R, H, F, ws.act_sh, F, pk.d_down, ws.h, H, true);
     if (!head) return;
     norm_rows(B, ws.h, ws.head_row, w.final_norm, ws.ustate, (uint16_t*)ws.xhead);
     lm_mfma(ws, B, logits, ldl, 1, ostride, ooff, tok, nullptr, defer_argmax);
