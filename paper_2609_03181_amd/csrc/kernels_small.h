@@ -516,7 +516,8 @@ __device__ __forceinline__ void attn_merge_row(const float* __restrict__ pp, int
 // coalesced 16-byte loads (the next tile's loads are issued before the
 // current tile is used) into LDS; wave w owns rows w, w+4: lane = key for
 // the scores, lane = 2 (or 1) dims for P.V.  Float32 scores and softmax.
-// The last block of a (z, head) merges all splits and writes bf16.
+// The last block of a (z, head) merges the splits that hold keys and writes
+// bf16.
 template <int DH, int NR>
 __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int spl,
                                                 const float* __restrict__ q,
@@ -559,6 +560,13 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
         if (i == wv + 4 * x) lim[x] = li;
     }
   }
+  // Splits past the group's last key hold no keys: only splits
+  // 0..n_live-1 take part (split 0 always, so a group of invalid rows still
+  // writes its zero rows).  An empty split's partial (m = -inf, l = 0,
+  // o = 0) has zero weight in the merge, so merging the n_live others gives
+  // the all-split merge's values bit for bit, with fewer partials to read.
+  const int n_live = max(1, min(n_split, (maxpos + spl) / spl));
+  if (s >= n_live) return;
   const int k0 = s * spl, k1 = min(k0 + spl, maxpos + 1);
   const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
   const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
@@ -668,7 +676,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
   int32_t* ctr = counters + (size_t)blockIdx.z * nh + h;
   if (threadIdx.x == 0)
     last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-           n_split - 1;
+           n_live - 1;
   __syncthreads();
   if (!last) return;
   if (threadIdx.x == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -678,7 +686,7 @@ __global__ void __launch_bounds__(256) k_s_attn(int C, int nh, int n_split, int 
     const int i = wv + 4 * x;
     if (i >= nr) break;
     const int r = b * C + i0 + i;
-    attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_split * (DH + 2), n_split,
+    attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_split * (DH + 2), n_live,
                        row_valid[r] != 0, ps[wv], out + (size_t)r * D + h * DH);
   }
 }
@@ -781,6 +789,13 @@ k_s_attn4(int C, int nh, int n_split, int spl, const float* __restrict__ q,
   int lim[4];
   attn4_seg_rows(z, h, C, ngroups, D, q, row_pos, row_valid, q0, q1, lim);
   const int maxpos = max(max(lim[0], lim[1]), max(lim[2], lim[3]));
+  // Splits past the group's last key hold no keys: only splits
+  // 0..n_live-1 take part (split 0 always, so a group of invalid rows still
+  // writes its zero rows).  An empty split's partial (m = -inf, l = 0,
+  // o = 0) has zero weight in the merge, so merging the n_live others gives
+  // the all-split merge's values bit for bit, with fewer partials to read.
+  const int n_live = max(1, min(n_split, (maxpos + spl) / spl));
+  if (s >= n_live) return;
   const int k0 = s * spl, k1 = min(k0 + spl, maxpos + 1);
   const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
   const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
@@ -919,13 +934,13 @@ k_s_attn4(int C, int nh, int n_split, int spl, const float* __restrict__ q,
   int32_t* ctr = counters + (size_t)z * nh + h;
   if (threadIdx.x == 0)
     last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-           n_split - 1;
+           n_live - 1;
   __syncthreads();
   if (!last) return;
   if (threadIdx.x == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (wv < nr) {
     const int r = b * C + i0 + wv;
-    attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_split * (DH + 2), n_split,
+    attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_split * (DH + 2), n_live,
                        row_valid[r] != 0, ps[wv], out + (size_t)r * D + h * DH);
   }
 }
