@@ -105,6 +105,8 @@ def class_kernel(kc, B, K):
         return "mtp::k_dense_gemm<2>"
     if kc == 7 and B > 16:
         return "mtp::k_dense_gemm<3>"
+    if kc == 4 and rows > 48:
+        return "mtp::k_dense_gemm<4>"
     return KERNEL_CLASSES[kc][1]
 
 
@@ -796,7 +798,7 @@ def run_workload(name, args, cpu=False):
                                "counters": {k.split("(")[0]: v for k, v in
                                             (_mfma_counters(name) or {}).items()
                                             if k.startswith(("mtp::k_gu_gemm<0>", "mtp::k_down_gemm",
-                                                             "mtp::k_lm_gemm"))} or None}
+                                                             "mtp::k_dense_gemm<4>"))} or None}
     if pages:
         rec["config"]["pages_per_s"] = round(B / dt, 4)
         rec["config"]["new_tokens_per_page"] = wl["new"]

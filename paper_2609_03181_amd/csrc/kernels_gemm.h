@@ -5,7 +5,9 @@
 // with an optional K split over blocks when there are few tiles.
 //
 // Block = 4 waves = 128 output features (wave w: two 16-wide strips) x 64
-// rows (four MFMA row tiles).  The rows are staged through LDS in K chunks
+// rows (four MFMA row tiles; the core and the dense kernel take the number
+// of row tiles MT as a parameter, 4 in every launch: eight row tiles per
+// wave leave one wave per SIMD, which measured slower for the LM head).  The rows are staged through LDS in K chunks
 // of 128 columns, double-buffered; each wave loads its own weight tiles
 // (the packed operand tiles of kernels_mfma.h) straight from memory, one K
 // chunk ahead of its products, so a chunk's weight loads fly during the
@@ -69,18 +71,19 @@ __device__ __forceinline__ bool gemm_item(int b, int E, int nbr, int nbs,
   return true;
 }
 
-// The 64 rows x 128 columns of one K chunk: thread piece u (of 4) is row
-// (tid + 256u) / 16, 8 columns at 8 * ((tid + 256u) % 16).
+// The 16*MT rows x 128 columns of one K chunk: thread piece u (of MT) is
+// row (tid + 256u) / 16, 8 columns at 8 * ((tid + 256u) % 16).
+template <int MT = 4>
 struct RowStage {
-  const uint16_t* src[4];  // the piece's row at column 0 (NULL: a row past the entries)
-  uint4 v[4];
+  const uint16_t* src[MT];  // the piece's row at column 0 (NULL: a row past the entries)
+  uint4 v[MT];
   __device__ __forceinline__ void load(int k0) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = src[u] ? *(const uint4*)(src[u] + k0) : make_uint4(0, 0, 0, 0);
+    for (int u = 0; u < MT; ++u) v[u] = src[u] ? *(const uint4*)(src[u] + k0) : make_uint4(0, 0, 0, 0);
   }
   __device__ __forceinline__ void store(uint16_t* xs) const {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < MT; ++u) {
       const int p = threadIdx.x + 256 * u;
       *(uint4*)(xs + (p >> 4) * kGemmLd + 8 * (p & 15)) = v[u];
     }
@@ -92,16 +95,16 @@ __device__ __forceinline__ int stage_row(int u) { return (threadIdx.x + 256 * u)
 __device__ __forceinline__ int stage_col(int u) { return 8 * ((threadIdx.x + 256 * u) & 15); }
 
 // acc[a][j][mt] = sum over K of matrix a's strip j (tile stream Wt[a][j],
-// lane offset included) times row tile mt of the staged rows.  K is a
+// lane offset included) times row tile mt (of MT) of the staged rows.  K is a
 // multiple of kGemmKC; st.src is set; xs0 / xs1 are the two LDS stages.
 // PF: the weight tiles of chunk kc + 1 are loaded during chunk kc's
 // products (two register sets); else each chunk's tiles are loaded at its
 // start (one set: with two matrices, two waves per SIMD fit instead of one,
 // and the other wave covers the load latency).
-template <int NA, bool PF>
+template <int NA, bool PF, int MT = 4>
 __device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K, bool once,
-                                          RowStage& st, uint16_t* xs0, uint16_t* xs1,
-                                          f32x4_t (&acc)[NA][2][4]) {
+                                          RowStage<MT>& st, uint16_t* xs0, uint16_t* xs1,
+                                          f32x4_t (&acc)[NA][2][MT]) {
   const int lane = threadIdx.x & 63, i16 = lane & 15, g = lane >> 4;
   const int nch = K / kGemmKC;
 #pragma unroll
@@ -109,7 +112,7 @@ __device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[a][j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   uint4 wa[NA][4][2];
   auto load_w = [&](uint4 (&wt)[NA][4][2], int kc) {
 #pragma unroll
@@ -123,15 +126,15 @@ __device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K
     const uint16_t* xb = xs + i16 * kGemmLd + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      uint4 bx[4];
+      uint4 bx[MT];
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) bx[mt] = *(const uint4*)(xb + mt * 16 * kGemmLd + 32 * ks);
+      for (int mt = 0; mt < MT; ++mt) bx[mt] = *(const uint4*)(xb + mt * 16 * kGemmLd + 32 * ks);
 #pragma unroll
       for (int a = 0; a < NA; ++a)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int mt = 0; mt < 4; ++mt) acc[a][j][mt] = mfma16(wt[a][ks][j], bx[mt], acc[a][j][mt]);
+          for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = mfma16(wt[a][ks][j], bx[mt], acc[a][j][mt]);
     }
   };
   st.load(0);
@@ -209,7 +212,7 @@ __global__ void __launch_bounds__(256) k_gu_gemm(int R, int H, int E, int I, int
     Wt[0][j] = base + (size_t)(s0 + j) * nkt * 64 + lane;       // gate
     Wt[1][j] = base + (size_t)(ns + s0 + j) * nkt * 64 + lane;  // up
   }
-  RowStage st;
+  RowStage<4> st;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int t = t0 + stage_row(u);
@@ -264,7 +267,7 @@ __global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H
   const uint4* Wt[1][2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) Wt[0][j] = base + (size_t)(s0 + j) * nkt * 64 + lane;
-  RowStage st;
+  RowStage<4> st;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int t = t0 + stage_row(u);
@@ -304,11 +307,17 @@ __global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H
 //              position (valid rows); a block's 128 features lie in one of
 //              q, k, v, and wave w takes the strips of dims d and d + dh/2
 //              of one head, so the rotation pairs are in its registers.
+//   DG_ARGMAX: the LM head: logits X[r] . W[v] for v < N (= the vocabulary;
+//              the last block's strips past it are masked), optionally
+//              stored to logits[r][ldl], and per row and 128-wide block the
+//              best logit, its id (lowest on ties) and the second best, at
+//              pv/pi/p2[r * ceil(N/128) + block] (as the LM-head kernels
+//              of fewer rows, for k_argmax_final).  Never split.
 // With few tiles the K range is split over S blocks per tile (split sk
 // takes K chunks [sk*cps, (sk+1)*cps)): each writes its float32 partial
 // sums to part[sk][r][col] and k_dense_reduce adds the S partials in order
 // and applies the epilogue.  S = 1 applies it directly.
-enum { DG_SET = 0, DG_ADD = 1, DG_QKV = 2, DG_SWIGLU = 3 };
+enum { DG_SET = 0, DG_ADD = 1, DG_QKV = 2, DG_SWIGLU = 3, DG_ARGMAX = 4 };
 struct DenseOut {
   float* y;            // DG_SET / DG_ADD
   int ldy;
@@ -320,6 +329,11 @@ struct DenseOut {
   const int32_t* row_valid;
   uint16_t* cache;
   float* q_out;
+  float* logits;       // DG_ARGMAX (NULL: not stored)
+  size_t ldl;
+  float* pv;
+  int32_t* pi;
+  float* p2;
 };
 
 // Partial columns per row: 2N for DG_SWIGLU (gate, then up), else N
@@ -384,22 +398,24 @@ __device__ __forceinline__ void to4(const f32x4_t a, float (&x)[4]) {
   x[3] = a[3];
 }
 
-// N output features (multiples of 128), K (multiple of 128); items = the
-// row chunks x N-blocks x S splits, chunk fastest, then split.
-template <int MODE>
+// N output features (multiples of 128, except DG_ARGMAX), K (multiple of
+// 128); items = the row chunks x N-blocks x S splits, chunk fastest, then
+// split.
+template <int MODE, int MT = 4>
 __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
                                                     const uint16_t* __restrict__ X, int ldx,
                                                     const uint4* __restrict__ Wp, int S,
                                                     float* __restrict__ part, DenseOut o) {
   constexpr int NA = MODE == DG_SWIGLU ? 2 : 1;
-  __shared__ __align__(16) uint16_t xs[2][kGemmM * kGemmLd];
+  constexpr int RM = 16 * MT;  // rows per block
+  __shared__ __align__(16) uint16_t xs[2][RM * kGemmLd];
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i16 = lane & 15, g = lane >> 4;
-  const int nz = (R + kGemmM - 1) / kGemmM, nbn = N / kGemmN;
+  const int nz = (R + RM - 1) / RM, nbn = (N + kGemmN - 1) / kGemmN;
   const int L = xcd_item(blockIdx.x, nz * nbn * S);
   if (L >= nz * nbn * S) return;
   const int z = L % nz, sk = (L / nz) % S, nb = L / nz / S;
-  const int t0 = z * kGemmM, nkt = K / 32, nch = K / kGemmKC;
+  const int t0 = z * RM, nkt = K / 32, nch = K / kGemmKC;
   const int cps = (nch + S - 1) / S, kc0 = sk * cps, nkc = min(cps, nch - kc0);
   // this wave's two strips: a rotate-half pair of one head (DG_QKV), else
   // strips 2w, 2w + 1 of the block
@@ -412,23 +428,94 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
     sa = nb * (kGemmN / 16) + 2 * w;
     sb = sa + 1;
   }
+  // strips past the packed matrix (the last LM-head block) read strip 0;
+  // their results are masked
+  const int nstr = (N + 15) / 16;
   const uint4* Wt[NA][2];
 #pragma unroll
   for (int a = 0; a < NA; ++a) {
-    Wt[a][0] = Wp + ((size_t)(a * (N / 16) + sa) * nkt + kc0 * 4) * 64 + lane;
-    Wt[a][1] = Wp + ((size_t)(a * (N / 16) + sb) * nkt + kc0 * 4) * 64 + lane;
+    Wt[a][0] = Wp + ((size_t)(a * (N / 16) + (sa < nstr ? sa : 0)) * nkt + kc0 * 4) * 64 + lane;
+    Wt[a][1] = Wp + ((size_t)(a * (N / 16) + (sb < nstr ? sb : 0)) * nkt + kc0 * 4) * 64 + lane;
   }
-  RowStage st;
+  RowStage<MT> st;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
+  for (int u = 0; u < MT; ++u) {
     const int t = t0 + stage_row(u);
     st.src[u] = t < R ? X + (size_t)t * ldx + kc0 * kGemmKC + stage_col(u) : nullptr;
   }
-  f32x4_t acc[NA][2][4];
-  gemm_core<NA, NA == 1>(Wt, nkc * kGemmKC, nz == 1, st, xs[0], xs[1], acc);
+  f32x4_t acc[NA][2][MT];
+  gemm_core<NA, NA == 1, MT>(Wt, nkc * kGemmKC, nz == 1, st, xs[0], xs[1], acc);
   const int fa = sa * 16 + 4 * g, fb = sb * 16 + 4 * g;
+  if constexpr (MODE == DG_ARGMAX) {
+    // per row: this lane's 8 logits (ascending ids), then the four lanes
+    // of the row, then the four waves (through LDS, in wave order)
+    __syncthreads();  // every wave is done with the staged rows
+    float* bv = (float*)xs[0];
+    float* sv = bv + 4 * RM;
+    int* bi = (int*)(sv + 4 * RM);
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
+      const int r = t0 + mt * 16 + i16;
+      float b1 = -INFINITY, b2 = -INFINITY;
+      int id = 1 << 30;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int v = (j ? fb : fa) + t;
+          const float x = v < N ? acc[0][j][mt][t] : -INFINITY;
+          if (o.logits && r < R && v < N) o.logits[(size_t)r * o.ldl + v] = x;
+          if (x > b1) {
+            b2 = b1;
+            b1 = x;
+            id = v;
+          } else if (x > b2) {
+            b2 = x;
+          }
+        }
+#pragma unroll
+      for (int sh = 16; sh <= 32; sh <<= 1) {
+        const float ob1 = __shfl_xor(b1, sh, MTP_WAVE), ob2 = __shfl_xor(b2, sh, MTP_WAVE);
+        const int oid = __shfl_xor(id, sh, MTP_WAVE);
+        if (ob1 > b1 || (ob1 == b1 && oid < id)) {
+          b2 = fmaxf(b1, ob2);
+          b1 = ob1;
+          id = oid;
+        } else {
+          b2 = fmaxf(b2, ob1);
+        }
+      }
+      if (lane < 16) {
+        bv[w * RM + mt * 16 + lane] = b1;
+        sv[w * RM + mt * 16 + lane] = b2;
+        bi[w * RM + mt * 16 + lane] = id;
+      }
+    }
+    __syncthreads();
+    const int rr = threadIdx.x;
+    if (rr < RM && t0 + rr < R) {
+      float c1 = bv[rr], c2 = sv[rr];
+      int cid = bi[rr];
+      for (int x = 1; x < 4; ++x) {
+        const float ob1 = bv[x * RM + rr], ob2 = sv[x * RM + rr];
+        const int oid = bi[x * RM + rr];
+        if (ob1 > c1 || (ob1 == c1 && oid < cid)) {
+          c2 = fmaxf(c1, ob2);
+          c1 = ob1;
+          cid = oid;
+        } else {
+          c2 = fmaxf(c2, ob1);
+        }
+      }
+      const size_t po = (size_t)(t0 + rr) * nbn + nb;
+      o.pv[po] = c1;
+      o.pi[po] = cid;
+      o.p2[po] = c2;
+    }
+    return;
+  }
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
     const int r = t0 + mt * 16 + i16;
     if (r >= R) continue;
     if (S > 1) {  // float32 partials of this split

@@ -1400,130 +1400,6 @@ __global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
   }
 }
 
-// ---------------------------------------------------------------- LM head (GEMM)
-// LM head for many rows as a tiled GEMM: block = 8 waves x one 16-row
-// vocabulary strip each (128 vocabulary rows) x NG 16-row groups of X
-// (blockIdx.y chunks of 16*NG rows).  X is staged through LDS four K-tiles
-// at a time, already in the MFMA B-operand layout, and shared by the 8
-// waves; each wave streams its strip's weight tiles with the next chunk in
-// flight and applies each tile to all NG groups.  Output as k_s_lm: per
-// row and block the best logit, its id (lowest on ties) and the second
-// best, at (row) * gridDim.x + blockIdx.x.
-template <int NG>
-__global__ void __launch_bounds__(512) k_lm_gemm(int nr, int V, int H,
-                                                 const uint16_t* __restrict__ X,
-                                                 const uint4* __restrict__ Wp,
-                                                 float* __restrict__ logits, size_t ldl,
-                                                 float* __restrict__ pv,
-                                                 int32_t* __restrict__ pi,
-                                                 float* __restrict__ p2) {
-  constexpr int KC = 4;
-  // the per-wave argmax candidates reuse the X staging area once the
-  // products are done (with NG = 16 the two would not leave room for a
-  // second block per CU)
-  static_assert(3 * 8 * 16 * NG * 4 <= KC * NG * 64 * 16, "candidates fit in the staging area");
-  __shared__ uint4 xs[KC][NG][64];
-  float(*bv)[16 * NG] = (float(*)[16 * NG])&xs[0][0][0];
-  float(*sv)[16 * NG] = bv + 8;
-  int(*bi)[16 * NG] = (int(*)[16 * NG])(bv + 16);
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int nkt = H / 32;
-  const int nt = blockIdx.x * 8 + wv;
-  const int r0 = blockIdx.y * 16 * NG;
-  const bool live = nt * 16 < V;
-  const uint4* A = Wp + (size_t)(live ? nt : 0) * nkt * 64;
-  const uint4 z = make_uint4(0, 0, 0, 0);
-  f32x4_t acc[NG];
-#pragma unroll
-  for (int g = 0; g < NG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  uint4 a[KC];
-#pragma unroll
-  for (int u = 0; u < KC; ++u) a[u] = (live && u < nkt) ? ld_tile(A + (size_t)u * 64 + lane, true) : z;
-  for (int k0 = 0; k0 < nkt; k0 += KC) {
-    __syncthreads();  // the previous chunk of xs is consumed
-    for (int idx = threadIdx.x; idx < KC * NG * 64; idx += 512) {
-      const int l = idx & 63, gq = (idx >> 6) % NG, kk = idx / (64 * NG);
-      const int row = r0 + 16 * gq + (l & 15), kt = k0 + kk;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (row < nr && kt < nkt) v = ldx(X + (size_t)row * H + kt * 32 + 8 * (l >> 4));
-      xs[kk][gq][l] = v;
-    }
-    __syncthreads();
-    uint4 an[KC];
-#pragma unroll
-    for (int u = 0; u < KC; ++u)
-      an[u] = (live && k0 + KC + u < nkt) ? ld_tile(A + (size_t)(k0 + KC + u) * 64 + lane, true) : z;
-#pragma unroll
-    for (int kk = 0; kk < KC; ++kk) {
-      if (k0 + kk < nkt) {
-#pragma unroll
-        for (int g = 0; g < NG; ++g) acc[g] = mfma16(a[kk], xs[kk][g][lane], acc[g]);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < KC; ++u) a[u] = an[u];
-  }
-  const int v0 = nt * 16 + 4 * (lane >> 4), r = lane & 15;
-  __syncthreads();  // every wave is done with xs
-#pragma unroll
-  for (int g = 0; g < NG; ++g) {
-    const int row = r0 + 16 * g + r;
-    float b1 = -INFINITY, b2 = -INFINITY;
-    int id = 1 << 30;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int v = v0 + t;
-      const float x = (live && v < V) ? acc[g][t] : -INFINITY;
-      if (logits && row < nr && live && v < V) logits[(size_t)row * ldl + v] = x;
-      if (x > b1) {
-        b2 = b1;
-        b1 = x;
-        id = v;
-      } else if (x > b2) {
-        b2 = x;
-      }
-    }
-#pragma unroll
-    for (int o = 16; o <= 32; o <<= 1) {
-      const float ob1 = __shfl_xor(b1, o, MTP_WAVE), ob2 = __shfl_xor(b2, o, MTP_WAVE);
-      const int oid = __shfl_xor(id, o, MTP_WAVE);
-      if (ob1 > b1 || (ob1 == b1 && oid < id)) {
-        b2 = fmaxf(b1, ob2);
-        b1 = ob1;
-        id = oid;
-      } else {
-        b2 = fmaxf(b2, ob1);
-      }
-    }
-    if (lane < 16) {
-      bv[wv][16 * g + lane] = b1;
-      sv[wv][16 * g + lane] = b2;
-      bi[wv][16 * g + lane] = id;
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x < 16 * NG && r0 + (int)threadIdx.x < nr) {
-    const int rr = threadIdx.x;
-    float c1 = bv[0][rr], c2 = sv[0][rr];
-    int cid = bi[0][rr];
-    for (int x = 1; x < 8; ++x) {
-      const float ob1 = bv[x][rr], ob2 = sv[x][rr];
-      const int oid = bi[x][rr];
-      if (ob1 > c1 || (ob1 == c1 && oid < cid)) {
-        c2 = fmaxf(c1, ob2);
-        c1 = ob1;
-        cid = oid;
-      } else {
-        c2 = fmaxf(c2, ob1);
-      }
-    }
-    const size_t o = (size_t)(r0 + rr) * gridDim.x + blockIdx.x;
-    pv[o] = c1;
-    pi[o] = cid;
-    p2[o] = c2;
-  }
-}
-
 // ---------------------------------------------------------------- LM head
 // Block = 4 vocabulary strips (64 rows) x RG 16-row groups (blockIdx.y)
 // of the nr input rows X (bf16): each weight tile feeds RG MFMAs.  Per row

@@ -584,16 +584,17 @@ struct Model {
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
     const unsigned G = groups(nr);
     unsigned nb = nblk;
-    if (G >= 4) {  // many rows: tiled GEMM, 128 vocabulary rows per block
-      nb = cdiv(V, 128);
-      const int NG = G >= 16 ? 16 : (G >= 8 ? 8 : 4);
-#define MTP_LMG(N)                                                                              \
-  launch_k(tm, MTP_KC_LM_HEAD, k_lm_gemm<N>, dim3(nb, cdiv(G, N)), dim3(512), 0, s, nr, V, H,   \
-           (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2)
-      if (NG == 16) MTP_LMG(16);
-      else if (NG == 8) MTP_LMG(8);
-      else MTP_LMG(4);
-#undef MTP_LMG
+    if (G >= 4) {  // many rows: the tiled GEMM, 128 vocabulary rows x 64 rows per block
+      nb = cdiv(V, kGemmN);
+      DenseOut o{};
+      o.logits = logits;
+      o.ldl = ldl;
+      o.pv = ws.pv;
+      o.pi = ws.pi;
+      o.p2 = ws.p2;
+      launch_k(tm, MTP_KC_LM_HEAD, k_dense_gemm<DG_ARGMAX>,
+               dim3(grid_xcd((size_t)cdiv(nr, kGemmM) * nb)), dim3(256), 0, s, nr, V, H,
+               (const uint16_t*)ws.xhead, H, pk.lm, 1, (float*)nullptr, o);
     } else if (G >= 2) {
       launch_k(tm, MTP_KC_LM_HEAD, k_s_lm<2>, dim3(nblk, cdiv(G, 2)), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, pk.lm, logits, ldl, ws.pv, ws.pi, ws.p2);
