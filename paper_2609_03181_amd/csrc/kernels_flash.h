@@ -26,10 +26,17 @@ __device__ __forceinline__ void split8(const float (&x)[8], uint4& hi, uint4& lo
 }
 
 // Block = 4 waves = 64 query rows (wave w: rows 16w..16w+15 of tile
-// blockIdx.x) of head blockIdx.y of sequence blockIdx.z; the C rows of each
-// sequence sit at row_pos[b*C + i] (invalid rows: zeros).  Keys run in
-// 64-key tiles up to the largest position of the block's valid rows; each
-// row masks keys past its own position.
+// blockIdx.x % ntile) of head blockIdx.y of sequence blockIdx.z; the C rows
+// of each sequence sit at row_pos[b*C + i] (invalid rows: zeros).  Keys run
+// in 64-key tiles up to the largest position of the block's valid rows;
+// each row masks keys past its own position.
+// SPLIT: the keys are cut into chunks of CH tiles, chunk c = blockIdx.x /
+// ntile (a row tile's chunks run in parallel instead of one after the
+// other); the block writes each row's unnormalised partial (o, m, l) of its
+// chunk to part[((row * nh + head) * n_part + c) * (DH + 2)] -- the split
+// partials of the decode attention -- and k_attn_merge combines a row's
+// chunks.  A chunk past the tile's last key writes nothing (no row of the
+// tile reads it).
 //
 // Layouts (lane l, g = l/16, i = l%16):
 //   S tile q (keys 16q..16q+15 of the key tile): A = K rows (lane: key i,
@@ -41,14 +48,16 @@ __device__ __forceinline__ void split8(const float (&x)[8], uint4& hi, uint4& lo
 //     B = P needs no data movement and A = V^T reads two 8-byte runs of the
 //     V tile, stored transposed in LDS ([dim][key]); the result lane holds
 //     O[row i][dim 16d + 4g + t] for dim tile d.
-template <int DH>
+template <int DH, bool SPLIT = false>
 __global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
                                                        const float* __restrict__ q,
                                                        const uint16_t* __restrict__ cache,
                                                        size_t seq_stride, int cap,
                                                        const int32_t* __restrict__ row_pos,
                                                        const int32_t* __restrict__ row_valid,
-                                                       float scale, uint16_t* __restrict__ out) {
+                                                       float scale, uint16_t* __restrict__ out,
+                                                       int ntile = 0, int CH = 0, int n_part = 0,
+                                                       float* __restrict__ part = nullptr) {
   static_assert(DH == 128, "four k-steps of 32 dims");
   constexpr int NS = DH / 32, ND = DH / 16, VL = 64 + 8;
   __shared__ __align__(16) uint16_t vt[DH * VL];  // V tile transposed: [dim][key]
@@ -56,7 +65,9 @@ __global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int i16 = lane & 15, g = lane >> 4;
   const int h = blockIdx.y, b = blockIdx.z, D = nh * DH;
-  const int r = blockIdx.x * 64 + 16 * w + i16;  // this lane's query row (of the sequence)
+  const int tile = SPLIT ? blockIdx.x % ntile : blockIdx.x;
+  const int chunk = SPLIT ? blockIdx.x / ntile : 0;
+  const int r = tile * 64 + 16 * w + i16;  // this lane's query row (of the sequence)
   const bool rv = r < C && row_valid[(size_t)b * C + r];
   const int rp = rv ? row_pos[(size_t)b * C + r] : -1;
   if (threadIdx.x == 0) s_kmax = 0;
@@ -77,7 +88,10 @@ __global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
     }
   }
   __syncthreads();
-  const int kmax = s_kmax < cap ? s_kmax : cap;
+  const int kend = s_kmax < cap ? s_kmax : cap;
+  const int kbeg = SPLIT ? chunk * CH * 64 : 0;
+  const int kmax = SPLIT ? min(kend, kbeg + CH * 64) : kend;
+  if (kbeg >= kmax && SPLIT) return;  // block-uniform
   const uint16_t* Kc = cache + (size_t)b * seq_stride + (size_t)h * cap * DH;
   const uint16_t* Vc = cache + (size_t)b * seq_stride + (size_t)(nh + h) * cap * DH;
   float m = -INFINITY, lsum = 0.f;
@@ -110,11 +124,11 @@ __global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
       vr[u] = *(const uint4*)(Vc + (size_t)key * DH + (c >> 6) * 8);
     }
   };
-  if (kmax > 0) {
-    load_k(0);
-    load_v(0);
+  if (kmax > kbeg) {
+    load_k(kbeg);
+    load_v(kbeg);
   }
-  for (int k0 = 0; k0 < kmax; k0 += 64) {
+  for (int k0 = kbeg; k0 < kmax; k0 += 64) {
     const bool more = k0 + 64 < kmax;
     __syncthreads();  // the previous tile's P.V is done with the V tile
 #pragma unroll
@@ -189,6 +203,19 @@ __global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
   // the row's sum over its four lanes, then O / l as bf16
   float lt = lsum + __shfl_xor(lsum, 16, MTP_WAVE);
   lt += __shfl_xor(lt, 32, MTP_WAVE);
+  if (SPLIT) {
+    if (r < C) {
+      float* pp = part + ((((size_t)b * C + r) * nh + h) * n_part + chunk) * (DH + 2);
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+        *(float4*)(pp + 16 * d + 4 * g) = make_float4(o[d][0], o[d][1], o[d][2], o[d][3]);
+      if (g == 0) {
+        pp[DH] = m;
+        pp[DH + 1] = lt;
+      }
+    }
+    return;
+  }
   if (r < C) {
     uint16_t* op = out + ((size_t)b * C + r) * D + (size_t)h * DH + 4 * g;
     const float inv = (rv && lt > 0.f) ? 1.f / lt : 0.f;
@@ -200,6 +227,26 @@ __global__ void __launch_bounds__(256) k_flash_prefill(int C, int nh,
       *(uint2*)(op + 16 * d) = pk;
     }
   }
+}
+
+// Combines the key chunks of the split prefill attention: one wave per
+// (row, head), the row's chunks being those that reach its position
+// (ceil(ceil((pos + 1) / 64) / CH)); writes the bf16 row (zeros for an
+// invalid row).
+template <int DH>
+__global__ void __launch_bounds__(256) k_attn_merge(int R, int nh, int CH, int n_part,
+                                                    const float* __restrict__ part,
+                                                    const int32_t* __restrict__ row_pos,
+                                                    const int32_t* __restrict__ row_valid,
+                                                    uint16_t* __restrict__ out) {
+  __shared__ float ws[4][64];
+  const int w = threadIdx.x >> 6, x = blockIdx.x * 4 + w;
+  if (x >= R * nh) return;
+  const int r = x / nh, h = x % nh;
+  const bool valid = row_valid[r] != 0;
+  const int n = valid ? min(n_part, ((row_pos[r] + 64) / 64 + CH - 1) / CH) : 0;
+  attn_merge_row<DH>(part + ((size_t)r * nh + h) * n_part * (DH + 2), n, valid, ws[w],
+                     out + (size_t)r * nh * DH + h * DH);
 }
 
 }  // namespace mtp

@@ -207,13 +207,16 @@ def test_full_shape_batch1_one_pass_prefill_forced_and_natural_steps(plain):
         f"{replay.assert_local_band(lstats)}")
 
 
-def test_full_shape_gundam_prefix_one_pass(plain):
+@pytest.mark.parametrize("n_txt", [64, 512])
+def test_full_shape_gundam_prefix_one_pass(plain, n_txt):
     """Gundam-mode page (Table "Model specification": 256 + 100 n visual
-    rows, n = 9 -> 1156, the largest) + 64 prompt tokens prefilled in one
-    pass of 1220 rows, then graph-replayed steps: prefill token, state,
-    every verifier K/V position and the draft cache against the oracle."""
+    rows, n = 9 -> 1156, the largest) + n_txt prompt tokens prefilled in one
+    pass, then graph-replayed steps: prefill token, state, every verifier
+    K/V position and the draft cache against the oracle.  1220 rows (200
+    row-tile x head blocks) run the key-split prefill attention, 1668 rows
+    (the benchmark's page, 270 blocks) the one-block-per-row-tile form."""
     w, model, orc = plain
-    K, n_vis, n_txt, n_steps = 3, 1156, 64, 3
+    K, n_vis, n_steps = 3, 1156, 3
     P = n_vis + n_txt
     tok, vis = prefix_inputs(CFG, 1, n_vis, n_txt)
     log(f"[gundam] GPU prefill of {P} rows in one pass")
