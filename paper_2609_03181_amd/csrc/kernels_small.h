@@ -1341,6 +1341,104 @@ __global__ void __launch_bounds__(256) k_s_down_split(int R, int H, int E, int I
   }
 }
 
+// ---------------------------------------------------------------- MoE down (slots)
+// 17..64 rows (few entries per expert, where a block of 16 output
+// features x 16 entries with K split over its 4 waves keeps more blocks in
+// flight than the grouped GEMM's 64-entry tiles): block = (16 output
+// features, expert y, cpb 16-entry chunks from z*16*cpb).  A routed
+// expert's wave tiles (I/128 <= MAXT) are loaded once and applied to the
+// block's chunks in turn; the shared block (K = SI) streams its tiles per chunk (the shared
+// weights stay in L2), so the registers are sized for one expert's K.
+// Routed y < E: slot[(row*(k+1) + slot)][n] = w * (Wd_y[n] . act_t);
+// y == E: slot[(r*(k+1) + k)][n] = Wsd[n] . act_sh[r] (the shared experts
+// as one width-SI SwiGLU).  k_combine_norm then adds the k+1 slots of
+// each row to h in a fixed order.
+template <int MAXT>
+__global__ void __launch_bounds__(256) k_s_down_slot(int cpb, int R, int E, int topk, int H,
+                                                     int I, int SI,
+                                                     const uint16_t* __restrict__ act,
+                                                     const uint16_t* __restrict__ act_sh,
+                                                     const uint4* __restrict__ edn,
+                                                     size_t e_stride,
+                                                     const uint4* __restrict__ sdn,
+                                                     const int32_t* __restrict__ cnt,
+                                                     const int32_t* __restrict__ off,
+                                                     const int32_t* __restrict__ ent_row,
+                                                     const int32_t* __restrict__ ent_slot,
+                                                     const float* __restrict__ ent_w,
+                                                     float* __restrict__ slot) {
+  __shared__ f32x4_t red[4 * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nt = blockIdx.x, e = blockIdx.y, tb = blockIdx.z * 16 * cpb;
+  const bool dense = e == E;
+  int n = R, o = 0;
+  if (!dense) {
+    n = cnt[e];
+    o = off[e];
+  }
+  if (tb >= n) return;
+  const int K = dense ? SI : I, nkt = K / 32, per = nkt / 4;
+  const uint4* A = dense ? sdn + (size_t)nt * nkt * 64
+                         : edn + (size_t)e * e_stride + (size_t)nt * nkt * 64;
+  // Chunk c's rows: entries tb + 16c + (lane & 15).
+  auto chunk_rows = [&](int c, const uint16_t*& xrow, int& row, int& sl, float& wt) {
+    const int t = tb + 16 * c + (lane & 15);
+    xrow = nullptr;
+    row = 0;
+    sl = topk;
+    wt = 1.f;
+    if (t < n) {
+      if (dense) {
+        xrow = act_sh + (size_t)t * SI;
+        row = t;
+      } else {
+        xrow = act + (size_t)(o + t) * I;
+        row = ent_row[o + t];
+        sl = ent_slot[o + t];
+        wt = ent_w[o + t];
+      }
+    }
+  };
+  auto store = [&](int c, f32x4_t acc, int row, int sl, float wt) {
+    const int t = tb + 16 * c + (lane & 15);
+    if (w == 0 && t < n) {
+      float4* dst =
+          (float4*)(slot + ((size_t)row * (topk + 1) + sl) * H + nt * 16 + 4 * (lane >> 4));
+      *dst = make_float4(wt * acc[0], wt * acc[1], wt * acc[2], wt * acc[3]);
+    }
+  };
+  const f32x4_t z4 = {0.f, 0.f, 0.f, 0.f};
+  if (dense) {  // the shared block streams its tiles per chunk (double-buffered)
+    for (int c = 0; c < cpb; ++c) {
+      if (tb + 16 * c >= n) break;  // block-uniform
+      if (c > 0) __syncthreads();
+      const uint16_t* xrow;
+      int row, sl;
+      float wt;
+      chunk_rows(c, xrow, row, sl, wt);
+      f32x4_t acc = sk_range<4>(A, w * per, (w + 1) * per, xrow, z4, n <= 16 * cpb);
+      acc = block_acc_sum<4>(acc, red);
+      store(c, acc, row, sl, wt);
+    }
+    return;
+  }
+  // a routed expert's wave tiles (I/128 <= MAXT) stay in registers; each
+  // chunk's B operands are all loaded before its products
+  uint4 a[MAXT];
+  preload<MAXT>(A, w * per, per, a, n <= 16 * cpb);  // read by this block only
+  for (int c = 0; c < cpb; ++c) {
+    if (tb + 16 * c >= n) break;  // block-uniform
+    if (c > 0) __syncthreads();
+    const uint16_t* xrow;
+    int row, sl;
+    float wt;
+    chunk_rows(c, xrow, row, sl, wt);
+    f32x4_t acc = mma_pre<MAXT>(a, w * per, per, xrow, z4);
+    acc = block_acc_sum<4>(acc, red);
+    store(c, acc, row, sl, wt);
+  }
+}
+
 // Grouping of (row, slot) pairs by expert for any number of rows: counts,
 // offsets (ascending expert id), one entry per pair, and the chunk-block
 // prefix cbp of the grouped GEMMs' work items (chunks of 16*cpb entries;

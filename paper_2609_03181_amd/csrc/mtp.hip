@@ -109,6 +109,7 @@ mtp_status scratch_addr(void** out) {
 constexpr int kLmBlk = 64;  // vocabulary rows per LM-head block
 constexpr int kDownSplit = 8;  // blocks per output strip of the small-batch MoE down
 constexpr int kMoeSpinMax = 1 << 20;  // polls of a fused-MoE wait before it gives up
+constexpr int kSlotRows = 64;   // passes of 17..64 rows: slot-form MoE down and split-K QKV
 constexpr int kFlashRows = 64;  // prefill passes of at least this many rows per sequence use
                                 // the flash-style attention
 constexpr int kFlashChunk = 2;  // key tiles per chunk of the split prefill attention
@@ -463,7 +464,10 @@ struct Model {
 
   void smm(const Ws& ws, int R, int N, int K, const uint16_t* X, int ldx_, const uint4* Wp,
            float* Y, int ldy, bool add) {
-    if (R > SR_MAX && N % kGemmN == 0 && K % kGemmKC == 0) {  // tiled GEMM, rows in LDS
+    // tiled GEMM (rows in LDS) beyond 16 rows, except the short products
+    // (K <= 2560: O projection, eh) of decode-sized passes, where the
+    // split-K form with one block per (strip, row group) measured faster
+    if (R > SR_MAX && N % kGemmN == 0 && K % kGemmKC == 0 && (K > 2560 || R > 256)) {
       DenseOut o{};
       o.y = Y;
       o.ldy = ldy;
@@ -554,7 +558,7 @@ struct Model {
   void attn_mfma(const Ws& ws, int B, int C, const float* g, const uint16_t* xg,
                  const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
-    if (xg && R > SR_MAX) {  // tiled GEMM over the normalised rows
+    if (xg && R > kSlotRows) {  // tiled GEMM over the normalised rows
       DenseOut o{};
       o.C = C;
       o.nh = nh;
@@ -708,12 +712,19 @@ struct Model {
       }
       const uint4* edn = pk.exp_down + (size_t)l * E * pk.exp_down_s;
       const uint4* sdn = pk.sh_down + l * pk.sh_down_s;
-      if (small)
+      if (small) {
         launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_split<kDownSplit>, dim3(H / 16, kDownSplit),
                  dim3(256), 0, s, R, H, E, I, S, (const uint16_t*)ws.act, ws.act_sh, edn,
                  pk.exp_down_s, sdn, ws.cnt, ws.off, ws.ent_row, ws.ent_w, ws.touched,
                  ws.n_touched, ws.dn_part, ws.dn_ctr, ws.h, ws.status);
-      else
+      } else if (R <= kSlotRows) {  // few entries per expert: 16-entry slot blocks
+#define MTP_DSLOT(M)                                                                           \
+  launch_k(tm, MTP_KC_MOE_DOWN, k_s_down_slot<M>, dim3(H / 16, E + 1, G), dim3(256), 0, s, 1, R, \
+           E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn, ws.cnt,  \
+           ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot)
+        MTP_MAXT_DISPATCH(I / 128, MTP_DSLOT);
+#undef MTP_DSLOT
+      } else
         launch_k(tm, MTP_KC_MOE_DOWN, k_down_gemm, dim3(grid_xcd(chunks * (H / kGemmN))), dim3(256), 0, s,
                  R, E, k, H, I, SI, (const uint16_t*)ws.act, ws.act_sh, edn, pk.exp_down_s, sdn,
                  ws.cnt, ws.off, ws.ent_row, ws.ent_slot, ws.ent_w, ws.slot, ws.cbp);
