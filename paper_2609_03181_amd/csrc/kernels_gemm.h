@@ -313,11 +313,14 @@ __global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H
 //              best logit, its id (lowest on ties) and the second best, at
 //              pv/pi/p2[r * ceil(N/128) + block] (as the LM-head kernels
 //              of fewer rows, for k_argmax_final).  Never split.
+//   DG_ARGMAX_W: DG_ARGMAX with 256 vocabulary rows per block (wave w:
+//              strips 4w..4w+3 as two strip pairs through the two-matrix
+//              core), partials per 256-wide block.
 // With few tiles the K range is split over S blocks per tile (split sk
 // takes K chunks [sk*cps, (sk+1)*cps)): each writes its float32 partial
 // sums to part[sk][r][col] and k_dense_reduce adds the S partials in order
 // and applies the epilogue.  S = 1 applies it directly.
-enum { DG_SET = 0, DG_ADD = 1, DG_QKV = 2, DG_SWIGLU = 3, DG_ARGMAX = 4 };
+enum { DG_SET = 0, DG_ADD = 1, DG_QKV = 2, DG_SWIGLU = 3, DG_ARGMAX = 4, DG_ARGMAX_W = 5 };
 struct DenseOut {
   float* y;            // DG_SET / DG_ADD
   int ldy;
@@ -406,12 +409,15 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
                                                     const uint16_t* __restrict__ X, int ldx,
                                                     const uint4* __restrict__ Wp, int S,
                                                     float* __restrict__ part, DenseOut o) {
-  constexpr int NA = MODE == DG_SWIGLU ? 2 : 1;
+  constexpr bool WIDE = MODE == DG_ARGMAX_W;
+  constexpr bool ARGMAX = MODE == DG_ARGMAX || WIDE;
+  constexpr int NA = (MODE == DG_SWIGLU || WIDE) ? 2 : 1;
+  constexpr int NBLK = WIDE ? 2 * kGemmN : kGemmN;  // output features per block
   constexpr int RM = 16 * MT;  // rows per block
   __shared__ __align__(16) uint16_t xs[2][RM * kGemmLd];
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i16 = lane & 15, g = lane >> 4;
-  const int nz = (R + RM - 1) / RM, nbn = (N + kGemmN - 1) / kGemmN;
+  const int nz = (R + RM - 1) / RM, nbn = (N + NBLK - 1) / NBLK;
   const int L = xcd_item(blockIdx.x, nz * nbn * S);
   if (L >= nz * nbn * S) return;
   const int z = L % nz, sk = (L / nz) % S, nb = L / nz / S;
@@ -425,7 +431,7 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
     sa = nb * (kGemmN / 16) + ls;
     sb = sa + tph;
   } else {
-    sa = nb * (kGemmN / 16) + 2 * w;
+    sa = nb * (NBLK / 16) + (WIDE ? 4 : 2) * w;
     sb = sa + 1;
   }
   // strips past the packed matrix (the last LM-head block) read strip 0;
@@ -434,8 +440,12 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
   const uint4* Wt[NA][2];
 #pragma unroll
   for (int a = 0; a < NA; ++a) {
-    Wt[a][0] = Wp + ((size_t)(a * (N / 16) + (sa < nstr ? sa : 0)) * nkt + kc0 * 4) * 64 + lane;
-    Wt[a][1] = Wp + ((size_t)(a * (N / 16) + (sb < nstr ? sb : 0)) * nkt + kc0 * 4) * 64 + lane;
+    // DG_SWIGLU: matrix a (gate, up) at strip offset a * N/16; wide
+    // DG_ARGMAX: strip pair a of the wave (strips sa + 2a, sb + 2a)
+    const int ta = WIDE ? sa + 2 * a : sa, tb = WIDE ? sb + 2 * a : sb;  // strips of the matrix
+    const int mo = WIDE ? 0 : a * (N / 16);                               // the matrix's first strip
+    Wt[a][0] = Wp + ((size_t)((ta < nstr ? ta : 0) + mo) * nkt + kc0 * 4) * 64 + lane;
+    Wt[a][1] = Wp + ((size_t)((tb < nstr ? tb : 0) + mo) * nkt + kc0 * 4) * 64 + lane;
   }
   RowStage<MT> st;
 #pragma unroll
@@ -446,7 +456,7 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
   f32x4_t acc[NA][2][MT];
   gemm_core<NA, NA == 1, MT>(Wt, nkc * kGemmKC, nz == 1, st, xs[0], xs[1], acc);
   const int fa = sa * 16 + 4 * g, fb = sb * 16 + 4 * g;
-  if constexpr (MODE == DG_ARGMAX) {
+  if constexpr (ARGMAX) {
     // per row: this lane's 8 logits (ascending ids), then the four lanes
     // of the row, then the four waves (through LDS, in wave order)
     __syncthreads();  // every wave is done with the staged rows
@@ -459,11 +469,13 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
       float b1 = -INFINITY, b2 = -INFINITY;
       int id = 1 << 30;
 #pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          const int v = (j ? fb : fa) + t;
-          const float x = v < N ? acc[0][j][mt][t] : -INFINITY;
+          const int v = (j ? fb : fa) + 32 * a + t;  // ascending ids
+          const float x = v < N ? acc[a][j][mt][t] : -INFINITY;
           if (o.logits && r < R && v < N) o.logits[(size_t)r * o.ldl + v] = x;
           if (x > b1) {
             b2 = b1;

@@ -607,15 +607,16 @@ struct Model {
     const unsigned nblk = cdiv(cdiv(V, 16), 4);
     const unsigned G = groups(nr);
     unsigned nb = nblk;
-    if (G >= 4) {  // many rows: the tiled GEMM, 128 vocabulary rows x 64 rows per block
-      nb = cdiv(V, kGemmN);
+    if (G >= 4) {  // many rows: the tiled GEMM, 128 (from 128 rows: 256) vocabulary rows x 64 rows per block
+      const bool wide = nr >= 2 * kGemmM;
+      nb = cdiv(V, wide ? 2 * kGemmN : kGemmN);
       DenseOut o{};
       o.logits = logits;
       o.ldl = ldl;
       o.pv = ws.pv;
       o.pi = ws.pi;
       o.p2 = ws.p2;
-      launch_k(tm, MTP_KC_LM_HEAD, k_dense_gemm<DG_ARGMAX>,
+      launch_k(tm, MTP_KC_LM_HEAD, wide ? k_dense_gemm<DG_ARGMAX_W> : k_dense_gemm<DG_ARGMAX>,
                dim3(grid_xcd((size_t)cdiv(nr, kGemmM) * nb)), dim3(256), 0, s, nr, V, H,
                (const uint16_t*)ws.xhead, H, pk.lm, 1, (float*)nullptr, o);
     } else if (G >= 2) {
