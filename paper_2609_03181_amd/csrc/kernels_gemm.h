@@ -81,6 +81,11 @@ struct RowStage {
 #pragma unroll
     for (int u = 0; u < MT; ++u) v[u] = src[u] ? *(const uint4*)(src[u] + k0) : make_uint4(0, 0, 0, 0);
   }
+  // every src set (no row past the entries)
+  __device__ __forceinline__ void load_set(int k0) {
+#pragma unroll
+    for (int u = 0; u < MT; ++u) v[u] = *(const uint4*)(src[u] + k0);
+  }
   __device__ __forceinline__ void store(uint16_t* xs) const {
 #pragma unroll
     for (int u = 0; u < MT; ++u) {
@@ -94,13 +99,84 @@ struct RowStage {
 __device__ __forceinline__ int stage_row(int u) { return (threadIdx.x + 256 * u) >> 4; }
 __device__ __forceinline__ int stage_col(int u) { return 8 * ((threadIdx.x + 256 * u) & 15); }
 
+// ld_tile with the non-temporal choice fixed at compile time
+template <bool NT>
+__device__ __forceinline__ uint4 ld_tile_t(const uint4* p) {
+  if constexpr (NT) {
+    const u32x4_t x = __builtin_nontemporal_load((const u32x4_t*)p);
+    return make_uint4(x[0], x[1], x[2], x[3]);
+  } else {
+    return *p;
+  }
+}
+
+// The prefetching form of gemm_core (PF): chunk kc + 1's weight tiles are
+// loaded during chunk kc's products (two register sets).  Chunk kc + 1's
+// rows are requested before its weights, so staging them into LDS after
+// chunk kc's products waits for the rows alone (loads complete in order)
+// while the weights stay in flight until chunk kc + 1's products.  Every
+// st.src is a row (a piece past the entries points at a valid row whose
+// products the caller discards), so the row loads carry no per-lane
+// branch.  NT: non-temporal weight loads.  Products and their order are
+// those of gemm_core.
+template <int NA, int MT, bool NT>
+__device__ __forceinline__ void gemm_pipe(const uint4* const (&Wt)[NA][2], int nch,
+                                          RowStage<MT>& st, uint16_t* xs0, uint16_t* xs1,
+                                          f32x4_t (&acc)[NA][2][MT]) {
+  const int lane = threadIdx.x & 63, i16 = lane & 15, g = lane >> 4;
+  typedef uint4 WSet[NA][4][2];
+  WSet w0, w1;
+  auto load_w = [&](WSet& wt, int kc) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) wt[a][ks][j] = ld_tile_t<NT>(Wt[a][j] + (size_t)(kc * 4 + ks) * 64);
+  };
+  auto mma = [&](const WSet& wt, const uint16_t* xs) {
+    const uint16_t* xb = xs + i16 * kGemmLd + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      uint4 bx[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) bx[mt] = *(const uint4*)(xb + mt * 16 * kGemmLd + 32 * ks);
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = mfma16(wt[a][ks][j], bx[mt], acc[a][j][mt]);
+    }
+  };
+  // chunk kc: weights wc, rows in LDS stage xc; wn (chunk kc - 1's weights,
+  // used) takes chunk kc + 1, whose rows go to xn after the products
+  auto step = [&](int kc, const WSet& wc, WSet& wn, const uint16_t* xc, uint16_t* xn) {
+    if (kc + 1 < nch) {
+      st.load_set((kc + 1) * kGemmKC);
+      load_w(wn, kc + 1);
+    }
+    __syncthreads();  // xc holds chunk kc; every wave is done reading xn
+    mma(wc, xc);
+    if (kc + 1 < nch) st.store(xn);
+  };
+  st.load_set(0);
+  load_w(w0, 0);
+  st.store(xs0);
+  for (int kc = 0; kc < nch; kc += 2) {
+    step(kc, w0, w1, xs0, xs1);
+    if (kc + 1 >= nch) break;
+    step(kc + 1, w1, w0, xs1, xs0);
+  }
+}
+
 // acc[a][j][mt] = sum over K of matrix a's strip j (tile stream Wt[a][j],
 // lane offset included) times row tile mt (of MT) of the staged rows.  K is a
 // multiple of kGemmKC; st.src is set; xs0 / xs1 are the two LDS stages.
-// PF: the weight tiles of chunk kc + 1 are loaded during chunk kc's
-// products (two register sets); else each chunk's tiles are loaded at its
-// start (one set: with two matrices, two waves per SIMD fit instead of one,
-// and the other wave covers the load latency).
+// PF: gemm_pipe (chunk kc + 1's loads in flight during chunk kc's products;
+// every st.src must point at a row); else each chunk's tiles are loaded at
+// its start (one register set: with two matrices, two waves per SIMD fit
+// instead of one, and the other wave covers the load latency).
 template <int NA, bool PF, int MT = 4>
 __device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K, bool once,
                                           RowStage<MT>& st, uint16_t* xs0, uint16_t* xs1,
@@ -137,38 +213,21 @@ __device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K
           for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = mfma16(wt[a][ks][j], bx[mt], acc[a][j][mt]);
     }
   };
+  if constexpr (PF) {
+    if (once) gemm_pipe<NA, MT, true>(Wt, nch, st, xs0, xs1, acc);
+    else gemm_pipe<NA, MT, false>(Wt, nch, st, xs0, xs1, acc);
+    return;
+  }
   st.load(0);
   load_w(wa, 0);
   st.store(xs0);
-  if constexpr (!PF) {
-    for (int kc = 0; kc < nch; ++kc) {
-      uint16_t* cur = (kc & 1) ? xs1 : xs0;
-      if (kc > 0) load_w(wa, kc);
-      if (kc + 1 < nch) st.load((kc + 1) * kGemmKC);
-      __syncthreads();  // cur holds chunk kc; every wave is done reading the other stage
-      mma(wa, cur);
-      if (kc + 1 < nch) st.store((kc & 1) ? xs0 : xs1);
-    }
-    return;
-  }
-  uint4 wb[NA][4][2];
-  for (int kc = 0; kc < nch; kc += 2) {
-    // chunk kc: weights wa, rows xs0; chunk kc + 1's loads in flight
-    if (kc + 1 < nch) {
-      load_w(wb, kc + 1);
-      st.load((kc + 1) * kGemmKC);
-    }
-    __syncthreads();  // xs0 holds chunk kc; every wave is done reading xs1
-    mma(wa, xs0);
-    if (kc + 1 >= nch) break;
-    st.store(xs1);
-    if (kc + 2 < nch) {
-      load_w(wa, kc + 2);
-      st.load((kc + 2) * kGemmKC);
-    }
-    __syncthreads();  // xs1 holds chunk kc + 1; every wave is done reading xs0
-    mma(wb, xs1);
-    if (kc + 2 < nch) st.store(xs0);
+  for (int kc = 0; kc < nch; ++kc) {
+    uint16_t* cur = (kc & 1) ? xs1 : xs0;
+    if (kc > 0) load_w(wa, kc);
+    if (kc + 1 < nch) st.load((kc + 1) * kGemmKC);
+    __syncthreads();  // cur holds chunk kc; every wave is done reading the other stage
+    mma(wa, cur);
+    if (kc + 1 < nch) st.store((kc & 1) ? xs0 : xs1);
   }
 }
 
@@ -241,7 +300,7 @@ __global__ void __launch_bounds__(256) k_gu_gemm(int R, int H, int E, int I, int
 // entry t: slot[(row * (k+1) + slot)][n] = w * (Wd_e[n] . act[entry]);
 // shared (e == E): slot[(r * (k+1) + k)][n] = Wsd[n] . act_sh[r] (K = SI).
 // k_combine_norm then adds the k+1 slots of each row to h in a fixed order.
-__global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H, int I, int SI,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_down_gemm(int R, int E, int topk, int H, int I, int SI,
                                                    const uint16_t* __restrict__ act,
                                                    const uint16_t* __restrict__ act_sh,
                                                    const uint4* __restrict__ edn, size_t e_stride,
@@ -270,9 +329,9 @@ __global__ void __launch_bounds__(256) k_down_gemm(int R, int E, int topk, int H
   RowStage<4> st;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int t = t0 + stage_row(u);
+    const int t = min(t0 + stage_row(u), n - 1);  // past the entries: a valid row, discarded
     const uint16_t* rowp = dense ? act_sh + (size_t)t * SI : act + (size_t)(o + t) * I;
-    st.src[u] = t < n ? rowp + stage_col(u) : nullptr;
+    st.src[u] = rowp + stage_col(u);
   }
   f32x4_t acc[1][2][4];
   gemm_core<1, true>(Wt, K, n <= kGemmM, st, xs[0], xs[1], acc);
@@ -405,7 +464,7 @@ __device__ __forceinline__ void to4(const f32x4_t a, float (&x)[4]) {
 // 128); items = the row chunks x N-blocks x S splits, chunk fastest, then
 // split.
 template <int MODE, int MT = 4>
-__global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_dense_gemm(int R, int N, int K,
                                                     const uint16_t* __restrict__ X, int ldx,
                                                     const uint4* __restrict__ Wp, int S,
                                                     float* __restrict__ part, DenseOut o) {
@@ -450,8 +509,8 @@ __global__ void __launch_bounds__(256) k_dense_gemm(int R, int N, int K,
   RowStage<MT> st;
 #pragma unroll
   for (int u = 0; u < MT; ++u) {
-    const int t = t0 + stage_row(u);
-    st.src[u] = t < R ? X + (size_t)t * ldx + kc0 * kGemmKC + stage_col(u) : nullptr;
+    const int t = min(t0 + stage_row(u), R - 1);  // past the rows: a valid row, discarded
+    st.src[u] = X + (size_t)t * ldx + kc0 * kGemmKC + stage_col(u);
   }
   f32x4_t acc[NA][2][MT];
   gemm_core<NA, NA == 1, MT>(Wt, nkc * kGemmKC, nz == 1, st, xs[0], xs[1], acc);
