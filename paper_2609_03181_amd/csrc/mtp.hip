@@ -112,7 +112,8 @@ constexpr int kMoeSpinMax = 1 << 20;  // polls of a fused-MoE wait before it giv
 constexpr int kSlotRows = 64;   // passes of 17..64 rows: slot-form MoE down and split-K QKV
 constexpr int kFlashRows = 64;  // prefill passes of at least this many rows per sequence use
                                 // the flash-style attention
-constexpr int kFlashChunk = 2;  // key tiles per chunk of the split prefill attention
+constexpr int kFlashChunk = 2;      // key tiles per chunk of the split prefill attention
+constexpr int kFlashChunkWide = 8;  // the same with at least as many (row tile, head) blocks as CUs
 
 // Blocks of the fused small-batch MoE that the device holds at once (its
 // waits need every block resident), or 0 when the shape is outside what it
@@ -524,20 +525,23 @@ struct Model {
   template <int DH>
   void sattn(const Ws& ws, int B, int C, uint16_t* cache, size_t seq_stride) {
     if (DH == 128 && prefill && C >= kFlashRows) {  // prefill passes: flash-style, both products on MFMA
-      // With fewer (row tile, head) blocks than compute units, the keys in
-      // chunks of kFlashChunk tiles, run in parallel and merged by a second
-      // launch (measured: 768 rows faster, 1,668 rows -- 270 blocks --
-      // slower than one block walking all of its tiles)
+      // The keys in chunks, run in parallel and merged by a second launch,
+      // so no block walks more than a chunk's tiles (the causal rows of the
+      // last row tiles would otherwise set the launch's length): chunks of
+      // kFlashChunk tiles with fewer (row tile, head) blocks than compute
+      // units, of kFlashChunkWide tiles with more (measured at 1,668 rows:
+      // 5.78 ms unsplit, 5.59 ms in chunks of 8; 200 blocks of the
+      // objective's draft passes: chunks of 2 ahead of 8 by 2 %)
       const int nt = cdiv(C, 64);
       const int kt = cdiv(pos_end > 0 && pos_end < c.max_ctx ? pos_end : c.max_ctx, 64);
-      const int nch = cdiv(kt, kFlashChunk);
-      if (nch > 1 && nch <= n_split && nt * c.n_heads * B < n_cu) {
+      const int fch = nt * c.n_heads * B < n_cu ? kFlashChunk : kFlashChunkWide;
+      const int nch = cdiv(kt, fch);
+      if (nch > 1 && nch <= n_split) {
         launch_k(tm, MTP_KC_ATTN, k_flash_prefill<128, true>, dim3(nt * nch, c.n_heads, B),
                  dim3(256), 0, s, C, c.n_heads, ws.q, cache, seq_stride, c.max_ctx, ws.row_pos,
-                 ws.row_valid, 1.0f / sqrtf(128.f), (uint16_t*)ws.attn, nt, kFlashChunk, nch,
-                 ws.part);
+                 ws.row_valid, 1.0f / sqrtf(128.f), (uint16_t*)ws.attn, nt, fch, nch, ws.part);
         launch_k(tm, MTP_KC_ATTN, k_attn_merge<128>, dim3(cdiv((size_t)B * C * c.n_heads, 4)),
-                 dim3(256), 0, s, B * C, c.n_heads, kFlashChunk, nch, (const float*)ws.part,
+                 dim3(256), 0, s, B * C, c.n_heads, fch, nch, (const float*)ws.part,
                  ws.row_pos, ws.row_valid, (uint16_t*)ws.attn);
         return;
       }
