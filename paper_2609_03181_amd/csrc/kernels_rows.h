@@ -4,6 +4,14 @@
 
 namespace mtp {
 
+// Zeroes words [0, n) of a 16-byte-aligned region with the whole grid
+// (16-byte stores, then the tail).
+__device__ __forceinline__ void zero_words(int32_t* __restrict__ z, int n) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
+  for (int q = t; q < n / 4; q += nt) ((int4*)z)[q] = make_int4(0, 0, 0, 0);
+  for (int q = (n / 4) * 4 + t; q < n; q += nt) z[q] = 0;
+}
+
 // Row r = b*C + i of a pass over B sequences with C rows each sits at
 // position pos0[b] + off + i (pos0 NULL: off + i).  It is valid when
 // i < nvalid[b] (nvalid NULL: all) and its position is inside the cache.
@@ -16,7 +24,7 @@ __global__ void k_rows_setup(int B, int C, const int32_t* __restrict__ pos0, int
   int r = blockIdx.x * blockDim.x + threadIdx.x;
   // counters that later kernels of the call expect at zero (the workspace
   // is carved differently by calls with other row counts)
-  for (int z = r; z < n_zero; z += gridDim.x * blockDim.x) zero[z] = 0;
+  zero_words(zero, n_zero);
   if (r >= B * C) return;
   int b = r / C, i = r - b * C;
   int p = (pos0 ? pos0[b] : 0) + off + i;
@@ -58,7 +66,7 @@ __global__ void k_draft_rows(int B, int C, const int32_t* __restrict__ row_pos_i
                              int32_t* __restrict__ draft_len, int32_t* __restrict__ status,
                              int32_t* __restrict__ zero, int n_zero) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  for (int z = r; z < n_zero; z += gridDim.x * blockDim.x) zero[z] = 0;
+  zero_words(zero, n_zero);
   if (r >= B * C) return;
   const int b = r / C, i = r - b * C;
   const int p0 = row_pos_in[b], p = p0 + i;
@@ -180,7 +188,7 @@ __global__ void __launch_bounds__(64) k_draft_rows_in(
     int32_t* __restrict__ draft_len, int32_t* __restrict__ status, int32_t* __restrict__ zero,
     int n_zero, uint16_t* __restrict__ x) {
   const int r = blockIdx.x, lane = threadIdx.x;
-  for (int zi = r * 64 + lane; zi < n_zero; zi += gridDim.x * 64) zero[zi] = 0;
+  zero_words(zero, n_zero);
   if (r >= B * C) return;
   const int b = r / C, i = r - b * C;
   const int p0 = row_pos_in[b], p = p0 + i, nr = n_rows[b];
@@ -304,9 +312,9 @@ __global__ void k_verify_rows(int B, int K, const int32_t* __restrict__ kv_len,
                               float* __restrict__ h, int32_t* __restrict__ status,
                               int32_t* __restrict__ zero, int n_zero) {
   using S = St<BF>;
-  for (int z = blockIdx.x * blockDim.x + threadIdx.x; z < n_zero; z += gridDim.x * blockDim.x)
-    zero[z] = 0;
+  zero_words(zero, n_zero);
   const int C = K + 1, r = blockIdx.x;
+  if (r >= B * C) return;  // blocks past the rows only clear counters
   const int b = r / C, i = r - b * C;
   const int p = kv_len[b] + i;
   const int valid = p >= 0 && p < cap;

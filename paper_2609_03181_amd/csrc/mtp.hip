@@ -163,6 +163,14 @@ struct Ws {
 // few tiles (64-row chunks x 128-wide N-blocks) the K range is split so that
 // about 384 blocks run, with at least two K chunks per split; 1 with 256
 // tiles or more.
+// Blocks of k_verify_rows: one per row, at least enough that the counters
+// it clears take 16 words per thread (the fused MoE's sync words are
+// ~64K words at up to 16 rows)
+inline int verify_rows_grid(int R, int n_ctr) {
+  const int zb = (n_ctr + 256 * 16 - 1) / (256 * 16);
+  return R > zb ? R : zb;
+}
+
 inline int dense_splits(int R, int N, int K) {
   const int tiles = ((R + kGemmM - 1) / kGemmM) * (N / kGemmN), nch = K / kGemmKC;
   if (tiles >= 256 || nch < 4) return 1;
@@ -1099,6 +1107,9 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
     Ws w = carve(c, batch, C, ws, ctx->n_split);
     const float eps = (float)c.rms_eps;
     const int n4 = H / 256;  // float4 per lane of a row (bf16 model)
+    // the draft block's counters (attention, down strips): the fused MoE's
+    // words after them belong to verify passes, whose first kernel clears them
+    const int n_zero = (int)(w.moe_sync ? w.moe_sync - w.att_ctr : w.n_ctr);
     // depth 1 over the catch-up rows; the last valid row starts the chain
     if constexpr (BF) {
 #define MTP_DRI(NV)                                                                          \
@@ -1106,13 +1117,13 @@ mtp_status mtp_draft_k(mtp_ctx* ctx, int32_t batch, int32_t k, const float* hid,
                                        (const uint16_t*)ctx->w.embed, hid, (size_t)C * H,     \
                                        ctx->w.d_enorm, ctx->w.d_hnorm, eps, w.row_pos,        \
                                        w.row_valid, w.head_row, w.row_tok, draft_len, w.status, \
-                                       w.att_ctr, w.n_ctr, (uint16_t*)w.xin)
+                                       w.att_ctr, n_zero, (uint16_t*)w.xin)
       MTP_NV_DISPATCH(n4, MTP_DRI);
 #undef MTP_DRI
     } else {
       k_draft_rows<<<cdiv(R, 256), 256, 0, s>>>(batch, C, row_pos, n_rows, next_tok, c.max_ctx,
                                                  w.row_pos, w.row_valid, w.head_row, w.row_tok,
-                                                 draft_len, w.status, w.att_ctr, w.n_ctr);
+                                                 draft_len, w.status, w.att_ctr, n_zero);
     }
     // depth d's output state u (ws.ustate, [B][H]) into draft_u[b][d-1]
     auto keep_u = [&](int d) {
@@ -1173,9 +1184,9 @@ mtp_status moe_verify_step(mtp_ctx* ctx, int32_t batch, int32_t k, const int32_t
     Model<BF> m{c, ctx->w, ctx->rope, s, ctx->pk, ctx->n_split, ctx->spl, &ctx->tm, ctx->n_cu, ctx->moe_blocks};
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ws, ctx->n_split);
-    k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
-                                        c.hidden, c.vocab, (const T*)ctx->w.embed, w.row_pos,
-                                        w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
+    k_verify_rows<BF><<<verify_rows_grid(R, w.n_ctr), 256, 0, s>>>(
+        batch, k, kv_len, pending, draft_tok, c.max_ctx, c.hidden, c.vocab,
+        (const T*)ctx->w.embed, w.row_pos, w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
     m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
                margin, route_idx, route_gap, /*embedded=*/true, layer_h);
     return launch_status();
@@ -1209,9 +1220,9 @@ mtp_status moe_verify_step_static(mtp_ctx* ctx, int32_t batch, int32_t k,
     const int C = k + 1, R = batch * C;
     Ws w = carve(c, batch, C, ctx->scratch, ctx->n_split);
     w.status = ctx->dstatus;  // device conditions go to the context's status word
-    k_verify_rows<BF><<<R, 256, 0, s>>>(batch, k, kv_len, pending, draft_tok, c.max_ctx,
-                                        c.hidden, c.vocab, (const T*)ctx->w.embed, w.row_pos,
-                                        w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
+    k_verify_rows<BF><<<verify_rows_grid(R, w.n_ctr), 256, 0, s>>>(
+        batch, k, kv_len, pending, draft_tok, c.max_ctx, c.hidden, c.vocab,
+        (const T*)ctx->w.embed, w.row_pos, w.row_valid, w.h, w.status, w.att_ctr, w.n_ctr);
     m.verifier(w, batch, C, nullptr, 0, 0, (T*)kv_cache, hid, true, verify_tok, R, 0, logits,
                margin, route_idx, route_gap, /*embedded=*/true, layer_h);
     return launch_status();
