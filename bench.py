@@ -506,16 +506,16 @@ def _time_prefill(s, pin, n=3):
 def prefill_flops(cfg, P):
     """Algorithmic FLOPs of a one-pass prefill of P rows: every row through
     the verifier's active parameters (no LM head but the last row's) and
-    causal attention over the rows before it, plus the draft-block prefill
-    of P - 1 rows (embedding/state projection, attention, dense FFN)."""
+    causal attention over the rows before it, plus the draft block's cache
+    rows for P - 1 rows (embedding/state projection, K and V projections:
+    nothing else of the draft block is read after a prefill)."""
     H, D, I, S, E, k = (cfg.hidden, cfg.n_heads * cfg.head_dim, cfg.moe_inter, cfg.n_shared,
                         cfg.n_routed, cfg.top_k)
-    L, V, F = cfg.n_layers, cfg.vocab, cfg.draft_inter
+    L, V = cfg.n_layers, cfg.vocab
     per_row = L * (3 * D * H + H * D + E * H + (k + S) * 3 * I * H)
     attn = L * P * (P + 1) // 2 * 2 * D
-    draft_row = 2 * H * H + 3 * D * H + H * D + 3 * F * H
-    draft_attn = (P - 1) * P // 2 * 2 * D
-    return 2 * (P * per_row + V * H + (P - 1) * draft_row) + 2 * (attn + draft_attn)
+    draft_row = 2 * H * H + 2 * D * H
+    return 2 * (P * per_row + V * H + (P - 1) * draft_row) + 2 * attn
 
 
 def objective_flops(cfg, T, K):

@@ -415,12 +415,16 @@ struct Model {
   // ws.xin already (row setup fused with the draft input)
   // defer_argmax (bf16 model): the head's token reduction is left to the
   // next depth's row setup
+  // kv_only (no head): the block's K/V rows are all the caller needs, so
+  // the bf16 block stops once they are appended (attention, O projection
+  // and FFN outputs would go unread), the float32 one after its attention
+  // sub-layer
   void draft(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision, int vis_ld,
              int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff, float* logits,
-             size_t ldl, bool xin_ready = false, bool defer_argmax = false) {
+             size_t ldl, bool xin_ready = false, bool defer_argmax = false, bool kv_only = false) {
     if constexpr (BF) {
       draft_mfma(ws, B, C, a, a_ld, vision, vis_ld, vis_off, dkv, head, tok, ostride, ooff,
-                 logits, ldl, xin_ready, defer_argmax);
+                 logits, ldl, xin_ready, defer_argmax, kv_only && !head);
       return;
     }
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
@@ -433,6 +437,7 @@ struct Model {
     k_linear<BF, false><<<cdiv(H, 4), 256, 0, s>>>(R, H, 2 * H, (const T*)ws.xin, 2 * H,
                                                    (const T*)w.d_eh_proj, ws.h, H);
     attn_sublayer(ws, B, C, w.d_attn_norm, (const T*)w.d_wqkv, (const T*)w.d_wo, dkv, seq_stride);
+    if (kv_only && !head) return;
     k_rmsnorm<BF><<<R, 256, 0, s>>>(H, ws.h, H, nullptr, w.d_ffn_norm, (float)c.rms_eps, nullptr,
                                     0, (T*)ws.xin, H, 0);
     k_linear<BF, false><<<cdiv(2 * F, 4), 256, 0, s>>>(R, 2 * F, H, (const T*)ws.xin, H,
@@ -566,9 +571,11 @@ struct Model {
   }
 
   // attention sub-layer: h += Wo attn(RMSNorm(h; g)).  With xg the
-  // normalised rows are already in xg (bf16) and g is unused.
+  // normalised rows are already in xg (bf16) and g is unused.  kv_only:
+  // only the K/V rows appended to the cache are wanted (stops after QKV).
   void attn_mfma(const Ws& ws, int B, int C, const float* g, const uint16_t* xg,
-                 const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride) {
+                 const uint4* wqkv, const uint4* wo, uint16_t* cache, size_t seq_stride,
+                 bool kv_only = false) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim, D = nh * dh;
     if (xg && R > kSlotRows) {  // tiled GEMM over the normalised rows
       DenseOut o{};
@@ -592,6 +599,7 @@ struct Model {
       MTP_MAXT_DISPATCH(H / 128, MTP_QKV);
 #undef MTP_QKV
     }
+    if (kv_only) return;
     if (dh == 128) sattn<128>(ws, B, C, cache, seq_stride);
     else sattn<64>(ws, B, C, cache, seq_stride);
     smm(ws, R, H, D, (const uint16_t*)ws.attn, D, wo, ws.h, H, true);
@@ -775,7 +783,7 @@ struct Model {
 
   void draft_mfma(const Ws& ws, int B, int C, const float* a, size_t a_ld, const T* vision,
                   int vis_ld, int vis_off, T* dkv, bool head, int32_t* tok, int ostride, int ooff,
-                  float* logits, size_t ldl, bool xin_ready, bool defer_argmax) {
+                  float* logits, size_t ldl, bool xin_ready, bool defer_argmax, bool kv_only) {
     const int R = B * C, H = c.hidden, nh = c.n_heads, dh = c.head_dim;
     const int F = c.draft_inter;
     const float eps = (float)c.rms_eps;
@@ -792,7 +800,9 @@ struct Model {
     const bool pre = G > 1;
     const uint16_t* xn = pre ? (const uint16_t*)ws.xin : nullptr;
     if (pre) norm_rows(R, ws.h, nullptr, w.d_attn_norm, nullptr, (uint16_t*)ws.xin);
-    attn_mfma(ws, B, C, w.d_attn_norm, xn, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride);
+    attn_mfma(ws, B, C, w.d_attn_norm, xn, pk.d_qkv, pk.d_wo, (uint16_t*)dkv, seq_stride,
+              kv_only);
+    if (kv_only) return;
     if (pre) norm_rows(R, ws.h, nullptr, w.d_ffn_norm, nullptr, (uint16_t*)ws.xin);
     if (pre) {  // tiled GEMM over the normalised rows
       DenseOut o{};
@@ -1074,7 +1084,7 @@ mtp_status mtp_prefill(mtp_ctx* ctx, int32_t batch, int32_t k, int32_t n_rows, c
                                                    w.row_pos, w.row_valid, nullptr, w.status);
         k_row_tokens<<<cdiv(R, 256), 256, 0, s>>>(batch, Cc, tok, n_rows, c0 + 1, w.row_tok);
         m.draft(w, batch, Cc, w.bbuf, (size_t)Cc * c.hidden, (const T*)vision, n_rows, c0 + 1,
-                (T*)draft_kv, false, nullptr, 0, 0, nullptr, 0);
+                (T*)draft_kv, false, nullptr, 0, 0, nullptr, 0, false, false, /*kv_only=*/true);
       }
     }
     k_prefill_state<<<cdiv(batch, 256), 256, 0, s>>>(batch, k, n_rows, w.tok_stage, kv_len,
