@@ -38,6 +38,37 @@ __device__ __forceinline__ double block_sum_d(double v, double* red /* 256 */) {
   return t;
 }
 
+// Running float32 maxima and float64 sums of one pass over a row of logits:
+// sp = sum exp(p - mp), sq = sum exp(q - mq), sqd = sum exp(q - mq) (q - p),
+// rescaled (factor exp(m_old - m_new) in float64) when a maximum grows.
+struct ObjStats {
+  float mp = -INFINITY, mq = -INFINITY;
+  double sp = 0.0, sq = 0.0, sqd = 0.0;
+  __device__ __forceinline__ void rescale(float np_, float nq_) {
+    if (np_ > mp) {
+      sp = mp == -INFINITY ? 0.0 : sp * exp((double)mp - (double)np_);
+      mp = np_;
+    }
+    if (nq_ > mq) {
+      const double f = mq == -INFINITY ? 0.0 : exp((double)mq - (double)nq_);
+      sq *= f;
+      sqd *= f;
+      mq = nq_;
+    }
+  }
+  // n logits of P and Q (the caller raised the maxima over them first)
+  template <int N>
+  __device__ __forceinline__ void add(const float (&pv)[N], const float (&qv)[N]) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const double eq = (double)expf(qv[j] - mq);
+      sp += (double)expf(pv[j] - mp);
+      sq += eq;
+      sqd += eq * ((double)qv[j] - (double)pv[j]);
+    }
+  }
+};
+
 // Loss terms of draft row p = c0 + i (one block per row): with P = softmax
 // of the draft logits lp[i], Q = softmax of the verifier logits lq[i] (of
 // b_{p+1}) and the target x_{p+2}:
@@ -46,6 +77,10 @@ __device__ __forceinline__ double block_sum_d(double v, double* red /* 256 */) {
 //   MSE = ||u_p - b_{p+1}||^2
 // for loss rows (n_prompt <= p <= n_rows - 3), zeros otherwise.  Maxima in
 // float32, exponentials in float32, every sum in float64.  terms: [rows][3].
+// One pass over the two rows (16-byte loads, four of each row in flight per
+// thread; with V not a multiple of 4, 4-byte loads): each thread keeps
+// running maxima and sums rescaled to them, then the block combines the
+// threads' sums at the row maxima.
 __global__ void __launch_bounds__(256) k_obj_terms(int c0, int n_rows, int n_prompt, int V, int H,
                                                    const float* __restrict__ lp,
                                                    const float* __restrict__ lq,
@@ -56,7 +91,7 @@ __global__ void __launch_bounds__(256) k_obj_terms(int c0, int n_rows, int n_pro
                                                    int32_t* __restrict__ status) {
   __shared__ float redf[16];
   __shared__ double redd[256];
-  const int i = blockIdx.x, p = c0 + i;
+  const int i = blockIdx.x, p = c0 + i, t0 = threadIdx.x, nt = blockDim.x;
   float* out = terms + (size_t)p * 3;
   if (p < n_prompt || p > n_rows - 3) {
     if (threadIdx.x < 3) out[threadIdx.x] = 0.f;
@@ -64,21 +99,46 @@ __global__ void __launch_bounds__(256) k_obj_terms(int c0, int n_rows, int n_pro
   }
   const float* P = lp + (size_t)i * V;
   const float* Q = lq + (size_t)i * V;
-  float mp = -INFINITY, mq = -INFINITY;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) {
-    mp = fmaxf(mp, P[v]);
-    mq = fmaxf(mq, Q[v]);
+  ObjStats st;
+  if (V % 4 == 0) {
+    constexpr int U = 4;
+    const float4* P4 = (const float4*)P;
+    const float4* Q4 = (const float4*)Q;
+    const int n4 = V / 4;
+    for (int v0 = t0; v0 < n4; v0 += U * nt) {
+      float pv[4 * U], qv[4 * U];
+#pragma unroll
+      for (int u_ = 0; u_ < U; ++u_) {
+        // past the row: a large negative finite value in both rows (its
+        // exponentials are 0 and its q - p is 0; the batch's first piece is
+        // always in the row, so it never sets a maximum)
+        const bool in = v0 + u_ * nt < n4;
+        const float4 a = in ? P4[v0 + u_ * nt] : make_float4(-3e38f, -3e38f, -3e38f, -3e38f);
+        const float4 c = in ? Q4[v0 + u_ * nt] : make_float4(-3e38f, -3e38f, -3e38f, -3e38f);
+        pv[4 * u_] = a.x; pv[4 * u_ + 1] = a.y; pv[4 * u_ + 2] = a.z; pv[4 * u_ + 3] = a.w;
+        qv[4 * u_] = c.x; qv[4 * u_ + 1] = c.y; qv[4 * u_ + 2] = c.z; qv[4 * u_ + 3] = c.w;
+      }
+      float bp = -INFINITY, bq = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4 * U; ++j) {
+        bp = fmaxf(bp, pv[j]);
+        bq = fmaxf(bq, qv[j]);
+      }
+      st.rescale(bp, bq);
+      st.add(pv, qv);
+    }
+  } else {
+    for (int v = t0; v < V; v += nt) {
+      float pv[1] = {P[v]}, qv[1] = {Q[v]};
+      st.rescale(pv[0], qv[0]);
+      st.add(pv, qv);
+    }
   }
-  mp = block_max(mp, redf);
-  mq = block_max(mq, redf);
-  double sp = 0.0, sq = 0.0, sqd = 0.0;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) {
-    const float pv = P[v], qv = Q[v];
-    const double eq = (double)expf(qv - mq);
-    sp += (double)expf(pv - mp);
-    sq += eq;
-    sqd += eq * ((double)qv - (double)pv);
-  }
+  // the block's maxima, then each thread's sums at them
+  const float mp = block_max(st.mp, redf), mq = block_max(st.mq, redf);
+  const double fp = st.mp == -INFINITY ? 0.0 : exp((double)st.mp - (double)mp);
+  const double fq = st.mq == -INFINITY ? 0.0 : exp((double)st.mq - (double)mq);
+  double sp = st.sp * fp, sq = st.sq * fq, sqd = st.sqd * fq;
   double ss = 0.0;
   const float* ur = u + (size_t)p * H;
   const float* br = b + (size_t)(p + 1) * H;
