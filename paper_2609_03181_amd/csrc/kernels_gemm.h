@@ -75,13 +75,10 @@ __device__ __forceinline__ bool gemm_item(int b, int E, int nbr, int nbs,
 // row (tid + 256u) / 16, 8 columns at 8 * ((tid + 256u) % 16).
 template <int MT = 4>
 struct RowStage {
-  const uint16_t* src[MT];  // the piece's row at column 0 (NULL: a row past the entries)
+  // the piece's row at column 0; a piece past the entries points at a valid
+  // row (its products are discarded), so loads carry no per-lane branch
+  const uint16_t* src[MT];
   uint4 v[MT];
-  __device__ __forceinline__ void load(int k0) {
-#pragma unroll
-    for (int u = 0; u < MT; ++u) v[u] = src[u] ? *(const uint4*)(src[u] + k0) : make_uint4(0, 0, 0, 0);
-  }
-  // every src set (no row past the entries)
   __device__ __forceinline__ void load_set(int k0) {
 #pragma unroll
     for (int u = 0; u < MT; ++u) v[u] = *(const uint4*)(src[u] + k0);
@@ -170,36 +167,30 @@ __device__ __forceinline__ void gemm_pipe(const uint4* const (&Wt)[NA][2], int n
   }
 }
 
-// acc[a][j][mt] = sum over K of matrix a's strip j (tile stream Wt[a][j],
-// lane offset included) times row tile mt (of MT) of the staged rows.  K is a
-// multiple of kGemmKC; st.src is set; xs0 / xs1 are the two LDS stages.
-// PF: gemm_pipe (chunk kc + 1's loads in flight during chunk kc's products;
-// every st.src must point at a row); else each chunk's tiles are loaded at
-// its start (one register set: with two matrices, two waves per SIMD fit
-// instead of one, and the other wave covers the load latency).
-template <int NA, bool PF, int MT = 4>
-__device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K, bool once,
+// The one-register-set form of gemm_core: as soon as a k-step's MFMAs have
+// taken its weight tiles, the same registers are reloaded with that k-step
+// of the next chunk, so those loads fly during the rest of this chunk's
+// products; the next chunk's rows are requested before them.  Every st.src
+// is a row (as gemm_pipe); NT: non-temporal weight loads.
+template <int NA, int MT, bool NT>
+__device__ __forceinline__ void gemm_roll(const uint4* const (&Wt)[NA][2], int nch,
                                           RowStage<MT>& st, uint16_t* xs0, uint16_t* xs1,
                                           f32x4_t (&acc)[NA][2][MT]) {
   const int lane = threadIdx.x & 63, i16 = lane & 15, g = lane >> 4;
-  const int nch = K / kGemmKC;
+  uint4 wt[NA][4][2];
 #pragma unroll
-  for (int a = 0; a < NA; ++a)
+  for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int a = 0; a < NA; ++a)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  uint4 wa[NA][4][2];
-  auto load_w = [&](uint4 (&wt)[NA][4][2], int kc) {
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) wt[a][ks][j] = ld_tile(Wt[a][j] + (size_t)(kc * 4 + ks) * 64, once);
-  };
-  auto mma = [&](const uint4 (&wt)[NA][4][2], const uint16_t* xs) {
-    const uint16_t* xb = xs + i16 * kGemmLd + 8 * g;
+      for (int j = 0; j < 2; ++j) wt[a][ks][j] = ld_tile_t<NT>(Wt[a][j] + (size_t)ks * 64);
+  st.load_set(0);
+  st.store(xs0);
+  for (int kc = 0; kc < nch; ++kc) {
+    const uint16_t* xb = ((kc & 1) ? xs1 : xs0) + i16 * kGemmLd + 8 * g;
+    const bool more = kc + 1 < nch;
+    if (more) st.load_set((kc + 1) * kGemmKC);
+    __syncthreads();  // chunk kc is staged; every wave is done reading the other stage
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       uint4 bx[MT];
@@ -211,23 +202,43 @@ __device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K
         for (int j = 0; j < 2; ++j)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = mfma16(wt[a][ks][j], bx[mt], acc[a][j][mt]);
+      if (more) {
+#pragma unroll
+        for (int a = 0; a < NA; ++a)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            wt[a][ks][j] = ld_tile_t<NT>(Wt[a][j] + (size_t)((kc + 1) * 4 + ks) * 64);
+      }
     }
-  };
+    if (more) st.store((kc & 1) ? xs0 : xs1);
+  }
+}
+
+// acc[a][j][mt] = sum over K of matrix a's strip j (tile stream Wt[a][j],
+// lane offset included) times row tile mt (of MT) of the staged rows.  K is a
+// multiple of kGemmKC; st.src is set; xs0 / xs1 are the two LDS stages.
+// Every st.src must point at a row.  PF: gemm_pipe (chunk kc + 1's loads in
+// flight during chunk kc's products, two register sets); else gemm_roll
+// (one set, each k-step's tiles reloaded with the next chunk's as soon as
+// its MFMAs have taken them: with two matrices, two sets would leave one
+// wave per SIMD).
+template <int NA, bool PF, int MT = 4>
+__device__ __forceinline__ void gemm_core(const uint4* const (&Wt)[NA][2], int K, bool once,
+                                          RowStage<MT>& st, uint16_t* xs0, uint16_t* xs1,
+                                          f32x4_t (&acc)[NA][2][MT]) {
+  const int nch = K / kGemmKC;
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[a][j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if constexpr (PF) {
     if (once) gemm_pipe<NA, MT, true>(Wt, nch, st, xs0, xs1, acc);
     else gemm_pipe<NA, MT, false>(Wt, nch, st, xs0, xs1, acc);
-    return;
-  }
-  st.load(0);
-  load_w(wa, 0);
-  st.store(xs0);
-  for (int kc = 0; kc < nch; ++kc) {
-    uint16_t* cur = (kc & 1) ? xs1 : xs0;
-    if (kc > 0) load_w(wa, kc);
-    if (kc + 1 < nch) st.load((kc + 1) * kGemmKC);
-    __syncthreads();  // cur holds chunk kc; every wave is done reading the other stage
-    mma(wa, cur);
-    if (kc + 1 < nch) st.store((kc & 1) ? xs0 : xs1);
+  } else {
+    if (once) gemm_roll<NA, MT, true>(Wt, nch, st, xs0, xs1, acc);
+    else gemm_roll<NA, MT, false>(Wt, nch, st, xs0, xs1, acc);
   }
 }
 
@@ -274,9 +285,8 @@ __global__ void __launch_bounds__(256) k_gu_gemm(int R, int H, int E, int I, int
   RowStage<4> st;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int t = t0 + stage_row(u);
-    const int row = t < n ? (dense ? t : ent_row[o + t]) : -1;
-    st.src[u] = row >= 0 ? xg + (size_t)row * H + stage_col(u) : nullptr;
+    const int t = min(t0 + stage_row(u), n - 1);  // past the entries: a valid row, discarded
+    st.src[u] = xg + (size_t)(dense ? t : ent_row[o + t]) * H + stage_col(u);
   }
   f32x4_t acc[2][2][4];
   gemm_core<2, false>(Wt, H, n <= kGemmM, st, xs[0], xs[1], acc);
