@@ -7,13 +7,15 @@
 // Block = 4 waves = 128 output features (wave w: two 16-wide strips) x 64
 // rows (four MFMA row tiles; the core and the dense kernel take the number
 // of row tiles MT as a parameter, 4 in every launch: eight row tiles per
-// wave leave one wave per SIMD, which measured slower for the LM head).  The rows are staged through LDS in K chunks
-// of 128 columns, double-buffered; each wave loads its own weight tiles
-// (the packed operand tiles of kernels_mfma.h) straight from memory, one K
-// chunk ahead of its products, so a chunk's weight loads fly during the
-// previous chunk's MFMAs.  Per k-step a wave issues 2 weight-tile loads per
-// matrix and 4 LDS row reads for 8 MFMAs per matrix.  K is summed in one
-// chain per output tile, in order.
+// wave leave one wave per SIMD, which measured slower for the LM head).
+// The rows are staged through LDS in K chunks of 128 columns,
+// double-buffered; each wave loads its own weight tiles (the packed operand
+// tiles of kernels_mfma.h) straight from memory into registers, so that
+// they fly during the previous chunk's MFMAs: one matrix, two register sets
+// (a chunk ahead); two matrices, one set whose k-steps are reloaded with
+// the next chunk's as the MFMAs take them.  Per k-step a wave issues 2
+// weight-tile loads per matrix and 4 LDS row reads for 8 MFMAs per matrix.
+// K is summed in one chain per output tile, in order.
 //
 // Work items: (weight slab = 128 features of one matrix, 64-row chunk),
 // ordered with the chunks of a slab consecutive; blocks are dispatched to
