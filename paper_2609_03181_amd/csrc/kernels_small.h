@@ -1505,12 +1505,20 @@ __global__ void __launch_bounds__(1024) k_group(int R, int E, int topk,
 // XL (one row group of more than a few rows): the block's rows are staged
 // in LDS once ([16][H + XPAD], dynamic) instead of every wave reading them
 // from L2 beside its weight tiles.
-template <int RG, bool XL = false>
+// NV > 0 (with XL; NV float4 per lane of a row): the rows are the RMSNorm
+// (gain gn) of the float32 rows hx[hidx[o]] (hidx NULL: hx[o]), computed by
+// each block while its first weight tiles load -- wave w takes rows w,
+// w + 4, ... with k_norm_rows's arithmetic, so the values are its values --
+// and block 0 also writes them as float32 to yf[o] (optional); X is unused.
+template <int RG, bool XL = false, int NV = 0>
 __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16_t* __restrict__ X,
                                               const uint4* __restrict__ Wp,
                                               float* __restrict__ logits, size_t ldl,
                                               float* __restrict__ pv, int32_t* __restrict__ pi,
-                                              float* __restrict__ p2) {
+                                              float* __restrict__ p2, const float* __restrict__ hx,
+                                              const int32_t* __restrict__ hidx,
+                                              const float* __restrict__ gn, float eps,
+                                              float* __restrict__ yf) {
   constexpr int BT = 4;  // A tiles per batch (each used by RG MFMAs)
   extern __shared__ __align__(16) uint16_t xs[];
   __shared__ float bv[4][16 * RG], sv[4][16 * RG];
@@ -1532,23 +1540,55 @@ __global__ void __launch_bounds__(256) k_s_lm(int nr, int V, int H, const uint16
     static_assert(RG == 1, "rows staged for one row group");
     constexpr int XC = 16 * 2048 / 8 / 256;  // 16-byte row chunks per thread (H <= 2048)
     const int ldx_l = H + XPAD, nrow = min(16, nr - r0), nx = nrow * H / 8;
-    // row loads first, then the first tile batch: writing the rows to LDS
-    // waits on the row loads only
-    uint4 xv[XC];
-#pragma unroll
-    for (int q = 0; q < XC; ++q) {
-      const int c = threadIdx.x + 256 * q;
-      xv[q] = c < nx ? ((const uint4*)(X + (size_t)r0 * H))[c] : make_uint4(0, 0, 0, 0);
-    }
     const uint4* A = Wp + (size_t)nt * nkt * 64;
     uint4 a[8];
+    if constexpr (NV > 0) {
+      // the first tile batch in flight, then the rows' RMSNorm into LDS
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      a[u] = (live && u < nkt) ? ld_tile(A + (size_t)u * 64 + lane, true) : make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < 8; ++u)
+        a[u] = (live && u < nkt) ? ld_tile(A + (size_t)u * 64 + lane, true) : make_uint4(0, 0, 0, 0);
+      const int n4 = H / 256;
+      for (int q = wv; q < nrow; q += 4) {
+        NormRow<NV> nw;
+        norm_row_load<NV>(H, hx + (size_t)(hidx ? hidx[r0 + q] : r0 + q) * H, gn, nw);
+        float ss = 0.f;
 #pragma unroll
-    for (int q = 0; q < XC; ++q) {
-      const int c = threadIdx.x + 256 * q;
-      if (c < nx) *(uint4*)(xs + (c / (H / 8)) * ldx_l + (c % (H / 8)) * 8) = xv[q];
+        for (int u = 0; u < NV; ++u)
+          ss += nw.x[u].x * nw.x[u].x + nw.x[u].y * nw.x[u].y + nw.x[u].z * nw.x[u].z +
+                nw.x[u].w * nw.x[u].w;
+        ss = wave_sum(ss);
+        const float rinv = rsqrtf(ss / (float)H + eps);
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+          if (u < n4) {
+            const float4 y = make_float4(nw.x[u].x * rinv * nw.g[u].x, nw.x[u].y * rinv * nw.g[u].y,
+                                         nw.x[u].z * rinv * nw.g[u].z, nw.x[u].w * rinv * nw.g[u].w);
+            const int j4 = u * 64 + lane;
+            if (yf && blockIdx.x == 0) ((float4*)(yf + (size_t)(r0 + q) * H))[j4] = y;
+            uint2 pk;
+            pk.x = (uint32_t)f2bf(y.x) | ((uint32_t)f2bf(y.y) << 16);
+            pk.y = (uint32_t)f2bf(y.z) | ((uint32_t)f2bf(y.w) << 16);
+            *(uint2*)(xs + q * ldx_l + 4 * j4) = pk;
+          }
+        }
+      }
+    } else {
+      // row loads first, then the first tile batch: writing the rows to LDS
+      // waits on the row loads only
+      uint4 xv[XC];
+#pragma unroll
+      for (int q = 0; q < XC; ++q) {
+        const int c = threadIdx.x + 256 * q;
+        xv[q] = c < nx ? ((const uint4*)(X + (size_t)r0 * H))[c] : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        a[u] = (live && u < nkt) ? ld_tile(A + (size_t)u * 64 + lane, true) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int q = 0; q < XC; ++q) {
+        const int c = threadIdx.x + 256 * q;
+        if (c < nx) *(uint4*)(xs + (c / (H / 8)) * ldx_l + (c % (H / 8)) * 8) = xv[q];
+      }
     }
     __syncthreads();
     if (live) acc[0] = sk_range_lx<8>(A, 0, nkt, xs + (r < nrow ? r : 0) * ldx_l, acc[0], true, a);
