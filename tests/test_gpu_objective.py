@@ -21,6 +21,8 @@ Bounds, with |d l| <= t (1 + |l|) for logits at tolerance t and
                                           + t_Q (1 + max|l_Q|) sum_v q_v |l_Qv - l_Pv - KL|
   MSE = ||u - b||^2:               |dMSE| <= sum_i 2 |u_i - b_i| e_i + e_i^2,
                                    e_i = t_u (1 + |u_i|)."""
+import dataclasses
+
 import numpy as np
 import pytest
 import scipy.special
@@ -78,8 +80,10 @@ def _bounds(ref, k, rows, t_p, t_q, t_u, b):
     return np.stack([ce_b, kl_b, mse_b], axis=1) + 1e-6
 
 
-def _check(name, n_vis, n_txt, n_prompt, K, **wkw):
+def _check(name, n_vis, n_txt, n_prompt, K, vocab=None, **wkw):
     cfg = synth.CONFIGS[name]
+    if vocab is not None:
+        cfg = dataclasses.replace(cfg, vocab=vocab)
     w = synth.make_weights(cfg, 0, 1, **wkw)
     orc = oracle.Oracle(cfg, w)
     tok, emb = _sequence(cfg, n_vis, n_txt)
@@ -117,6 +121,13 @@ def _check(name, n_vis, n_txt, n_prompt, K, **wkw):
 
 def test_objective_mid_bf16():
     _check("mid", 8, 40, 16, 3, gain_jitter=0.1)
+
+
+def test_objective_odd_vocabulary():
+    """A vocabulary that is not a multiple of 4 (the loss terms read the
+    logit rows with 4-byte loads) nor of 16 (the LM head's last strip is
+    ragged)."""
+    _check("tinyb", 4, 22, 8, 2, vocab=3001)
 
 
 def test_objective_tiny_f32_untied():
