@@ -139,10 +139,10 @@ def test_objective_one_depth_and_a_short_sequence():
 
 
 def test_objective_mid_several_chunks():
-    """299 draft rows: a 256-row pass and a 43-row pass per depth, so the
-    states of a chunk's first row and the attended rows of the earlier
+    """1,323 draft rows: a 1,280-row pass and a 43-row pass per depth, so
+    the states of a chunk's first row and the attended rows of the earlier
     chunk cross the chunk boundary."""
-    _check("mid", 16, 284, 40, 3, gain_jitter=0.1)
+    _check("mid", 16, 1308, 40, 3, gain_jitter=0.1)
 
 
 def test_objective_full_shape():
