@@ -159,10 +159,6 @@ struct Ws {
   size_t bytes;
 };
 
-// K splits of a dense tiled product of R rows, N outputs and K inputs: with
-// few tiles (64-row chunks x 128-wide N-blocks) the K range is split so that
-// about 384 blocks run, with at least two K chunks per split; 1 with 256
-// tiles or more.
 // Blocks of k_verify_rows: one per row, at least enough that the counters
 // it clears take 16 words per thread (the fused MoE's sync words are
 // ~64K words at up to 16 rows)
@@ -171,10 +167,15 @@ inline int verify_rows_grid(int R, int n_ctr) {
   return R > zb ? R : zb;
 }
 
+// K splits of a dense tiled product of R rows, N outputs and K inputs: with
+// few tiles (64-row chunks x 128-wide N-blocks) the K range is split so that
+// about 256 blocks run, with at least two K chunks per split; 1 with 256
+// tiles or more.  (Aiming at 384 or 768 blocks measured no faster at
+// batch 16 and 64, and more splits write and read more float32 partials.)
 inline int dense_splits(int R, int N, int K) {
   const int tiles = ((R + kGemmM - 1) / kGemmM) * (N / kGemmN), nch = K / kGemmKC;
   if (tiles >= 256 || nch < 4) return 1;
-  const int want = (384 + tiles - 1) / tiles;
+  const int want = (256 + tiles - 1) / tiles;
   const int cps = std::max(2, (nch + want - 1) / want);
   return (nch + cps - 1) / cps;
 }
