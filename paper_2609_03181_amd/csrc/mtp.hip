@@ -112,7 +112,7 @@ constexpr int kMoeSpinMax = 1 << 20;  // polls of a fused-MoE wait before it giv
 constexpr int kSlotRows = 64;   // passes of 17..64 rows: slot-form MoE down and split-K QKV
 constexpr int kFlashRows = 64;  // prefill passes of at least this many rows per sequence use
                                 // the flash-style attention
-constexpr int kFlashChunk = 2;      // key tiles per chunk of the split prefill attention
+constexpr int kFlashChunk = 4;      // key tiles per chunk of the split prefill attention
 constexpr int kFlashChunkWide = 8;  // the same with at least as many (row tile, head) blocks as CUs
 
 // Blocks of the fused small-batch MoE that the device holds at once (its
@@ -549,8 +549,8 @@ struct Model {
       // last row tiles would otherwise set the launch's length): chunks of
       // kFlashChunk tiles with fewer (row tile, head) blocks than compute
       // units, of kFlashChunkWide tiles with more (measured at 1,668 rows:
-      // 5.78 ms unsplit, 5.59 ms in chunks of 8; 200 blocks of the
-      // objective's draft passes: chunks of 2 ahead of 8 by 2 %)
+      // 5.78 ms unsplit, 5.59 ms in chunks of 8; at 768 rows, 120 blocks:
+      // 3.01 ms in chunks of 4 against 3.12 in chunks of 2)
       const int nt = cdiv(C, 64);
       const int kt = cdiv(pos_end > 0 && pos_end < c.max_ctx ? pos_end : c.max_ctx, 64);
       const int fch = nt * c.n_heads * B < n_cu ? kFlashChunk : kFlashChunkWide;
