@@ -534,6 +534,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     float* bv = (float*)xs[0];
     float* sv = bv + 4 * RM;
     int* bi = (int*)(sv + 4 * RM);
+    // a lane's four logits of a strip are consecutive: one 16-byte store
+    // where the row stride and the base allow it (scattered 4-byte stores
+    // had made the 1,280-row head of the objective store-bound)
+    const bool l16 = ((o.ldl & 3) == 0) && ((reinterpret_cast<uintptr_t>(o.logits) & 15) == 0);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int r = t0 + mt * 16 + i16;
@@ -542,12 +546,23 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 #pragma unroll
       for (int a = 0; a < NA; ++a)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j) {
+        const int v0 = (j ? fb : fa) + 32 * a;
+        if (o.logits && r < R) {
+          float* dst = o.logits + (size_t)r * o.ldl + v0;
+          const f32x4_t y = acc[a][j][mt];
+          if (l16 && v0 + 3 < N) {
+            *(float4*)dst = make_float4(y[0], y[1], y[2], y[3]);
+          } else {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+              if (v0 + t < N) dst[t] = y[t];
+          }
+        }
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          const int v = (j ? fb : fa) + 32 * a + t;  // ascending ids
+          const int v = v0 + t;  // ascending ids
           const float x = v < N ? acc[a][j][mt][t] : -INFINITY;
-          if (o.logits && r < R && v < N) o.logits[(size_t)r * o.ldl + v] = x;
           if (x > b1) {
             b2 = b1;
             b1 = x;
@@ -556,6 +571,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
             b2 = x;
           }
         }
+      }
 #pragma unroll
       for (int sh = 16; sh <= 32; sh <<= 1) {
         const float ob1 = __shfl_xor(b1, sh, MTP_WAVE), ob2 = __shfl_xor(b2, sh, MTP_WAVE);
